@@ -1,0 +1,370 @@
+"""Float64 CPU oracle for the GRPO/PPO trainer-step core.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the CPU-baseline
+leg of the benchmark import this module; the library's product path never
+calls it and shares no code with it.
+
+It is the plain definition of what the trainer step computes, written out in
+numpy float64, row block by row block, with no online log-sum-exp, no fusion
+and no reordering beyond what the definitions state:
+
+* Log-probabilities of the sampled response tokens under the policy (Sec. 3.1.1,
+  the ``Experience`` carries the rollout model's log-probs of the response
+  tokens because PPO and GRPO need them; Sec. 2.1.2, the trainer computes the
+  policy's).  The policy head is ``z = W h`` over the whole vocabulary,
+  ``log p = z - logsumexp(z)``.
+* Entropy of the policy per token (Sec. 3.4.2, the "actor entropy" plotted as
+  an exploration signal): ``H = -sum_j p_j log p_j``.
+* GRPO group-relative advantages (Sec. 3.2, Listing 4, ``advantage_fn:
+  "grpo"`` with ``repeat_times: 8``; Sec. 3.3.1, 8 rollouts per task): every
+  reward is normalised by the mean and standard deviation of its group.
+* The clipped PPO surrogate (Sec. 3.3.2: the clipping range of the probability
+  ratio defaults to 1 +/- 0.2) and a KL term toward the reference model
+  (Sec. 3.3.2, "KL penalty or loss"; Sec. 3.2, Listing 4, ``use_reference``),
+  over the tokens the action mask marks (Sec. 2.2 and Sec. 3.1.2: multi-turn
+  rollouts are concatenated and masked; Listing 4: the loss takes
+  ``logprob, old_logprob, action_mask, advantages``).
+* The gradient of that loss with respect to the log-probs, the logits, the
+  hidden states and the lm_head weight (the trainer's backward through the
+  policy head).
+
+Readings where the paper is silent (it prints no formula):
+  R1 KL estimator: k3 = exp(d) - d - 1 with d = ref - logp, added to the loss
+     with coefficient beta.
+  R2 Aggregation: mode 0 = mean over rollouts of the per-rollout token mean
+     (weight 1/(S n_i)); mode 1 = mean over all valid tokens (weight 1/N).
+     ``denom_override > 0`` replaces S (mode 0) or N (mode 1).
+  R3 Group std: sample std (divisor G-1), eps = 1e-6 added to the std; a group
+     whose rewards are all equal (or G = 1) gets advantage exactly 0.
+  R4 Clip decision: strict inequalities, taken in fp32 on ``logp - old``
+     against ``fp32(log(1 +/- eps))`` so that a GPU fed the same fp32 inputs
+     takes the same decision; values are fp64.
+  R5 Masked rows give 0 in every per-row output; out-of-range token ids in a
+     valid row give NaN log-prob, are counted in ``n_bad_ids`` and contribute
+     nothing to the loss or its gradient (they still count in N and n_i).
+  R6 N = 0 gives loss 0 and zero gradients.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+AGG_SEQ_MEAN_TOKEN_MEAN = 0
+AGG_TOKEN_MEAN = 1
+
+
+def _f64(x):
+    if hasattr(x, "detach"):
+        x = x.detach().cpu()
+        if str(x.dtype) == "torch.bfloat16":
+            x = x.float()
+        x = x.numpy()
+    return np.asarray(x, dtype=np.float64)
+
+
+def _take(X, rr):
+    """Rows ``rr`` of a numpy array or a (possibly device) torch tensor, as fp64."""
+    if hasattr(X, "detach"):
+        import torch
+        return _f64(X[torch.as_tensor(rr, dtype=torch.long, device=X.device)])
+    return _f64(X[rr])
+
+
+def _int(x, dtype=np.int64):
+    if hasattr(x, "detach"):
+        x = x.detach().cpu().numpy()
+    return np.asarray(x).astype(dtype)
+
+
+# ---------------------------------------------------------------- counts ----
+def token_counts(mask, seq_start):
+    """Valid-token bookkeeping (Sec. 2.2 / Sec. 3.1.2 masking; Listing 4
+    ``action_mask``).
+
+    Returns a dict with ``rows`` (indices of valid rows, ascending), ``seq``
+    (rollout of each valid row), ``n`` (valid tokens per rollout), ``N`` and
+    ``S`` (rollouts with at least one valid token).
+    """
+    m = _int(mask) != 0
+    ss = _int(seq_start)
+    n_seq = len(ss) - 1
+    n = np.zeros(n_seq, dtype=np.int64)
+    for i in range(n_seq):
+        n[i] = int(np.count_nonzero(m[ss[i]:ss[i + 1]]))
+    rows = np.nonzero(m)[0].astype(np.int64)
+    seq = np.searchsorted(ss, rows, side="right") - 1
+    return {"rows": rows, "seq": seq.astype(np.int64), "n": n,
+            "N": int(n.sum()), "S": int(np.count_nonzero(n))}
+
+
+# ------------------------------------------------------------ advantages ----
+def group_advantages(rewards, group_size, eps=1e-6):
+    """GRPO advantages (Sec. 3.2 Listing 4 ``advantage_fn: "grpo"``; reading R3).
+
+    Rewards of consecutive rollouts ``[g*G, (g+1)*G)`` form one group:
+    ``A_i = (r_i - mean) / (std + eps)`` with the sample standard deviation.
+    """
+    r = _f64(rewards)
+    G = int(group_size)
+    assert r.size % G == 0
+    out = np.zeros_like(r)
+    for g0 in range(0, r.size, G):
+        grp = r[g0:g0 + G]
+        if G < 2 or np.all(grp == grp[0]):
+            continue                      # degenerate group: advantage 0
+        mu = grp.sum() / G
+        sd = math.sqrt(((grp - mu) ** 2).sum() / (G - 1))
+        out[g0:g0 + G] = (grp - mu) / (sd + eps)
+    return out
+
+
+# ------------------------------------------------------------- log-probs ----
+def _row_stats(z, y, V):
+    """Plain two-pass log-softmax statistics of one block of logit rows."""
+    M = z.max(axis=1, keepdims=True)
+    lse = (M + np.log(np.exp(z - M).sum(axis=1, keepdims=True)))[:, 0]
+    logp_all = z - lse[:, None]
+    p = np.exp(logp_all)
+    ent = -(p * logp_all).sum(axis=1)
+    ok = (y >= 0) & (y < V)
+    logp = np.full(z.shape[0], np.nan)
+    idx = np.nonzero(ok)[0]
+    logp[idx] = logp_all[idx, y[idx]]
+    return logp, ent, lse
+
+
+def token_logprobs(H, W, ids, mask, rows=None, block=256):
+    """Per-token log-prob of the sampled id, entropy and log-sum-exp of the
+    policy head ``z = W h`` (Sec. 3.1.1 log-probs of response tokens; Sec. 3.4.2
+    actor entropy).  Masked rows are 0.
+
+    ``rows`` restricts the computation to those row indices (all rows of the
+    returned arrays outside it stay 0); it is how full-size workloads are
+    sampled one row at a time.
+    """
+    Wd = _f64(W)
+    V = Wd.shape[0]
+    m = _int(mask) != 0
+    y = _int(ids)
+    T = m.size
+    logp = np.zeros(T)
+    ent = np.zeros(T)
+    lse = np.zeros(T)
+    want = np.nonzero(m)[0] if rows is None else np.asarray([r for r in _int(rows) if m[r]],
+                                                            dtype=np.int64)
+    for b0 in range(0, want.size, block):
+        rr = want[b0:b0 + block]
+        h = _take(H, rr)
+        z = h @ Wd.T
+        lp, en, ls = _row_stats(z, y[rr], V)
+        logp[rr], ent[rr], lse[rr] = lp, en, ls
+    return logp, ent, lse
+
+
+def token_logprobs_from_logits(logits, ids, mask, rows=None, block=256):
+    """Same statistics from given logits ``[T, V]`` (the loss-only path)."""
+    m = _int(mask) != 0
+    y = _int(ids)
+    T = m.size
+    V = logits.shape[1]
+    logp = np.zeros(T)
+    ent = np.zeros(T)
+    lse = np.zeros(T)
+    want = np.nonzero(m)[0] if rows is None else np.asarray([r for r in _int(rows) if m[r]],
+                                                            dtype=np.int64)
+    for b0 in range(0, want.size, block):
+        rr = want[b0:b0 + block]
+        z = _take(logits, rr)
+        lp, en, ls = _row_stats(z, y[rr], V)
+        logp[rr], ent[rr], lse[rr] = lp, en, ls
+    return logp, ent, lse
+
+
+# ------------------------------------------------------------------ loss ----
+def clip_thresholds(eps_low, eps_high):
+    """fp32 thresholds on ``logp - old`` equivalent to ``rho < 1-eps_low`` and
+    ``rho > 1+eps_high`` (reading R4)."""
+    lo = np.float32(math.log(1.0 - eps_low)) if eps_low < 1.0 else np.float32(-np.inf)
+    hi = np.float32(math.log1p(eps_high)) if math.isfinite(eps_high) else np.float32(np.inf)
+    return lo, hi
+
+
+def ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids=None, V=None,
+                      eps_low=0.2, eps_high=0.2, beta=0.0, agg=AGG_SEQ_MEAN_TOKEN_MEAN,
+                      denom_override=0.0, entropy=None):
+    """Clipped PPO surrogate with a k3 KL term toward the reference policy,
+    aggregated over the masked tokens (Sec. 3.3.2 clip 1 +/- 0.2 and KL; Sec. 3.2
+    Listing 4 loss-function call shape returning the loss and its metrics;
+    readings R1, R2, R4, R5, R6).
+
+    Returns a dict with the loss, its parts, the statistics and ``grad_logp``
+    (d loss / d logp per row, 0 on masked rows).
+    """
+    cnt = token_counts(mask, seq_start)
+    rows, seq, n, N, S = cnt["rows"], cnt["seq"], cnt["n"], cnt["N"], cnt["S"]
+    lp_all = _f64(logp)
+    T = lp_all.size
+    lp = lp_all[rows]
+    old = _f64(old_logp)[rows]
+    ref = _f64(ref_logp)[rows] if ref_logp is not None else np.zeros_like(lp)
+    A = _f64(adv_seq)[seq]
+    good = np.ones(rows.size, dtype=bool)
+    if ids is not None and V is not None:
+        yy = _int(ids)[rows]
+        good = (yy >= 0) & (yy < V)
+    n_bad = int((~good).sum())
+
+    if agg == AGG_SEQ_MEAN_TOKEN_MEAN:
+        Sd = denom_override if denom_override > 0 else S
+        w = np.zeros(rows.size) if Sd == 0 else 1.0 / (Sd * n[seq].astype(np.float64))
+    elif agg == AGG_TOKEN_MEAN:
+        Nd = denom_override if denom_override > 0 else N
+        w = np.zeros(rows.size) if Nd == 0 else np.full(rows.size, 1.0 / Nd)
+    else:
+        raise ValueError(agg)
+
+    delta = lp - old
+    rho = np.exp(delta)
+    rho_bar = np.clip(rho, 1.0 - eps_low, 1.0 + eps_high)
+    pg = np.maximum(-A * rho, -A * rho_bar)
+    lo32, hi32 = clip_thresholds(eps_low, eps_high)
+    d32 = (lp.astype(np.float32) - old.astype(np.float32)).astype(np.float32)
+    clipped = ((A > 0) & (d32 > hi32)) | ((A < 0) & (d32 < lo32))
+    dk = ref - lp
+    kl = np.exp(dk) - dk - 1.0
+    ell = pg + beta * kl
+    g = np.where(clipped, 0.0, -A * rho) + beta * (1.0 - np.exp(dk))
+    c = w * g
+    # bad ids contribute nothing
+    pg = np.where(good, pg, 0.0)
+    kl = np.where(good, kl, 0.0)
+    ell = np.where(good, ell, 0.0)
+    c = np.where(good, c, 0.0)
+    clipped = clipped & good
+    rho_s = np.where(good, rho, 0.0)
+
+    grad = np.zeros(T)
+    grad[rows] = c
+    out = {
+        "loss": float((w * ell).sum()),
+        "pg_loss": float((w * pg).sum()),
+        "kl_loss": float((w * beta * kl).sum()),
+        "kl_mean": float(kl.sum() / N) if N else 0.0,
+        "ratio_mean": float(rho_s.sum() / N) if N else 0.0,
+        "clipfrac": float(clipped.sum() / N) if N else 0.0,
+        "n_valid": N, "n_seq_valid": S, "n_clipped": int(clipped.sum()), "n_bad_ids": n_bad,
+        "grad_logp": grad, "weights_rows": rows, "weights": w,
+        "clipped_rows": rows[clipped],
+        "margin": np.minimum(np.abs(d32.astype(np.float64) - float(hi32)),
+                             np.abs(d32.astype(np.float64) - float(lo32))),
+    }
+    if entropy is not None:
+        ent = _f64(entropy)[rows]
+        out["entropy_mean"] = float(ent.sum() / N) if N else 0.0
+    else:
+        out["entropy_mean"] = 0.0
+    return out
+
+
+# -------------------------------------------------------------- backward ----
+def logit_grad_rows(z, y, lse, c):
+    """d loss / d z for a block of rows: ``c (onehot(y) - exp(z - lse))``."""
+    p = np.exp(z - lse[:, None])
+    dz = -p
+    ok = np.nonzero((y >= 0) & (y < z.shape[1]))[0]
+    dz[ok, y[ok]] += 1.0
+    return c[:, None] * dz
+
+
+def ppo_clip_loss_bwd(H, W, lse, grad_logp, ids, mask, rows=None, dw_rows=None, block=256,
+                      want_dw=True):
+    """Backward through the policy head: ``dZ = c (onehot(y) - softmax(z))``,
+    ``dH = dZ W`` and ``dW = dZ^T H`` over the valid rows.
+
+    ``rows`` restricts which rows of dH are returned (others 0).  ``dw_rows``
+    returns only those rows of dW, each summed over every valid token, so a
+    full-size weight gradient can be sampled without forming all of it.
+    """
+    Wd = _f64(W)
+    V, d = Wd.shape
+    m = _int(mask) != 0
+    y = _int(ids)
+    L = _f64(lse)
+    C = _f64(grad_logp)
+    T = m.size
+    valid = np.nonzero(m)[0]
+    dH = np.zeros((T, d))
+    want = valid if rows is None else np.asarray([r for r in _int(rows) if m[r]], dtype=np.int64)
+    for b0 in range(0, want.size, block):
+        rr = want[b0:b0 + block]
+        h = _take(H, rr)
+        dz = logit_grad_rows(h @ Wd.T, y[rr], L[rr], C[rr])
+        dH[rr] = dz @ Wd
+    dW = None
+    if want_dw and dw_rows is None:
+        dW = np.zeros((V, d))
+        for b0 in range(0, valid.size, block):
+            rr = valid[b0:b0 + block]
+            h = _take(H, rr)
+            dz = logit_grad_rows(h @ Wd.T, y[rr], L[rr], C[rr])
+            dW += dz.T @ h
+    elif want_dw:
+        js = _int(dw_rows)
+        dW = np.zeros((js.size, d))
+        Wj = Wd[js]
+        for b0 in range(0, valid.size, 4096):
+            rr = valid[b0:b0 + 4096]
+            h = _take(H, rr)
+            zj = h @ Wj.T                                  # [B, J]
+            dz = -np.exp(zj - L[rr][:, None])
+            dz += (y[rr][:, None] == js[None, :])
+            dz *= C[rr][:, None]
+            dW += dz.T @ h
+    return dH, dW
+
+
+def bwd_logits(logits, lse, grad_logp, ids, mask, rows=None, block=256):
+    """``dlogits = c (onehot(y) - exp(z - lse))`` on valid rows, 0 elsewhere."""
+    m = _int(mask) != 0
+    y = _int(ids)
+    L = _f64(lse)
+    C = _f64(grad_logp)
+    T, V = logits.shape
+    want = np.nonzero(m)[0] if rows is None else np.asarray([r for r in _int(rows) if m[r]],
+                                                            dtype=np.int64)
+    out = {}
+    for b0 in range(0, want.size, block):
+        rr = want[b0:b0 + block]
+        z = _take(logits, rr)
+        dz = logit_grad_rows(z, y[rr], L[rr], C[rr])
+        for k, r in enumerate(rr):
+            out[int(r)] = dz[k]
+    return out
+
+
+# ------------------------------------------------------------ whole step ----
+def trainer_step(H, W, ids, mask, seq_start, rewards, group_size, old_logp, ref_logp,
+                 eps_low, eps_high, beta, agg, denom_override=0.0, adv_eps=1e-6, want_dw=True):
+    """One pass of the whole path: advantages, log-probs/entropy, loss and the
+    gradients to H and W."""
+    adv = group_advantages(rewards, group_size, adv_eps)
+    logp, ent, lse = token_logprobs(H, W, ids, mask)
+    V = _f64(W).shape[0]
+    fw = ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv, mask, seq_start, ids, V,
+                           eps_low, eps_high, beta, agg, denom_override, entropy=ent)
+    dH, dW = ppo_clip_loss_bwd(H, W, lse, fw["grad_logp"], ids, mask, want_dw=want_dw)
+    return {"adv": adv, "logp": logp, "entropy": ent, "lse": lse, "fwd": fw, "dH": dH, "dW": dW}
+
+
+def loss_only_step(logits, ids, mask, seq_start, rewards, group_size, old_logp, ref_logp,
+                   eps_low, eps_high, beta, agg, denom_override=0.0, adv_eps=1e-6, rows=None):
+    """The loss-only path from given logits: log-probs, entropy, loss, dlogits.
+    ``rows`` samples the dlogits rows returned; the loss always uses every row."""
+    adv = group_advantages(rewards, group_size, adv_eps)
+    logp, ent, lse = token_logprobs_from_logits(logits, ids, mask)
+    V = logits.shape[1]
+    fw = ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv, mask, seq_start, ids, V,
+                           eps_low, eps_high, beta, agg, denom_override, entropy=ent)
+    dl = bwd_logits(logits, lse, fw["grad_logp"], ids, mask, rows=rows)
+    return {"adv": adv, "logp": logp, "entropy": ent, "lse": lse, "fwd": fw, "dlogits": dl}

@@ -1,0 +1,517 @@
+"""Pins of the float64 oracle against what the objective fixes (CPU only).
+
+Each test checks the oracle against something other than itself: closed
+forms, invariants, library routines, brute force or finite differences, so
+that a dropped term, a wrong sign or index, or a transposed operand fails at
+least one of them.
+"""
+import json
+import math
+import os
+
+import mpmath
+import numpy as np
+import pytest
+import scipy.special
+import scipy.stats
+import torch
+
+from oracle import rft_oracle as O
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "closed_forms.json")))
+rng0 = np.random.default_rng(12345)
+
+
+def _layout(lengths, pad):
+    n_seq = len(lengths)
+    ss = np.arange(n_seq + 1, dtype=np.int32) * pad
+    mask = np.zeros(n_seq * pad, dtype=np.uint8)
+    for i, L in enumerate(lengths):
+        mask[i * pad:i * pad + L] = 1
+    return ss, mask
+
+
+# ------------------------------------------------------------------ counts --
+def test_counts_brute_force():
+    rng = np.random.default_rng(1)
+    for _ in range(20):
+        n_seq = int(rng.integers(1, 9))
+        lens = rng.integers(0, 7, size=n_seq)
+        ss = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        T = int(ss[-1])
+        mask = (rng.random(T) < 0.6).astype(np.uint8)
+        c = O.token_counts(mask, ss)
+        # pure-Python loops
+        rows, seq, n = [], [], [0] * n_seq
+        for i in range(n_seq):
+            for t in range(int(ss[i]), int(ss[i + 1])):
+                if mask[t]:
+                    rows.append(t)
+                    seq.append(i)
+                    n[i] += 1
+        assert c["rows"].tolist() == rows
+        assert c["seq"].tolist() == seq
+        assert c["n"].tolist() == n
+        assert c["N"] == sum(n)
+        assert c["S"] == sum(1 for x in n if x > 0)
+
+
+# -------------------------------------------------------------- log-probs --
+def _one_layer(T=6, d=5, V=11, scale=1.0, seed=0):
+    rng = np.random.default_rng(seed)
+    H = rng.standard_normal((T, d))
+    W = rng.standard_normal((V, d)) * scale
+    ids = rng.integers(0, V, size=T)
+    return H, W, ids
+
+
+def test_logprobs_normalise_over_vocab():
+    H, W, _ = _one_layer(T=4, d=6, V=37, scale=1.5)
+    mask = np.ones(4, dtype=np.uint8)
+    tot = np.zeros(4)
+    for j in range(37):
+        lp, _, _ = O.token_logprobs(H, W, np.full(4, j), mask)
+        tot += np.exp(lp)
+    np.testing.assert_allclose(tot, 1.0, rtol=0, atol=1e-13)
+
+
+def test_logprobs_zero_weight_is_uniform():
+    V = 512
+    H = rng0.standard_normal((5, 8))
+    W = np.zeros((V, 8))
+    lp, ent, lse = O.token_logprobs(H, W, np.arange(5), np.ones(5, np.uint8))
+    assert np.all(lp == -math.log(V)) or np.allclose(lp, -math.log(V), atol=1e-15)
+    np.testing.assert_allclose(ent, math.log(V), atol=1e-13)
+    np.testing.assert_allclose(lse, math.log(V), atol=1e-13)
+
+
+def test_logprobs_dominant_logit():
+    V = 64
+    logits = rng0.standard_normal((3, V))
+    logits[:, 5] += 1000.0
+    lp, ent, lse = O.token_logprobs_from_logits(logits, np.full(3, 5), np.ones(3, np.uint8))
+    np.testing.assert_allclose(lp, 0.0, atol=1e-300)
+    np.testing.assert_allclose(ent, 0.0, atol=1e-300)
+    np.testing.assert_allclose(lse, logits[:, 5], rtol=1e-15)
+
+
+def test_logprobs_row_shift_invariance_and_library():
+    V = 300
+    logits = rng0.standard_normal((7, V)) * 3
+    ids = rng0.integers(0, V, size=7)
+    m = np.ones(7, np.uint8)
+    lp, ent, lse = O.token_logprobs_from_logits(logits, ids, m)
+    shift = rng0.standard_normal(7) * 50
+    lp2, ent2, lse2 = O.token_logprobs_from_logits(logits + shift[:, None], ids, m)
+    np.testing.assert_allclose(lp2, lp, atol=1e-12)
+    np.testing.assert_allclose(ent2, ent, atol=1e-11)
+    np.testing.assert_allclose(lse2, lse + shift, atol=1e-12)
+    # library routines: scipy logsumexp, scipy entropy
+    np.testing.assert_allclose(lse, scipy.special.logsumexp(logits, axis=1), rtol=1e-14)
+    p = scipy.special.softmax(logits, axis=1)
+    np.testing.assert_allclose(ent, scipy.stats.entropy(p, axis=1), rtol=1e-12)
+    np.testing.assert_allclose(lp, np.log(p[np.arange(7), ids]), rtol=1e-12)
+
+
+def test_logprobs_mpmath_brute_force():
+    H, W, ids = _one_layer(T=3, d=4, V=9, scale=2.0, seed=3)
+    lp, ent, lse = O.token_logprobs(H, W, ids, np.ones(3, np.uint8))
+    mpmath.mp.dps = 40
+    for t in range(3):
+        z = [mpmath.fsum(mpmath.mpf(float(W[j, k])) * mpmath.mpf(float(H[t, k])) for k in range(4))
+             for j in range(9)]
+        s = mpmath.fsum(mpmath.e ** zj for zj in z)
+        L = mpmath.log(s)
+        assert abs(float(L) - lse[t]) < 1e-14
+        assert abs(float(z[ids[t]] - L) - lp[t]) < 1e-14
+        Hent = -mpmath.fsum((mpmath.e ** (zj - L)) * (zj - L) for zj in z)
+        assert abs(float(Hent) - ent[t]) < 1e-14
+
+
+def test_golden_two_logit():
+    g = GOLD["two_logit_softmax"]
+    logits = np.array([g["logits"], g["logits"]])
+    lp, ent, lse = O.token_logprobs_from_logits(logits, np.array([1, 0]), np.ones(2, np.uint8))
+    assert lse[0] == pytest.approx(g["lse"], abs=1e-15)
+    assert lp[0] == pytest.approx(g["logp_id1"], abs=1e-15)
+    assert lp[1] == pytest.approx(g["logp_id0"], abs=1e-15)
+    assert ent[0] == pytest.approx(g["entropy"], abs=1e-15)
+
+
+def test_two_logit_entropy_closed_form():
+    for a in [-30.0, -2.0, 0.0, 0.3, 5.0, 40.0]:
+        logits = np.array([[0.0, a]])
+        _, ent, _ = O.token_logprobs_from_logits(logits, np.array([0]), np.ones(1, np.uint8))
+        s = 1.0 / (1.0 + math.exp(-a))              # p of the second logit
+        expect = math.log1p(math.exp(a)) - a * s if a < 30 else (1 + a) * math.exp(-a)
+        assert ent[0] == pytest.approx(expect, rel=1e-9, abs=1e-12)
+        assert ent[0] >= 0
+
+
+def test_gaussian_logits_statistics():
+    # logits ~ N(0, 2^2), V = 151936: lse ~ ln V + 2, entropy ~ ln V - 2
+    rng = np.random.default_rng(7)
+    V = 151936
+    logits = rng.standard_normal((4, V)) * 2.0
+    _, ent, lse = O.token_logprobs_from_logits(logits, np.zeros(4, np.int64), np.ones(4, np.uint8))
+    assert np.all(np.abs(lse - (math.log(V) + 2)) < 0.1)
+    assert np.all(np.abs(ent - (math.log(V) - 2)) < 0.2)
+
+
+def test_masked_rows_and_compaction():
+    H, W, ids = _one_layer(T=10, d=4, V=13, seed=5)
+    mask = np.array([1, 0, 1, 1, 0, 0, 1, 0, 1, 1], np.uint8)
+    lp, ent, lse = O.token_logprobs(H, W, ids, mask)
+    v = np.nonzero(mask)[0]
+    lp2, ent2, lse2 = O.token_logprobs(H[v], W, ids[v], np.ones(v.size, np.uint8))
+    assert np.all(lp[mask == 0] == 0) and np.all(ent[mask == 0] == 0) and np.all(lse[mask == 0] == 0)
+    np.testing.assert_array_equal(lp[v], lp2)
+    np.testing.assert_array_equal(ent[v], ent2)
+
+
+def test_bad_ids_give_nan_logp():
+    H, W, ids = _one_layer(T=4, d=3, V=5)
+    ids = np.array([0, 5, -1, 4])
+    lp, ent, _ = O.token_logprobs(H, W, ids, np.ones(4, np.uint8))
+    assert np.isfinite(lp[0]) and np.isfinite(lp[3])
+    assert np.isnan(lp[1]) and np.isnan(lp[2])
+    assert np.all(np.isfinite(ent))
+
+
+# ------------------------------------------------------------- advantages --
+def test_advantages_moments_and_degenerate():
+    rng = np.random.default_rng(11)
+    for G in [2, 3, 8, 16, 33]:
+        r = rng.standard_normal(G * 5)
+        r[:G] = 0.7                                   # degenerate group
+        a = O.group_advantages(r, G)
+        assert np.all(a[:G] == 0.0)
+        for g in range(1, 5):
+            grp = a[g * G:(g + 1) * G]
+            raw = r[g * G:(g + 1) * G]
+            assert abs(grp.mean()) < 1e-12
+            sd = np.std(raw, ddof=1)                  # library sample std
+            assert abs(np.std(grp, ddof=1) - sd / (sd + 1e-6)) < 1e-12
+            assert abs(np.std(grp, ddof=1) - 1.0) <= 1e-5
+
+
+def test_advantages_group_of_two_golden():
+    g = GOLD["grpo_group_of_two"]
+    a = O.group_advantages(np.array(g["rewards"]), 2)
+    np.testing.assert_allclose(a, g["adv"], rtol=1e-14)
+    np.testing.assert_allclose(np.abs(a), 1 / math.sqrt(2), rtol=2e-6)
+
+
+def test_advantages_affine_and_permutation():
+    rng = np.random.default_rng(2)
+    r = rng.random(32)
+    a = O.group_advantages(r, 8)
+    a2 = O.group_advantages(3.5 * r - 7.0, 8)
+    np.testing.assert_allclose(a2, a, atol=1e-5)      # eps breaks exact scale invariance
+    perm = np.concatenate([g * 8 + rng.permutation(8) for g in range(4)])
+    np.testing.assert_allclose(O.group_advantages(r[perm], 8), a[perm], atol=1e-14)
+    assert np.all(O.group_advantages(np.ones(8), 1) == 0)
+
+
+def test_advantages_binary_rewards():
+    # k successes out of G with 0/1 rewards: A = (r - k/G) / (sqrt(k(G-k)/(G(G-1))) + eps)
+    G = 8
+    for k in range(1, G):
+        r = np.array([1.0] * k + [0.0] * (G - k))
+        sd = math.sqrt(k * (G - k) / (G * (G - 1)))
+        np.testing.assert_allclose(O.group_advantages(r, G), (r - k / G) / (sd + 1e-6), rtol=1e-14)
+
+
+# ------------------------------------------------------------------- loss --
+def _loss_case(seed=0, n_seq=6, pad=7, V=50):
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(0, pad + 1, size=n_seq)
+    lens[0] = pad
+    ss, mask = _layout(lens, pad)
+    T = n_seq * pad
+    logp = -rng.random(T) * 5
+    old = logp + rng.standard_normal(T) * 0.3
+    ref = logp + rng.standard_normal(T) * 0.3
+    adv = rng.standard_normal(n_seq)
+    ids = rng.integers(0, V, size=T)
+    return ss, mask, logp, old, ref, adv, ids, V
+
+
+def test_ratio_one_gives_minus_mean_advantage():
+    ss, mask, logp, _, ref, adv, ids, V = _loss_case(seed=4)
+    c = O.token_counts(mask, ss)
+    for agg in (0, 1):
+        out = O.ppo_clip_loss_fwd(logp, logp, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.0, agg)
+        # pure-Python expectation
+        if agg == 0:
+            S = sum(1 for x in c["n"] if x > 0)
+            exp = -sum(adv[i] for i in range(len(adv)) if c["n"][i] > 0) / S
+        else:
+            tot = 0.0
+            for t in range(mask.size):
+                if mask[t]:
+                    i = int(np.searchsorted(ss, t, side="right") - 1)
+                    tot += adv[i]
+            exp = -tot / c["N"]
+        assert out["loss"] == pytest.approx(exp, rel=1e-13, abs=1e-15)
+        assert out["clipfrac"] == 0.0 and out["kl_loss"] == 0.0
+        assert out["ratio_mean"] == pytest.approx(1.0, abs=1e-15)
+
+
+def test_zero_advantage():
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=5)
+    out = O.ppo_clip_loss_fwd(logp, old, ref, np.zeros_like(adv), mask, ss, ids, V, 0.2, 0.2, 0.0, 0)
+    assert out["pg_loss"] == 0.0 and np.all(out["grad_logp"] == 0.0)
+    out = O.ppo_clip_loss_fwd(logp, old, ref, np.zeros_like(adv), mask, ss, ids, V, 0.2, 0.2, 0.3, 0)
+    w = dict(zip(out["weights_rows"].tolist(), out["weights"].tolist()))
+    for t in range(mask.size):
+        if mask[t]:
+            assert out["grad_logp"][t] == pytest.approx(w[t] * 0.3 * (1 - math.exp(ref[t] - logp[t])),
+                                                        rel=1e-13)
+
+
+@pytest.mark.parametrize("eps_low,eps_high", [(0.2, 0.2), (0.2, 0.28), (0.1, 0.5)])
+def test_clip_branches_single_token(eps_low, eps_high):
+    ss = np.array([0, 1], np.int32)
+    mask = np.ones(1, np.uint8)
+    cases = [  # (A, rho, clipped, pg)
+        (1.0, 1.6, 1.6 > 1 + eps_high, -min(1.6, 1 + eps_high)),
+        (1.0, 0.5, False, -0.5),
+        (-1.0, 0.5, 0.5 < 1 - eps_low, max(0.5, 1 - eps_low)),
+        (-1.0, 1.6, False, 1.6),
+        (2.0, 1.1, False, -2.2),
+    ]
+    for A, rho, clipped, pg in cases:
+        lp = np.array([-1.0])
+        old = lp - math.log(rho)
+        out = O.ppo_clip_loss_fwd(lp, old, None, np.array([A]), mask, ss, None, None,
+                                  eps_low, eps_high, 0.0, 0)
+        assert out["pg_loss"] == pytest.approx(pg, rel=1e-12)
+        assert out["n_clipped"] == int(clipped)
+        g = 0.0 if clipped else -A * rho
+        assert out["grad_logp"][0] == pytest.approx(g, rel=1e-12, abs=1e-300)
+
+
+def test_golden_ppo_tokens():
+    for key in ("ppo_single_token_clipped", "ppo_single_token_unclipped_negative_adv"):
+        g = GOLD[key]
+        out = O.ppo_clip_loss_fwd(np.array([g["logp"]]), np.array([g["old_logp"]]),
+                                  np.array([g["ref_logp"]]), np.array([g["adv"]]),
+                                  np.ones(1, np.uint8), np.array([0, 1]), None, None,
+                                  g["eps"], g["eps"], g["beta"], 0)
+        assert out["pg_loss"] == pytest.approx(g["pg_loss"], rel=1e-12)
+        assert out["loss"] == pytest.approx(g["loss"], rel=1e-12)
+        assert out["grad_logp"][0] == pytest.approx(g["grad_logp"], rel=1e-12)
+
+
+def test_unbounded_clip_is_plain_importance_gradient():
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=6)
+    out = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 1.0, math.inf, 0.0, 0)
+    c = O.token_counts(mask, ss)
+    A = adv[c["seq"]]
+    rho = np.exp(logp[c["rows"]] - old[c["rows"]])
+    np.testing.assert_allclose(out["grad_logp"][c["rows"]], out["weights"] * (-A * rho), rtol=1e-13)
+    assert out["n_clipped"] == 0
+
+
+def test_kl_properties():
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=7)
+    out0 = O.ppo_clip_loss_fwd(logp, old, logp, adv, mask, ss, ids, V, 0.2, 0.2, 0.7, 0)
+    assert out0["kl_loss"] == 0.0 and out0["kl_mean"] == 0.0
+    small = logp + 1e-3 * np.random.default_rng(0).standard_normal(logp.size)
+    out = O.ppo_clip_loss_fwd(logp, old, small, adv, mask, ss, ids, V, 0.2, 0.2, 1.0, 1)
+    c = O.token_counts(mask, ss)
+    dlt = (small - logp)[c["rows"]]
+    assert out["kl_mean"] == pytest.approx(float((dlt ** 2 / 2).mean()), rel=2e-3)
+    out = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 1.0, 0)
+    assert out["kl_mean"] > 0
+    # kl of one token against the closed form
+    g = GOLD["ppo_single_token_clipped"]
+    o1 = O.ppo_clip_loss_fwd(np.array([g["logp"]]), np.array([g["logp"]]), np.array([g["ref_logp"]]),
+                             np.array([0.0]), np.ones(1, np.uint8), np.array([0, 1]), None, None,
+                             0.2, 0.2, 1.0, 0)
+    assert o1["kl_mean"] == pytest.approx(g["kl"], rel=1e-13)
+
+
+def test_aggregations_coincide_on_equal_lengths():
+    rng = np.random.default_rng(9)
+    ss = np.arange(5, dtype=np.int32) * 6
+    mask = np.ones(24, np.uint8)
+    logp = -rng.random(24)
+    old = logp + 0.2 * rng.standard_normal(24)
+    adv = rng.standard_normal(4)
+    a = O.ppo_clip_loss_fwd(logp, old, logp, adv, mask, ss, None, None, 0.2, 0.2, 0.0, 0)
+    b = O.ppo_clip_loss_fwd(logp, old, logp, adv, mask, ss, None, None, 0.2, 0.2, 0.0, 1)
+    assert a["loss"] == pytest.approx(b["loss"], rel=1e-14)
+    np.testing.assert_allclose(a["grad_logp"], b["grad_logp"], rtol=1e-14)
+
+
+def test_denominator_override_scales():
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=10)
+    for agg in (0, 1):
+        a = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.1, agg)
+        base = a["n_seq_valid"] if agg == 0 else a["n_valid"]
+        b = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.1, agg,
+                                denom_override=4.0 * base)
+        assert b["loss"] == pytest.approx(a["loss"] / 4.0, rel=1e-13)
+
+
+def test_empty_batch():
+    ss = np.array([0, 3, 6], np.int32)
+    mask = np.zeros(6, np.uint8)
+    out = O.ppo_clip_loss_fwd(np.zeros(6), np.zeros(6), np.zeros(6), np.ones(2), mask, ss,
+                              None, None, 0.2, 0.2, 0.1, 0)
+    assert out["loss"] == 0.0 and out["n_valid"] == 0 and np.all(out["grad_logp"] == 0)
+
+
+def test_bad_ids_in_loss():
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=12)
+    v = np.nonzero(mask)[0]
+    ids = ids.copy()
+    ids[v[0]] = V
+    ids[v[3]] = -2
+    out = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.1, 0)
+    assert out["n_bad_ids"] == 2
+    assert out["grad_logp"][v[0]] == 0.0 and out["grad_logp"][v[3]] == 0.0
+    assert out["n_valid"] == v.size
+
+
+# --------------------------------------------------------------- gradients --
+def _loss_of(H, W, ids, mask, ss, old, ref, adv, eps_l, eps_h, beta, agg):
+    lp, _, _ = O.token_logprobs(H, W, ids, mask)
+    return O.ppo_clip_loss_fwd(lp, old, ref, adv, mask, ss, ids, W.shape[0], eps_l, eps_h,
+                               beta, agg)
+
+
+def _grad_case(seed):
+    rng = np.random.default_rng(seed)
+    lens = [5, 3, 0, 4]
+    ss, mask = _layout(lens, 5)
+    T, d, V = 20, 6, 9
+    H = rng.standard_normal((T, d))
+    W = rng.standard_normal((V, d)) * 0.8
+    ids = rng.integers(0, V, size=T)
+    lp, _, _ = O.token_logprobs(H, W, ids, mask)
+    old = lp + rng.standard_normal(T) * 0.25
+    ref = lp + rng.standard_normal(T) * 0.3
+    adv = rng.standard_normal(4)
+    return H, W, ids, mask, ss, old, ref, adv
+
+
+@pytest.mark.parametrize("agg", [0, 1])
+def test_finite_difference_gradients(agg):
+    # first seed whose tokens all lie more than 1e-3 from a clip bound
+    for seed in range(21 + 100 * agg, 121 + 100 * agg):
+        H, W, ids, mask, ss, old, ref, adv = _grad_case(seed)
+        args = (ids, mask, ss, old, ref, adv, 0.2, 0.28, 0.05, agg)
+        base = _loss_of(H, W, *args)
+        if base["margin"].min() > 1e-3:
+            break
+    assert base["margin"].min() > 1e-3
+    assert base["n_clipped"] > 0          # the clipped branch is exercised
+    _, _, lse = O.token_logprobs(H, W, ids, mask)
+    dH, dW = O.ppo_clip_loss_bwd(H, W, lse, base["grad_logp"], ids, mask)
+    h = 1e-6
+    for X, G in ((H, dH), (W, dW)):
+        for idx in np.ndindex(X.shape):
+            if X is H and not mask[idx[0]]:
+                assert G[idx] == 0.0
+                continue
+            Xp = X.copy(); Xp[idx] += h
+            Xm = X.copy(); Xm[idx] -= h
+            Hp, Wp = (Xp, W) if X is H else (H, Xp)
+            Hm, Wm = (Xm, W) if X is H else (H, Xm)
+            fd = (_loss_of(Hp, Wp, *args)["loss"] - _loss_of(Hm, Wm, *args)["loss"]) / (2 * h)
+            assert abs(fd - G[idx]) <= 1e-6 * max(1.0, abs(G).max()), (X is H, idx, fd, G[idx])
+
+
+def test_finite_difference_logits():
+    rng = np.random.default_rng(5)
+    ss = np.array([0, 4, 8], np.int32)
+    mask = np.array([1, 1, 0, 1, 1, 1, 1, 0], np.uint8)
+    T, V = 8, 7
+    logits = rng.standard_normal((T, V)) * 2
+    ids = rng.integers(0, V, size=T)
+    lp, _, lse = O.token_logprobs_from_logits(logits, ids, mask)
+    old = lp + 0.2 * rng.standard_normal(T)
+    ref = lp + 0.2 * rng.standard_normal(T)
+    adv = np.array([0.8, -1.1])
+
+    def L(z):
+        l2, _, _ = O.token_logprobs_from_logits(z, ids, mask)
+        return O.ppo_clip_loss_fwd(l2, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.1, 0)
+
+    base = L(logits)
+    dl = O.bwd_logits(logits, lse, base["grad_logp"], ids, mask)
+    h = 1e-6
+    for t in range(T):
+        for j in range(V):
+            zp = logits.copy(); zp[t, j] += h
+            zm = logits.copy(); zm[t, j] -= h
+            fd = (L(zp)["loss"] - L(zm)["loss"]) / (2 * h)
+            g = dl[t][j] if t in dl else 0.0
+            assert abs(fd - g) < 1e-8, (t, j, fd, g)
+
+
+def test_torch_autograd_third_implementation():
+    """torch float64 autograd of the naive loss expression on tiny inputs."""
+    H, W, ids, mask, ss, old, ref, adv = _grad_case(31)
+    eps_l, eps_h, beta = 0.2, 0.28, 0.05
+    base = _loss_of(H, W, ids, mask, ss, old, ref, adv, eps_l, eps_h, beta, 0)
+    _, _, lse = O.token_logprobs(H, W, ids, mask)
+    dH, dW = O.ppo_clip_loss_bwd(H, W, lse, base["grad_logp"], ids, mask)
+
+    Ht = torch.tensor(H, requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    logits = Ht @ Wt.T
+    logprob = torch.log_softmax(logits, dim=-1).gather(1, torch.tensor(ids)[:, None])[:, 0]
+    m = torch.tensor(mask, dtype=torch.float64)
+    T = mask.size
+    seq = torch.tensor(np.searchsorted(ss, np.arange(T), side="right") - 1)
+    A = torch.tensor(adv)[seq]
+    ratio = torch.exp(logprob - torch.tensor(old))
+    surr = torch.maximum(-A * ratio, -A * torch.clamp(ratio, 1 - eps_l, 1 + eps_h))
+    dk = torch.tensor(ref) - logprob
+    per_tok = surr + beta * (torch.exp(dk) - dk - 1)
+    n_i = torch.zeros(len(ss) - 1, dtype=torch.float64).index_add_(0, seq, m)
+    S = (n_i > 0).sum()
+    loss = ((per_tok * m) / n_i[seq].clamp(min=1)).sum() / S
+    loss.backward()
+    assert loss.item() == pytest.approx(base["loss"], rel=1e-12)
+    np.testing.assert_allclose(dH, Ht.grad.numpy(), rtol=1e-10, atol=1e-14)
+    np.testing.assert_allclose(dW, Wt.grad.numpy(), rtol=1e-10, atol=1e-14)
+
+
+def test_weight_gradient_invariants():
+    H, W, ids, mask, ss, old, ref, adv = _grad_case(41)
+    base = _loss_of(H, W, ids, mask, ss, old, ref, adv, 0.2, 0.2, 0.01, 0)
+    _, _, lse = O.token_logprobs(H, W, ids, mask)
+    dH, dW = O.ppo_clip_loss_bwd(H, W, lse, base["grad_logp"], ids, mask)
+    # rows of dZ sum to zero, hence the columns of dW sum to zero
+    np.testing.assert_allclose(dW.sum(axis=0), 0.0, atol=1e-13)
+    # adding a common vector to every row of W leaves log-probs and dH unchanged
+    u = np.random.default_rng(0).standard_normal(W.shape[1])
+    W2 = W + u[None, :]
+    lp2, _, lse2 = O.token_logprobs(H, W2, ids, mask)
+    lp1, _, _ = O.token_logprobs(H, W, ids, mask)
+    np.testing.assert_allclose(lp2, lp1, atol=1e-12)
+    dH2, _ = O.ppo_clip_loss_bwd(H, W2, lse2, base["grad_logp"], ids, mask)
+    np.testing.assert_allclose(dH2, dH, atol=1e-12)
+    # sampled dW rows agree with the full dW
+    _, dWs = O.ppo_clip_loss_bwd(H, W, lse, base["grad_logp"], ids, mask, dw_rows=[0, 3, 8])
+    np.testing.assert_allclose(dWs, dW[[0, 3, 8]], rtol=1e-12, atol=1e-15)
+
+
+def test_whole_step_composition():
+    rng = np.random.default_rng(3)
+    ss, mask = _layout([4, 4, 2, 3], 4)
+    T, d, V = 16, 5, 11
+    H = rng.standard_normal((T, d))
+    W = rng.standard_normal((V, d))
+    ids = rng.integers(0, V, size=T)
+    r = np.array([1.0, 0.0, 1.0, 1.0])
+    lp, _, _ = O.token_logprobs(H, W, ids, mask)
+    out = O.trainer_step(H, W, ids, mask, ss, r, 2, lp, lp, 0.2, 0.2, 0.0, 0)
+    # ratio 1, no KL: loss = -mean advantage over rollouts with tokens
+    a = O.group_advantages(r, 2)
+    assert out["fwd"]["loss"] == pytest.approx(-a.mean(), abs=1e-14)
