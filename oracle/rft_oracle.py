@@ -41,7 +41,8 @@ Readings where the paper is silent (it prints no formula):
      takes the same decision; values are fp64.
   R5 Masked rows give 0 in every per-row output; out-of-range token ids in a
      valid row give NaN log-prob, are counted in ``n_bad_ids`` and contribute
-     nothing to the loss or its gradient (they still count in N and n_i).
+     nothing to the loss, its metrics or its gradient (they still count in N
+     and n_i).
   R6 N = 0 gives loss 0 and zero gradients.
 """
 from __future__ import annotations
@@ -260,7 +261,7 @@ def ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids=No
                              np.abs(d32.astype(np.float64) - float(lo32))),
     }
     if entropy is not None:
-        ent = _f64(entropy)[rows]
+        ent = np.where(good, _f64(entropy)[rows], 0.0)
         out["entropy_mean"] = float(ent.sum() / N) if N else 0.0
     else:
         out["entropy_mean"] = 0.0
