@@ -1,0 +1,233 @@
+"""Benchmark of the GRPO/PPO trainer-step core on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 7b|1.5b|longcot|lossonly|tiny]
+
+One step is one pass of the whole hot path over one synthetic batch that is
+already resident in HBM: group advantages, per-token log-probs and entropy
+through the lm_head (online log-sum-exp, no stored logits), the PPO-clip/KL
+loss, and the backward to the hidden states and the lm_head weight (the
+loss-only workload: log-softmax statistics, loss and d_logits from given
+logits).  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "response tokens/s for fused logprob+PPO-clip fwd+bwd; % bf16 MFMA / HBM peak"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+WORKLOADS = {"tiny": 0, "1.5b": 1, "7b": 2, "longcot": 3, "lossonly": 4}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="7b", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline sample")
+    return ap.parse_args()
+
+
+def cpu_baseline(batch, target_s, extra):
+    """Time the float64 oracle on a bounded sample of the same workload."""
+    import numpy as np
+    from oracle import rft_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    cfg = batch.cfg
+    mask = batch.mask.cpu().numpy()
+    valid = np.nonzero(mask)[0]
+
+    def run(n_rows):
+        rows = valid[:n_rows]
+        ss = np.array([0, n_rows], dtype=np.int32)
+        m = np.ones(n_rows, dtype=np.uint8)
+        ids = batch.ids.cpu().numpy()[rows]
+        rewards = np.array([1.0], dtype=np.float64)
+        t0 = time.perf_counter()
+        if cfg.dtype == "logits":
+            z = batch.logits[rows].cpu()
+            lp, _, _ = O.token_logprobs_from_logits(z, ids, m)
+            O.loss_only_step(z, ids, m, ss, rewards, 1, lp + 0.1, lp - 0.1, cfg.eps_low,
+                             cfg.eps_high, cfg.beta, cfg.agg)
+            lp2 = None
+        else:
+            H = batch.H[rows].cpu()
+            W = extra["W_cpu"]
+            lp, _, _ = O.token_logprobs(H, W, ids, m)
+            O.trainer_step(H, W, ids, m, ss, rewards, 1, lp + 0.1, lp - 0.1, cfg.eps_low,
+                           cfg.eps_high, cfg.beta, cfg.agg)
+        return time.perf_counter() - t0
+
+    if cfg.dtype != "logits":
+        extra["W_cpu"] = batch.W.cpu()
+    n0 = 32
+    t0 = run(n0)
+    n = int(min(valid.size, max(n0, n0 * target_s / max(t0, 1e-3))))
+    t = run(n) if n > n0 else t0
+    return {"value": n / t, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {n} valid tokens of the same batch as one rollout, whole step "
+                      f"(log-probs, loss, dH and dW over the full vocabulary) in float64; "
+                      f"{t:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the path would shard by whole GRPO groups (see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2505_17826_amd as R
+    from gen import synth
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cid = WORKLOADS[args.workload]
+    cfg = synth.config(cid)
+    t_gen = time.perf_counter()
+    b = synth.make_batch(cfg, dev)
+    torch.cuda.synchronize()
+    t_gen = time.perf_counter() - t_gen
+    print(f"[bench] workload {cfg.name}: T={b.T} generated in {t_gen:.1f} s", file=sys.stderr,
+          flush=True)
+
+    tok = R.Tokens(b.seq_start, b.mask, b.ids)
+    N = int(b.mask.sum().item())
+    n_seq = cfg.n_seq
+    params = R.ppo_params(cfg.eps_low, cfg.eps_high, cfg.beta, cfg.agg)
+    T = b.T
+    f32 = dict(dtype=torch.float32, device=dev)
+    adv = torch.empty(n_seq, **f32)
+    logp = torch.empty(T, **f32)
+    ent = torch.empty(T, **f32)
+    lse = torch.empty(T, **f32)
+    grad = torch.empty(T, **f32)
+    stats = torch.zeros(R.STATS_BYTES, dtype=torch.uint8, device=dev)
+    V = cfg.V
+    events = []
+
+    if cfg.dtype == "logits":
+        dl = torch.empty_like(b.logits)
+        ws_f = torch.empty(max(1, R.workspace_bytes(R.RFT_OP_PPO_FUSED_LOGITS, tok, 0, V)),
+                           dtype=torch.uint8, device=dev)
+        # rollout-side log-probs for the old / reference policies (setup, untimed)
+        R.rft_token_logprobs_from_logits(tok, b.logits, logp=logp, entropy=ent, lse=lse)
+        old = torch.where(b.mask.bool(), logp + b.old_noise, torch.zeros_like(logp))
+        ref = torch.where(b.mask.bool(), logp + b.ref_noise, torch.zeros_like(logp))
+
+        def step(ev=None):
+            R.rft_group_advantages(b.rewards, cfg.group, out=adv)
+            if ev is not None:
+                ev[0].record()
+            R.rft_ppo_clip_fused_logits(tok, b.logits, old, ref, adv, params, logp=logp,
+                                        entropy=ent, lse=lse, grad_logp=grad, d_logits=dl,
+                                        stats=stats, ws=ws_f)
+            if ev is not None:
+                ev[1].record()
+        dom_name = "k_logits_fused (one workgroup per row: stats, loss, d_logits)"
+        # algorithmic bytes: read every valid row once, write every row of d_logits once
+        dom_work = (N * V * 4 + T * V * 4) / 1e9  # GB
+        bound = "hbm"
+    else:
+        d = cfg.d
+        dt = R.RFT_BF16 if cfg.dtype == "bf16" else R.RFT_F32
+        dH = torch.empty((T, d), **f32)
+        dW = torch.empty((V, d), **f32)
+        ws_fwd = torch.empty(R.workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, tok, d, V, dt),
+                             dtype=torch.uint8, device=dev)
+        ws_loss = torch.empty(R.workspace_bytes(R.RFT_OP_PPO_FWD, tok, d, V, dt),
+                              dtype=torch.uint8, device=dev)
+        ws_bwd = torch.empty(R.workspace_bytes(R.RFT_OP_PPO_BWD, tok, d, V, dt),
+                             dtype=torch.uint8, device=dev)
+        R.rft_token_logprobs(tok, b.H, b.W, logp=logp, entropy=ent, lse=lse, ws=ws_fwd)
+        old = torch.where(b.mask.bool(), logp + b.old_noise, torch.zeros_like(logp))
+        ref = torch.where(b.mask.bool(), logp + b.ref_noise, torch.zeros_like(logp))
+
+        def step(ev=None):
+            R.rft_group_advantages(b.rewards, cfg.group, out=adv)
+            if ev is not None:
+                ev[0].record()
+            R.rft_token_logprobs(tok, b.H, b.W, logp=logp, entropy=ent, lse=lse, ws=ws_fwd)
+            if ev is not None:
+                ev[1].record()
+            R.rft_ppo_clip_loss_fwd(tok, V, logp, old, ref, adv, params, entropy=ent,
+                                    grad_logp=grad, stats=stats, ws=ws_loss)
+            R.rft_ppo_clip_loss_bwd(tok, b.H, b.W, lse, grad, d_hidden=dH, d_weight=dW,
+                                    ws=ws_bwd)
+        dom_name = "rft_token_logprobs (MFMA lm_head forward + online LSE), 2*N*d*V per call"
+        dom_work = 2.0 * N * d * V / 1e12  # TFLOP
+        bound = "mfma" if cfg.dtype == "bf16" else "alu"
+
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for k in range(args.steps):
+        step(evs[k])
+    t_end.record()
+    torch.cuda.synchronize()
+    ms = t_start.elapsed_time(t_end) / max(args.steps, 1)
+    dom_ms = float(np.mean([a.elapsed_time(z) for a, z in evs])) if args.steps else float("nan")
+    st = R.stats_to_dict(stats)
+    tokens_per_s = N / (ms / 1e3)
+
+    out = {
+        "metric": METRIC, "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": {"bf16": "bf16", "f32": "f32", "logits": "f32"}[cfg.dtype],
+        "data": "synthetic (seeded; shapes and distributions of the workload, no dataset)",
+        "config": {"workload": cfg.name, "n_seq": n_seq, "group": cfg.group, "T": T,
+                   "valid_tokens": N, "V": V, "d": cfg.d, "eps": [cfg.eps_low, cfg.eps_high],
+                   "kl_coef": cfg.beta, "agg": cfg.agg},
+    }
+    if bound == "hbm":
+        ach = dom_work / (dom_ms / 1e3)
+        out["roofline"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                           "frac": ach / PEAK_HBM_GBS, "traffic": None, "kernel": dom_name,
+                           "ms_per_launch": dom_ms}
+    else:
+        ach = dom_work / (dom_ms / 1e3)
+        peak = PEAK_BF16_TFLOPS if bound == "mfma" else 157.3
+        out["roofline"] = {"bound": bound, "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                           "frac": ach / peak, "traffic": None, "kernel": dom_name,
+                           "ms_per_launch": dom_ms}
+        alg = 6.0 * N * cfg.d * V / 1e12
+        out["step_mfma"] = {"algorithmic_tflop": alg, "algorithmic_tflops": alg / (ms / 1e3),
+                            "frac_algorithmic": alg / (ms / 1e3) / peak,
+                            "frac_executed": (8.0 * N * cfg.d * V / 1e12) / (ms / 1e3) / peak}
+    out["loss"] = st["loss"]
+    out["clipfrac"] = st["clipfrac"]
+    if not args.no_cpu_baseline:
+        print("[bench] timing the float64 oracle on a CPU sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds, {})
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

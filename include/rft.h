@@ -1,0 +1,227 @@
+/*
+ * rft.h - C ABI of the MI355X (gfx950) GRPO/PPO trainer-step core.
+ *
+ * The library computes the data-parallel core of one reinforcement
+ * fine-tuning trainer step as described in the Trinity-RFT report
+ * (arXiv 2505.17826): per-token policy log-probabilities and entropy over the
+ * whole vocabulary, GRPO group-normalised advantages, the clipped PPO
+ * surrogate with a KL term toward a reference policy, and the backward pass
+ * of that loss to the hidden states and the lm_head weight.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Memory.  Every pointer argument is a DEVICE pointer unless its comment
+ *    says (host).  The caller allocates and owns every buffer; the library
+ *    never allocates or frees device memory inside a call.  Scratch memory
+ *    is passed in as a workspace (`ws`, `ws_bytes`) sized by
+ *    rft_workspace_bytes().  Device buffers must be 16-byte aligned.
+ *  - Streams.  `stream` is a hipStream_t (NULL = the default stream).  Every
+ *    call only enqueues work on that stream and returns without a device
+ *    synchronisation.  A return value other than RFT_OK means nothing was
+ *    enqueued (except RFT_E_HIP, which reports a launch failure).
+ *  - Errors.  Calls return an rft_status; rft_last_error() gives a
+ *    thread-local text describing the last failure.  No call aborts or lets
+ *    an exception cross the ABI.  Problems that only the device can see
+ *    (token ids out of range) are reported in rft_ppo_stats.n_bad_ids and by
+ *    a NaN log-probability for that row; ids are never clamped.
+ *  - Token layout (rft_tokens).  T rows (tokens) form n_seq rollouts;
+ *    rollout i owns rows [seq_start[i], seq_start[i+1]) with seq_start[0] = 0,
+ *    non-decreasing, seq_start[n_seq] = T (a padded [n_seq, L] batch has
+ *    seq_start[i] = i*L).  mask[t] != 0 marks a response token that enters
+ *    the objective (action mask; multi-turn rollouts mask the environment's
+ *    tokens, Sec. 2.2 and Sec. 3.1.2).  Masked rows are never read from the
+ *    hidden states or logits and give 0 in every per-row output.  The
+ *    contents of seq_start are not validated; an invalid layout gives
+ *    unspecified values but every access stays in bounds.
+ *  - Matrices are row-major.  hidden is [T, d], weight is [V, d] (the
+ *    nn.Linear layout; logits z_t = weight . hidden_t), logits are [T, V].
+ *    bf16 data requires d % 8 == 0.
+ */
+#ifndef RFT_H_
+#define RFT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RFT_ABI_VERSION 1
+
+typedef enum {
+  RFT_OK = 0,
+  RFT_E_NULL = 1,        /* a required pointer is NULL                         */
+  RFT_E_SHAPE = 2,       /* a size is negative, inconsistent or unsupported   */
+  RFT_E_DTYPE = 3,       /* unknown dtype                                      */
+  RFT_E_PARAM = 4,       /* a scalar parameter is out of range                 */
+  RFT_E_WORKSPACE = 5,   /* workspace NULL or smaller than required            */
+  RFT_E_UNSUPPORTED = 6, /* valid request the library does not implement       */
+  RFT_E_HIP = 7          /* the HIP runtime reported an error                  */
+} rft_status;
+
+typedef enum { RFT_F32 = 0, RFT_BF16 = 1 } rft_dtype;
+
+/* Loss aggregation over the masked tokens. */
+typedef enum {
+  RFT_AGG_SEQ_MEAN_TOKEN_MEAN = 0, /* mean over rollouts of per-rollout token means:
+                                      weight 1/(S * n_i), S = rollouts with n_i > 0 */
+  RFT_AGG_TOKEN_MEAN = 1           /* mean over all valid tokens: weight 1/N          */
+} rft_agg;
+
+/* Operations, for rft_workspace_bytes(). */
+typedef enum {
+  RFT_OP_TOKEN_LOGPROBS = 0,
+  RFT_OP_TOKEN_LOGPROBS_FROM_LOGITS = 1,
+  RFT_OP_PPO_FWD = 2,
+  RFT_OP_PPO_BWD = 3,
+  RFT_OP_PPO_BWD_LOGITS = 4,
+  RFT_OP_PPO_FUSED_LOGITS = 5
+} rft_op;
+
+/* (host struct holding device pointers) */
+typedef struct {
+  int64_t T;                 /* rows                                             */
+  int64_t n_seq;             /* rollouts                                         */
+  const int32_t* seq_start;  /* [n_seq + 1] row offsets                          */
+  const uint8_t* mask;       /* [T] 1 = token in the objective                   */
+  const int32_t* token_ids;  /* [T] sampled ids; valid rows should be in [0, V)  */
+} rft_tokens;
+
+/* (host struct) PPO-clip / KL parameters. */
+typedef struct {
+  float eps_low;          /* ratio lower bound 1 - eps_low, 0 <= eps_low <= 1       */
+  float eps_high;         /* ratio upper bound 1 + eps_high, eps_high >= 0 (inf ok) */
+  float kl_coef;          /* beta >= 0; 0 disables the KL term (ref_logp may be NULL) */
+  int32_t agg;            /* rft_agg                                                */
+  double denom_override;  /* 0: use the call's own S (or N); > 0: use this value,
+                             e.g. the global count across micro-batches             */
+} rft_ppo_params;
+
+/* (device struct) loss value and metrics written by the loss calls. */
+typedef struct {
+  double loss;          /* pg_loss + kl_loss                          */
+  double pg_loss;       /* sum_t w_t * clipped surrogate              */
+  double kl_loss;       /* sum_t w_t * beta * kl_t                    */
+  double kl_mean;       /* mean over valid tokens of kl_t             */
+  double entropy_mean;  /* mean over valid tokens of entropy (0 if no entropy given) */
+  double ratio_mean;    /* mean over valid tokens of exp(logp - old)  */
+  double clipfrac;      /* n_clipped / N                              */
+  int64_t n_valid;      /* N                                          */
+  int64_t n_seq_valid;  /* S                                          */
+  int64_t n_clipped;
+  int64_t n_bad_ids;
+} rft_ppo_stats;
+
+/* Version of this ABI (RFT_ABI_VERSION). */
+int rft_abi_version(void);
+
+/* Static text for a status code. */
+const char* rft_status_str(int status);
+
+/* (host) Thread-local description of the last failure in this thread. */
+const char* rft_last_error(void);
+
+/* Workspace bytes the operation `op` needs for this layout and sizes (d and V
+ * as in the call; dtype of hidden/weight).  For RFT_OP_PPO_BWD the value is
+ * the recommended size; any size >= rft_workspace_min_bytes() works, a larger
+ * workspace processes more rows per backward chunk.  Returns 0 for invalid
+ * arguments. */
+size_t rft_workspace_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
+size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
+
+/* GRPO group-relative advantages (Sec. 3.2, Listing 4: advantage_fn "grpo",
+ * repeat_times 8; Sec. 3.3.1: 8 rollouts per task).
+ * rewards[n_groups * group_size] (f32); rollouts g*G .. g*G+G-1 form group g.
+ * adv_i = (r_i - mean_g) / (std_g + eps), std the sample standard deviation
+ * (divisor G - 1); a group whose rewards are all equal (or G == 1) gets 0.
+ * adv[n_groups * group_size] (f32) may not alias rewards.
+ * Errors: RFT_E_NULL, RFT_E_SHAPE (n_groups < 0, group_size < 1),
+ * RFT_E_PARAM (eps < 0 or not finite). */
+rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t group_size,
+                                float eps, float* adv, void* stream);
+
+/* Per-token log-probability of the sampled id, entropy and log-sum-exp of the
+ * policy head z_t = weight . hidden_t over the whole vocabulary (Sec. 3.1.1:
+ * log-probs of the response tokens; Sec. 3.4.2: actor entropy).
+ * hidden [T, d] and weight [V, d] in `dtype` (bf16: MFMA tiles with fp32
+ * accumulation; f32: fp32 arithmetic).  The logits are formed tile by tile
+ * and folded into an online log-sum-exp; the T x V logits are never stored.
+ * Outputs (f32, [T]): logp (NaN for a valid row whose id is out of range),
+ * entropy (may be NULL), lse.  Masked rows are 0.  hidden and the outputs may
+ * be NULL when T == 0.
+ * Errors: RFT_E_NULL, RFT_E_SHAPE (d < 1, V < 1, T < 0, bf16 with d % 8),
+ * RFT_E_DTYPE, RFT_E_WORKSPACE. */
+rft_status rft_token_logprobs(const rft_tokens* tok, const void* hidden, const void* weight,
+                              int dtype, int64_t d, int64_t V, float* logp, float* entropy,
+                              float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* The same statistics from given fp32 logits [T, V].  gathered (may be NULL)
+ * receives logits[t, id_t] (bit-exact copy; NaN for an out-of-range id). */
+rft_status rft_token_logprobs_from_logits(const rft_tokens* tok, const float* logits, int64_t V,
+                                          float* logp, float* entropy, float* lse,
+                                          float* gathered, void* ws, size_t ws_bytes,
+                                          void* stream);
+
+/* Clipped PPO surrogate with a k3 KL term toward the reference policy over the
+ * masked tokens (Sec. 3.3.2: ratio clipped to 1 +/- 0.2 by default, KL
+ * penalty or loss; Sec. 3.2, Listing 4: the policy loss takes the log-probs,
+ * the old log-probs, the action mask and the advantages and returns the loss
+ * with its metrics).  Per valid token t of rollout i:
+ *   rho = exp(logp - old), A = adv[i],
+ *   pg = max(-A rho, -A clamp(rho, 1-eps_low, 1+eps_high)),
+ *   kl = exp(ref - logp) - (ref - logp) - 1,
+ *   loss = sum_t w_t (pg + beta kl)  with w_t from params.agg,
+ *   grad_logp[t] = w_t (-A rho [not clipped] + beta (1 - exp(ref - logp))).
+ * "Clipped" means A > 0 and rho > 1+eps_high, or A < 0 and rho < 1-eps_low,
+ * decided in fp32 on logp - old against fp32(log(1 +/- eps)).
+ * Inputs f32 [T] (adv is [n_seq]); ref_logp may be NULL iff kl_coef == 0;
+ * entropy may be NULL (entropy_mean 0).  Outputs: grad_logp [T] (0 on
+ * masked rows), *stats (device).  A valid row with an out-of-range id counts
+ * in n_bad_ids and adds nothing to the loss, metrics or gradient.  With N = 0
+ * the loss and every metric are 0.  Reductions run in fp64 in a fixed order.
+ * Errors: RFT_E_NULL, RFT_E_SHAPE, RFT_E_PARAM, RFT_E_WORKSPACE. */
+rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* logp,
+                                 const float* old_logp, const float* ref_logp, const float* adv,
+                                 const float* entropy, const rft_ppo_params* params,
+                                 float* grad_logp, rft_ppo_stats* stats, void* ws,
+                                 size_t ws_bytes, void* stream);
+
+/* Backward of the loss through the policy head: with c_t = grad_logp[t],
+ *   dZ_tj = c_t ([j == id_t] - exp(z_tj - lse_t)),
+ *   d_hidden = dZ . weight   ([T, d] f32, masked rows 0, always overwritten),
+ *   d_weight = dZ^T . hidden ([V, d] f32, overwritten, or added to when
+ *              accumulate_dw != 0).
+ * z is recomputed from hidden and weight (it is never stored by the forward);
+ * dZ is formed in chunks of rows in the workspace (bf16 for bf16 inputs).
+ * lse and grad_logp [T] are normally the outputs of rft_token_logprobs and
+ * rft_ppo_clip_loss_fwd.
+ * Errors: as rft_token_logprobs. */
+rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, const void* weight,
+                                 int dtype, int64_t d, int64_t V, const float* lse,
+                                 const float* grad_logp, float* d_hidden, float* d_weight,
+                                 int32_t accumulate_dw, void* ws, size_t ws_bytes, void* stream);
+
+/* d_logits[t, j] = c_t ([j == id_t] - exp(logits[t, j] - lse_t)) on valid
+ * rows, 0 on masked rows (every row of d_logits [T, V] f32 is written). */
+rft_status rft_ppo_clip_loss_bwd_logits(const rft_tokens* tok, const float* logits, int64_t V,
+                                        const float* lse, const float* grad_logp,
+                                        float* d_logits, void* ws, size_t ws_bytes, void* stream);
+
+/* The loss-only path in one pass per row: log-softmax statistics of the given
+ * logits, the PPO-clip/KL loss and metrics, and d_logits, reading each valid
+ * logits row once from HBM (a second read of the row is served from cache)
+ * and writing d_logits once.  Outputs as rft_token_logprobs_from_logits,
+ * rft_ppo_clip_loss_fwd and rft_ppo_clip_loss_bwd_logits (entropy may be
+ * NULL; lse and grad_logp may be NULL). */
+rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits, int64_t V,
+                                     const float* old_logp, const float* ref_logp,
+                                     const float* adv, const rft_ppo_params* params, float* logp,
+                                     float* entropy, float* lse, float* grad_logp,
+                                     float* d_logits, rft_ppo_stats* stats, void* ws,
+                                     size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RFT_H_ */

@@ -1,0 +1,197 @@
+// GRPO group advantages, the per-token PPO-clip/KL loss with its fixed-order
+// fp64 reduction, and the merge of the per-tile log-sum-exp partials into
+// per-token log-prob / entropy / lse.
+#include "rft_internal.h"
+
+namespace rft {
+
+// ---------------------------------------------------------- advantages ----
+// GRPO (Sec. 3.2, Listing 4, advantage_fn "grpo"): one wavefront per group;
+// mean and sample std by wavefront shuffles, computed in fp64.
+__global__ void __launch_bounds__(256) k_group_adv(const float* __restrict__ r, int64_t n_groups,
+                                                   int G, float eps, float* __restrict__ adv) {
+  int lane = threadIdx.x & 63;
+  int64_t g = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (g >= n_groups) return;
+  const float* rg = r + g * G;
+  double s = 0.0;
+  float mn = INFINITY, mx = -INFINITY;
+  for (int j = lane; j < G; j += 64) {
+    float v = rg[j];
+    s += (double)v;
+    mn = fminf(mn, v);
+    mx = fmaxf(mx, v);
+  }
+  s = wave_sum_d(s);
+  mn = wave_min_f(mn);
+  mx = wave_max_f(mx);
+  double mu = s / (double)G;
+  double q = 0.0;
+  for (int j = lane; j < G; j += 64) {
+    double dv = (double)rg[j] - mu;
+    q += dv * dv;
+  }
+  q = wave_sum_d(q);
+  bool degenerate = (G < 2) || (mn == mx);
+  double sd = degenerate ? 0.0 : sqrt(q / (double)(G - 1));
+  for (int j = lane; j < G; j += 64)
+    adv[g * G + j] = degenerate ? 0.f : (float)(((double)rg[j] - mu) / (sd + (double)eps));
+}
+
+hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, float* adv,
+                            hipStream_t s) {
+  if (n_groups > 0) k_group_adv<<<(unsigned)((n_groups + 3) / 4), 256, 0, s>>>(r, n_groups, G, eps, adv);
+  return hipGetLastError();
+}
+
+// -------------------------------------------------------- loss reduction ----
+__device__ void block_reduce_partial(LossPartial& p, LossPartial* out) {
+  __shared__ LossPartial sh[16];
+  int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  p.loss = wave_sum_d(p.loss);
+  p.pg = wave_sum_d(p.pg);
+  p.klw = wave_sum_d(p.klw);
+  p.kl = wave_sum_d(p.kl);
+  p.ent = wave_sum_d(p.ent);
+  p.ratio = wave_sum_d(p.ratio);
+  p.clipped = wave_sum_ll(p.clipped);
+  p.bad = wave_sum_ll(p.bad);
+  if (lane == 0) sh[w] = p;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    LossPartial t = sh[0];
+    for (int i = 1; i < (int)(blockDim.x >> 6); ++i) {
+      t.loss += sh[i].loss; t.pg += sh[i].pg; t.klw += sh[i].klw; t.kl += sh[i].kl;
+      t.ent += sh[i].ent; t.ratio += sh[i].ratio; t.clipped += sh[i].clipped; t.bad += sh[i].bad;
+    }
+    *out = t;
+  }
+}
+
+// Per-token loss over rows [0, T): grid of 256-row blocks.
+__global__ void __launch_bounds__(256) k_loss_fwd(
+    const uint8_t* __restrict__ mask, const int32_t* __restrict__ ids, const int32_t* __restrict__ kidx,
+    const int32_t* __restrict__ row_seq, const int32_t* __restrict__ n_i, const int32_t* __restrict__ meta,
+    int64_t T, const float* __restrict__ logp, const float* __restrict__ old,
+    const float* __restrict__ ref, const float* __restrict__ adv, const float* __restrict__ ent,
+    LossConst c, float* __restrict__ grad, LossPartial* __restrict__ parts) {
+  int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  LossPartial p = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (t < T) {
+    int k = kidx[t];
+    float gout = 0.f;
+    if (k >= 0) {
+      int i = row_seq[k];
+      int y = ids[t];
+      if (y < 0 || (int64_t)y >= c.V) {
+        p.bad = 1;
+      } else {
+        float lp = logp[t];
+        float rf = ref ? ref[t] : lp;
+        TokLoss L = token_loss(lp, old[t], rf, adv[i], n_i[i], meta[0], meta[1], c);
+        double ell = (double)L.pg + (double)c.beta * (double)L.kl;
+        p.loss = L.w * ell;
+        p.pg = L.w * (double)L.pg;
+        p.klw = L.w * (double)c.beta * (double)L.kl;
+        p.kl = (double)L.kl;
+        p.ratio = (double)L.rho;
+        p.ent = ent ? (double)ent[t] : 0.0;
+        p.clipped = L.clipped ? 1 : 0;
+        gout = (float)(L.w * (double)L.g);
+      }
+    }
+    grad[t] = gout;
+  }
+  block_reduce_partial(p, parts + blockIdx.x);
+}
+
+// One block: fixed-order sum of the block partials into the stats struct.
+__global__ void __launch_bounds__(1024) k_loss_final(const LossPartial* __restrict__ parts, int n,
+                                                     const int32_t* __restrict__ meta,
+                                                     rft_ppo_stats* __restrict__ st) {
+  LossPartial p = {0, 0, 0, 0, 0, 0, 0, 0};
+  // each thread sums a contiguous run, in order
+  int per = (n + 1023) / 1024;
+  int a = threadIdx.x * per, b = min(n, a + per);
+  for (int i = a; i < b; ++i) {
+    p.loss += parts[i].loss; p.pg += parts[i].pg; p.klw += parts[i].klw; p.kl += parts[i].kl;
+    p.ent += parts[i].ent; p.ratio += parts[i].ratio; p.clipped += parts[i].clipped; p.bad += parts[i].bad;
+  }
+  __shared__ LossPartial out;
+  block_reduce_partial(p, &out);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int N = meta[0], S = meta[1];
+    double inv = N > 0 ? 1.0 / (double)N : 0.0;
+    st->loss = N > 0 ? out.loss : 0.0;
+    st->pg_loss = N > 0 ? out.pg : 0.0;
+    st->kl_loss = N > 0 ? out.klw : 0.0;
+    st->kl_mean = out.kl * inv;
+    st->entropy_mean = out.ent * inv;
+    st->ratio_mean = out.ratio * inv;
+    st->clipfrac = (double)out.clipped * inv;
+    st->n_valid = N;
+    st->n_seq_valid = S;
+    st->n_clipped = out.clipped;
+    st->n_bad_ids = out.bad;
+  }
+}
+
+hipError_t launch_loss_final(const LossPartial* parts, int nparts, const int32_t* meta,
+                             rft_ppo_stats* stats, hipStream_t s) {
+  k_loss_final<<<1, 1024, 0, s>>>(parts, nparts, meta, stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_loss_fwd(const rft_tokens& tok, const TokMeta& m, const float* logp,
+                           const float* old, const float* ref, const float* adv, const float* ent,
+                           const LossConst& c, float* grad, LossPartial* parts, rft_ppo_stats* st,
+                           hipStream_t s) {
+  int nb = (int)((tok.T + 255) / 256);
+  if (nb > 0)
+    k_loss_fwd<<<nb, 256, 0, s>>>(tok.mask, tok.token_ids, m.kidx, m.row_seq, m.n_i, m.meta, tok.T,
+                                  logp, old, ref, adv, ent, c, grad, parts);
+  return launch_loss_final(parts, nb, m.meta, st, s);
+}
+
+// -------------------------------------------------------- lse partials ----
+// Merge the per-vocabulary-tile partials (m, s, u) of each valid row into
+// lse, entropy = lse - u/s and logp = z_y - lse; masked rows get 0.
+// parts are [ntiles][ld] with the compacted row index as the inner index.
+__global__ void __launch_bounds__(256) k_merge_rows(
+    const int32_t* __restrict__ kidx, const int32_t* __restrict__ ids, int64_t T, int64_t V,
+    const float* __restrict__ pm, const float* __restrict__ ps, const float* __restrict__ pu,
+    int ntiles, int64_t ld, const float* __restrict__ zy, float* __restrict__ logp,
+    float* __restrict__ ent, float* __restrict__ lse) {
+  int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= T) return;
+  int k = kidx[t];
+  if (k < 0) {
+    logp[t] = 0.f;
+    if (ent) ent[t] = 0.f;
+    lse[t] = 0.f;
+    return;
+  }
+  float m = -INFINITY, sm = 0.f, u = 0.f;
+  for (int j = 0; j < ntiles; ++j) {
+    int64_t o = (int64_t)j * ld + k;
+    lse_merge(m, sm, u, pm[o], ps[o], pu[o]);
+  }
+  float L = m + logf(sm);
+  lse[t] = L;
+  if (ent) ent[t] = L - u / sm;
+  int y = ids[t];
+  logp[t] = (y >= 0 && (int64_t)y < V) ? zy[k] - L : __int_as_float(0x7fc00000);
+}
+
+hipError_t launch_merge_rows(const rft_tokens& tok, const TokMeta& m, int64_t V, const float* pm,
+                             const float* ps, const float* pu, int ntiles, int64_t ld,
+                             const float* zy, float* logp, float* ent, float* lse, hipStream_t s) {
+  int nb = (int)((tok.T + 255) / 256);
+  if (nb > 0)
+    k_merge_rows<<<nb, 256, 0, s>>>(m.kidx, tok.token_ids, tok.T, V, pm, ps, pu, ntiles, ld, zy,
+                                    logp, ent, lse);
+  return hipGetLastError();
+}
+
+}  // namespace rft

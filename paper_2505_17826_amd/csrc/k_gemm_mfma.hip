@@ -1,0 +1,422 @@
+// bf16 MFMA "NT" GEMM core for gfx950 with the trainer-step epilogues:
+//   C[m, n] = sum_k A[m, k] * B[n, k]   (both operands K-contiguous, bf16)
+// 256x256 workgroup tile, BK = 64, four wavefronts each owning 128x128 of C
+// as 4x4 v_mfma_f32_32x32x16_bf16 tiles (fp32 accumulators).  Operands go
+// straight from HBM/L2 into LDS with buffer_load_dwordx4 ... lds (no staging
+// registers); the buffer descriptor covers only the tile's valid rows, so rows
+// past the end and the K tail read as zeros without branches.  LDS holds
+// 16-byte chunks XOR-swizzled by row (conflict-free ds_read_b128 of MFMA
+// fragments) in two stages.  Workgroups map to tiles so that the ones resident
+// on one XCD work on neighbouring tiles (shared L2), and the number of rows
+// can come from a device counter, so the host never waits for the count of
+// valid tokens.
+//
+// Epilogues:
+//   EPI_STATS  forward of the policy head: per row and 256-column vocabulary
+//              tile, online log-sum-exp partials (max, sum exp, sum exp*z) and
+//              the logit of the sampled token.  Logits are never stored.
+//   EPI_DZ     backward recompute: dZ = c (onehot(y) - exp(z - lse)) in bf16,
+//              written row-major [rows, Vpad] and transposed [Vpad, rows].
+//   EPI_STORE  fp32 result, optionally scattered to rows through a map and
+//              optionally added to the existing values.
+#include "rft_internal.h"
+
+namespace rft {
+namespace mf {
+
+constexpr int BM = 256, BN = 256, BK = 64, NT = 256;
+constexpr int A_BYTES = BM * BK * 2;
+constexpr int B_BYTES = BN * BK * 2;
+constexpr int STAGE = A_BYTES + B_BYTES;  // 64 KiB
+constexpr int ROWP = BM * 16;             // per-row epilogue parameters
+constexpr int LDS_TOTAL = 2 * STAGE + ROWP;
+
+enum { EPI_STATS = 0, EPI_DZ = 1, EPI_STORE = 2 };
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// wait for this wave's outstanding vector-memory loads (including the
+// loads that write LDS directly)
+__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+struct Args {
+  const uint16_t* A;  // [M, lda]
+  int64_t lda;
+  const uint16_t* B;  // [NB, ldb]
+  int64_t ldb;
+  int M, N, K;        // host values (M, K are caps when taken from the device counter)
+  int NB;             // rows of B that exist (read only for n < NB; 0 = N)
+  const int32_t* cnt; // device counter: c = clamp(*cnt - cnt_off, 0, cnt_cap) (nullptr = none)
+  int64_t cnt_off;
+  int64_t cnt_cap;
+  int m_from_cnt;     // M = c
+  int k_from_cnt;     // K = round_up(c, BK)
+  // epilogue data
+  const int32_t* rows;  // compacted row -> token row (index rows_off + m)
+  int64_t rows_off;
+  const int32_t* ids;
+  const float* lse;
+  const float* cgrad;
+  float* pm; float* ps; float* pu; int64_t ldp; float* zy;  // EPI_STATS (index rows_off + m)
+  uint16_t* dz; int64_t ldz; uint16_t* dzt; int64_t ldzt; int64_t Vvalid;  // EPI_DZ
+  float* C; int64_t ldc; int accumulate; int c_scatter;  // EPI_STORE
+};
+
+// Raw buffer descriptor (wave-uniform) over `bytes` bytes from p.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int64_t bytes) {
+  uint64_t a = (uint64_t)p;
+  uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  int nr = __builtin_amdgcn_readfirstlane((int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), 0, nr, 0x00020000);
+}
+
+// Stage loader: wave w fills rows [w*64, w*64+64) of the A and B tiles with
+// 8 instructions of 8 rows each.  Lane l writes LDS slot l of an instruction
+// (row l/8, physical chunk l%8), so it loads logical chunk (l%8) ^ (row & 7)
+// of its row; chunks at or past K are read from outside the descriptor (0).
+__device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB,
+                                           char* dst, int k0, int K, int ld_chunk, uint32_t voffA,
+                                           uint32_t voffB, uint32_t strideA8, uint32_t strideB8) {
+  const bool kin = k0 + ld_chunk * 8 < K;
+  const uint32_t va = kin ? voffA + (uint32_t)k0 * 2u : 0x80000000u;
+  const uint32_t vb = kin ? voffB + (uint32_t)k0 * 2u : 0x80000000u;
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_ptr)(dst + p * 1024), 16,
+                                             va + (uint32_t)p * strideA8, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES + p * 1024), 16,
+                                             vb + (uint32_t)p * strideB8, 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void tile_of(int L, int nTm, int nTn, int& mt, int& nt) {
+  constexpr int GM = 8;
+  int per = GM * nTn;
+  int g = L / per, r = L - g * per;
+  int m_first = g * GM;
+  int gsz = min(nTm - m_first, GM);
+  mt = m_first + r % gsz;
+  nt = r / gsz;
+}
+
+template <int EPI>
+__global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
+  __shared__ __attribute__((aligned(16))) char lds[LDS_TOTAL];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 1, wn = wid & 1;
+
+  int M = g.M, K = g.K;
+  if (g.cnt) {
+    int64_t c = (int64_t)g.cnt[0] - g.cnt_off;
+    c = c < 0 ? 0 : (c > g.cnt_cap ? g.cnt_cap : c);
+    if (g.m_from_cnt) M = (int)c;
+    if (g.k_from_cnt) K = (int)((c + BK - 1) / BK * BK);
+  }
+  const int N = g.N;
+  const int NB = g.NB > 0 ? g.NB : N;
+  if (EPI == EPI_STORE && g.k_from_cnt && K == 0 && g.accumulate) return;  // nothing to add
+  const int nTm = (M + BM - 1) / BM, nTn = (N + BN - 1) / BN;
+  const int total = nTm * nTn;
+  // Workgroup b runs on XCD b % 8: give each XCD a contiguous run of tiles so
+  // the workgroups resident on one XCD share operand tiles in its L2.  The
+  // grid is sized for the largest possible M; workgroups past the device
+  // count exit at once (they are dispatched last).
+  const int per_xcd = (total + 7) >> 3;
+  const int L = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if ((int)(blockIdx.x >> 3) >= per_xcd || L >= total) return;
+  const int nk = (K + BK - 1) / BK;
+
+  // per-lane load geometry (see gload): row w*64 + p*8 + (lane>>3), chunk below
+  const int ld_row = wid * 64 + (lane >> 3);
+  const int ld_chunk = (lane & 7) ^ ((lane >> 3) & 7);
+  const uint32_t voffA = (uint32_t)(ld_row * g.lda * 2 + ld_chunk * 16);
+  const uint32_t voffB = (uint32_t)(ld_row * g.ldb * 2 + ld_chunk * 16);
+  const uint32_t strideA8 = (uint32_t)(8 * g.lda * 2), strideB8 = (uint32_t)(8 * g.ldb * 2);
+  // per-lane MFMA operand offsets (row = base + (lane&31), chunk = ks*2 + (lane>>5))
+  const int fr = lane & 31, fh = lane >> 5;
+
+  int32_t* rp_i = (int32_t*)(lds + 2 * STAGE);
+  float* rp_a = (float*)(lds + 2 * STAGE + BM * 4);
+  float* rp_b = (float*)(lds + 2 * STAGE + BM * 8);
+
+  {
+    int mt, nt;
+    tile_of(L, nTm, nTn, mt, nt);
+    const int m0 = mt * BM, n0 = nt * BN;
+
+    // buffer descriptors over the tile's valid rows: everything else reads 0
+    const int rowsA = min(BM, M - m0);
+    const int rowsB = NB > n0 ? min(BN, NB - n0) : 0;
+    const int nb0 = rowsB > 0 ? n0 : 0;
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(g.A + (int64_t)m0 * g.lda, rowsA * g.lda * 2);
+    const __amdgpu_buffer_rsrc_t rB = make_rsrc(g.B + (int64_t)nb0 * g.ldb, rowsB * g.ldb * 2);
+
+    // per-row epilogue parameters for this tile
+    {
+      int m = m0 + tid;
+      bool v = m < M;
+      if (EPI == EPI_STATS) {
+        int y = -1;
+        if (v) y = g.ids[g.rows[g.rows_off + m]];
+        rp_i[tid] = y;
+      } else if (EPI == EPI_DZ) {
+        int y = -1;
+        float L_ = 0.f, c_ = 0.f;
+        if (v) {
+          int t = g.rows[g.rows_off + m];
+          y = g.ids[t];
+          L_ = g.lse[t];
+          c_ = g.cgrad[t];
+        }
+        rp_i[tid] = y;
+        rp_a[tid] = L_;
+        rp_b[tid] = c_;
+      } else {
+        rp_i[tid] = (v && g.c_scatter) ? g.rows[g.rows_off + m] : m;
+      }
+    }
+
+    floatx16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    if (nk > 0)
+      load_stage(rA, rB, lds + wid * 64 * 128, 0, K, ld_chunk, voffA, voffB, strideA8, strideB8);
+    wait_vm();
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + 1 < nk)
+        load_stage(rA, rB, lds + ((kt + 1) & 1) * STAGE + wid * 64 * 128, (kt + 1) * BK, K,
+                   ld_chunk, voffA, voffB, strideA8, strideB8);
+      const char* As = lds + (kt & 1) * STAGE;
+      const char* Bs = As + A_BYTES;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int ch = ((ks * 2 + fh) ^ (fr & 7)) << 4;
+        bf16x8 a[4], b[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          a[i] = *(const bf16x8*)(As + (wm * 128 + i * 32 + fr) * 128 + ch);
+          b[i] = *(const bf16x8*)(Bs + (wn * 128 + i * 32 + fr) * 128 + ch);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      }
+      wait_vm();
+      __syncthreads();
+    }
+
+    // ------------------------------------------------------------ epilogue
+    // accumulator element e of tile (i, j): row = wm*128 + i*32 + (e>>2)*8 + fh*4 + (e&3),
+    //                                       col = wn*128 + j*32 + fr
+    const int colb = n0 + wn * 128 + fr;
+    if (EPI == EPI_STATS) {
+      float* xm = (float*)lds;  // cross-wave exchange [256 rows][3]
+      bool cv[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cv[j] = colb + j * 32 < N;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_barrier(0);  // keep the accumulator reads of one tile row together
+        float mx[16], sm[16], um[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          float v = -INFINITY;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v = cv[j] ? fmaxf(v, acc[i][j][e]) : v;
+          mx[e] = v;
+        }
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx[e] = half_max(mx[e]);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          float s = 0.f, u = 0.f;
+          float mk = mx[e] == -INFINITY ? 0.f : mx[e] * kLog2e;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            float z = acc[i][j][e];
+            float p = cv[j] ? exp2f(z * kLog2e - mk) : 0.f;
+            s += p;
+            u += cv[j] ? p * z : 0.f;
+          }
+          sm[e] = s;
+          um[e] = u;
+        }
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          sm[e] = half_sum(sm[e]);
+          um[e] = half_sum(um[e]);
+        }
+        // logit of the sampled token
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          int rl = wm * 128 + i * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
+          int y = rp_i[rl];
+          int yl = y - (n0 + wn * 128);
+          if (yl >= 0 && yl < 128 && (yl & 31) == fr) {
+            int jj = yl >> 5;
+            float z = jj == 0 ? acc[i][0][e] : jj == 1 ? acc[i][1][e] : jj == 2 ? acc[i][2][e] : acc[i][3][e];
+            g.zy[g.rows_off + m0 + rl] = z;
+          }
+        }
+        // lane (fr) < 16 owns row e = fr of its half
+        float om = mx[0], os = sm[0], ou = um[0];
+#pragma unroll
+        for (int e = 1; e < 16; ++e) {
+          bool sel = (fr & 15) == e;
+          om = sel ? mx[e] : om;
+          os = sel ? sm[e] : os;
+          ou = sel ? um[e] : ou;
+        }
+        const int e_own = fr & 15;
+        const int rl = wm * 128 + i * 32 + (e_own >> 2) * 8 + fh * 4 + (e_own & 3);
+        if (wn == 1 && fr < 16) {
+          xm[rl * 3 + 0] = om;
+          xm[rl * 3 + 1] = os;
+          xm[rl * 3 + 2] = ou;
+        }
+        __syncthreads();
+        if (wn == 0 && fr < 16) {
+          int m = m0 + rl;
+          if (m < M) {
+            lse_merge(om, os, ou, xm[rl * 3 + 0], xm[rl * 3 + 1], xm[rl * 3 + 2]);
+            int64_t o = (int64_t)nt * g.ldp + g.rows_off + m;
+            g.pm[o] = om;
+            g.ps[o] = os;
+            g.pu[o] = ou;
+          }
+        }
+        __syncthreads();
+      }
+    } else if (EPI == EPI_DZ) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          __builtin_amdgcn_sched_barrier(0);
+          const int rl0 = wm * 128 + i * 32 + e4 * 8 + fh * 4;
+          float Lr[4], cr[4];
+          int yr[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            yr[q] = rp_i[rl0 + q];
+            Lr[q] = rp_a[rl0 + q] * kLog2e;
+            cr[q] = rp_b[rl0 + q];
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int col = colb + j * 32;
+            const bool cvalid = col < g.Vvalid;
+            uint16_t hb[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              float z = acc[i][j][e4 * 4 + q];
+              float p = exp2f(z * kLog2e - Lr[q]);
+              float d = cr[q] * ((col == yr[q] ? 1.f : 0.f) - p);
+              d = cvalid ? d : 0.f;
+              hb[q] = f32_to_bf16(d);
+              g.dz[(int64_t)(m0 + rl0 + q) * g.ldz + col] = hb[q];
+            }
+            uint2 pk;
+            pk.x = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
+            pk.y = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
+            *(uint2*)(g.dzt + (int64_t)col * g.ldzt + m0 + rl0) = pk;
+          }
+        }
+      }
+    } else {  // EPI_STORE
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int rl = wm * 128 + i * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
+          const int m = m0 + rl;
+          if (m >= M) continue;
+          const int64_t dst = (int64_t)rp_i[rl] * g.ldc;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int col = colb + j * 32;
+            if (col < N) {
+              float v = acc[i][j][e];
+              if (g.accumulate) v += g.C[dst + col];
+              g.C[dst + col] = v;
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+}  // namespace mf
+
+// ------------------------------------------------------------ launchers ----
+static unsigned grid_for(int64_t M_cap, int64_t N) {
+  int64_t tiles = ((M_cap + mf::BM - 1) / mf::BM) * ((N + mf::BN - 1) / mf::BN);
+  return (unsigned)((tiles + 7) / 8 * 8);
+}
+
+// Forward of the policy head over the compacted hidden rows Hc [rows_off, rows_off + cap):
+// online-LSE partials [ntiles][ldp] and the sampled-token logit zy.
+hipError_t mfma_fwd_stats(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V,
+                          const int32_t* rows, const int32_t* ids, const int32_t* cnt,
+                          int64_t rows_off, int64_t cap, float* pm, float* ps, float* pu,
+                          int64_t ldp, float* zy, hipStream_t s) {
+  mf::Args a = {};
+  a.A = Hc + rows_off * d; a.lda = d;
+  a.B = W; a.ldb = d;
+  a.M = (int)cap; a.N = (int)V; a.K = (int)d;
+  a.cnt = cnt; a.cnt_off = rows_off; a.cnt_cap = cap; a.m_from_cnt = 1;
+  a.rows = rows; a.rows_off = rows_off; a.ids = ids;
+  a.pm = pm; a.ps = ps; a.pu = pu; a.ldp = ldp; a.zy = zy;
+  mf::k_gemm<mf::EPI_STATS><<<grid_for(cap, V), mf::NT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+// Backward recompute of one chunk of compacted rows [c0, c0 + Tc): dZ (bf16)
+// into dz [Tc, ldz] and dzt [Vpad, Tc].
+hipError_t mfma_dz(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
+                   const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
+                   const int32_t* cnt, int64_t c0, int64_t Tc, uint16_t* dz, uint16_t* dzt,
+                   hipStream_t s) {
+  mf::Args a = {};
+  a.A = Hc + c0 * d; a.lda = d;
+  a.B = W; a.ldb = d;
+  a.M = (int)Tc; a.N = (int)Vpad; a.K = (int)d;
+  a.cnt = cnt; a.cnt_off = c0; a.cnt_cap = Tc; a.m_from_cnt = 1;
+  a.rows = rows; a.rows_off = c0; a.ids = ids; a.lse = lse; a.cgrad = cgrad;
+  a.dz = dz; a.ldz = Vpad; a.dzt = dzt; a.ldzt = Tc; a.Vvalid = V;
+  a.NB = (int)V;  // W has V rows; columns V..Vpad-1 of dZ are written as 0
+  // dz rows are indexed by the chunk-local m (m0 + row), dzt columns likewise
+  mf::k_gemm<mf::EPI_DZ><<<grid_for(Tc, Vpad), mf::NT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+// C[M, N] (+)= A[M, K] . B[N, K]^T with fp32 output; optional row scatter of C
+// through rows[rows_off + m]; M or K can come from the device counter.
+hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
+                           int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
+                           int64_t cnt_cap, int m_from_cnt, int k_from_cnt, float* C, int64_t ldc,
+                           const int32_t* rows, int64_t rows_off, int accumulate, hipStream_t s) {
+  mf::Args a = {};
+  a.A = A; a.lda = lda; a.B = B; a.ldb = ldb;
+  a.M = (int)M; a.N = (int)N; a.K = (int)K;
+  a.cnt = cnt; a.cnt_off = cnt_off; a.cnt_cap = cnt_cap; a.m_from_cnt = m_from_cnt;
+  a.k_from_cnt = k_from_cnt;
+  a.C = C; a.ldc = ldc; a.rows = rows; a.rows_off = rows_off; a.c_scatter = rows != nullptr;
+  a.accumulate = accumulate;
+  mf::k_gemm<mf::EPI_STORE><<<grid_for(M, N), mf::NT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace rft

@@ -1,0 +1,459 @@
+// C ABI of librft: argument validation, workspace layout and the launch
+// sequence of every entry point declared in rft.h.  Every call enqueues on the
+// caller's stream and returns without synchronising.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <cmath>
+#include <limits>
+#include <string>
+
+#include "rft_internal.h"
+
+using namespace rft;
+
+namespace {
+
+thread_local std::string g_err;
+
+rft_status fail(rft_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+rft_status hip_fail(hipError_t e, const char* where) {
+  return fail(RFT_E_HIP, "%s: HIP error %d (%s)", where, (int)e, hipGetErrorString(e));
+}
+
+#define RFT_HIP(call, where)                        \
+  do {                                              \
+    hipError_t e_ = (call);                         \
+    if (e_ != hipSuccess) return hip_fail(e_, where); \
+  } while (0)
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+rft_status check_tokens(const rft_tokens* tok, const char* fn) {
+  if (!tok) return fail(RFT_E_NULL, "%s: tokens is NULL", fn);
+  if (tok->T < 0 || tok->n_seq < 0)
+    return fail(RFT_E_SHAPE, "%s: T=%lld n_seq=%lld must be >= 0", fn, (long long)tok->T,
+                (long long)tok->n_seq);
+  if (tok->T > (int64_t)std::numeric_limits<int32_t>::max() / 2)
+    return fail(RFT_E_SHAPE, "%s: T=%lld exceeds the supported 2^30 rows", fn, (long long)tok->T);
+  if (tok->n_seq == 0 && tok->T != 0)
+    return fail(RFT_E_SHAPE, "%s: T=%lld rows but n_seq = 0", fn, (long long)tok->T);
+  if (!tok->seq_start) return fail(RFT_E_NULL, "%s: tokens.seq_start is NULL", fn);
+  if (tok->T > 0 && (!tok->mask || !tok->token_ids))
+    return fail(RFT_E_NULL, "%s: tokens.mask / tokens.token_ids is NULL", fn);
+  return RFT_OK;
+}
+
+rft_status check_hw(const char* fn, int64_t T, const void* hidden, const void* weight, int dtype,
+                    int64_t d, int64_t V) {
+  if (dtype != RFT_F32 && dtype != RFT_BF16) return fail(RFT_E_DTYPE, "%s: dtype %d unknown", fn, dtype);
+  if (d < 1 || V < 1) return fail(RFT_E_SHAPE, "%s: d=%lld V=%lld must be >= 1", fn, (long long)d, (long long)V);
+  if (V > (int64_t)std::numeric_limits<int32_t>::max() / 2 || d > (1 << 20))
+    return fail(RFT_E_SHAPE, "%s: d=%lld V=%lld too large", fn, (long long)d, (long long)V);
+  if (!weight || (T > 0 && !hidden)) return fail(RFT_E_NULL, "%s: hidden / weight is NULL", fn);
+  if (dtype == RFT_BF16) {
+    if (d % 8) return fail(RFT_E_SHAPE, "%s: bf16 needs d %% 8 == 0 (d=%lld)", fn, (long long)d);
+    if ((hidden && !aligned16(hidden)) || !aligned16(weight))
+      return fail(RFT_E_SHAPE, "%s: bf16 hidden / weight must be 16-byte aligned", fn);
+  }
+  return RFT_OK;
+}
+
+rft_status check_params(const rft_ppo_params* p, const char* fn) {
+  if (!p) return fail(RFT_E_NULL, "%s: params is NULL", fn);
+  if (!(p->eps_low >= 0.f && p->eps_low <= 1.f))
+    return fail(RFT_E_PARAM, "%s: eps_low=%g must be in [0, 1]", fn, (double)p->eps_low);
+  if (!(p->eps_high >= 0.f)) return fail(RFT_E_PARAM, "%s: eps_high=%g must be >= 0", fn, (double)p->eps_high);
+  if (!(p->kl_coef >= 0.f) || !std::isfinite(p->kl_coef))
+    return fail(RFT_E_PARAM, "%s: kl_coef=%g must be finite and >= 0", fn, (double)p->kl_coef);
+  if (p->agg != RFT_AGG_SEQ_MEAN_TOKEN_MEAN && p->agg != RFT_AGG_TOKEN_MEAN)
+    return fail(RFT_E_PARAM, "%s: agg=%d unknown", fn, p->agg);
+  if (!(p->denom_override >= 0.0) || !std::isfinite(p->denom_override))
+    return fail(RFT_E_PARAM, "%s: denom_override=%g must be finite and >= 0", fn, p->denom_override);
+  return RFT_OK;
+}
+
+LossConst loss_const(const rft_ppo_params* p, int64_t V) {
+  LossConst c;
+  c.eps_low = p->eps_low;
+  c.eps_high = p->eps_high;
+  c.beta = p->kl_coef;
+  c.agg = p->agg;
+  c.denom = p->denom_override;
+  c.V = V;
+  c.thr_lo = p->eps_low < 1.f ? (float)std::log(1.0 - (double)p->eps_low)
+                              : -std::numeric_limits<float>::infinity();
+  c.thr_hi = std::isfinite(p->eps_high) ? (float)std::log1p((double)p->eps_high)
+                                        : std::numeric_limits<float>::infinity();
+  return c;
+}
+
+rft_status check_ws(const char* fn, void* ws, size_t have, size_t need) {
+  if (need == 0) return RFT_OK;
+  if (!ws) return fail(RFT_E_WORKSPACE, "%s: workspace is NULL (%zu bytes needed)", fn, need);
+  if (!aligned16(ws)) return fail(RFT_E_WORKSPACE, "%s: workspace must be 16-byte aligned", fn);
+  if (have < need) return fail(RFT_E_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, have, need);
+  return RFT_OK;
+}
+
+// ---------------------------------------------------- workspace layouts --
+struct FwdWs {
+  TokMeta m;
+  uint16_t* hc;  // compacted hidden rows (bf16 path)
+  float *pm, *ps, *pu, *zy;
+  int ntiles;
+  int64_t ldp;
+  size_t bytes;
+};
+FwdWs carve_fwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dtype) {
+  Carver c(base);
+  FwdWs w;
+  w.m = carve_tokmeta(c, tok.T, tok.n_seq);
+  w.hc = dtype == RFT_BF16 ? c.take<uint16_t>((size_t)(tok.T > 0 ? tok.T : 1) * d) : nullptr;
+  int tn = dtype == RFT_BF16 ? kMfmaTileN : kSimtTileN;
+  w.ntiles = (int)((V + tn - 1) / tn);
+  w.ldp = tok.T > 0 ? tok.T : 1;
+  w.pm = c.take<float>((size_t)w.ntiles * w.ldp);
+  w.ps = c.take<float>((size_t)w.ntiles * w.ldp);
+  w.pu = c.take<float>((size_t)w.ntiles * w.ldp);
+  w.zy = c.take<float>((size_t)w.ldp);
+  w.bytes = c.bytes();
+  return w;
+}
+
+struct LossWs {
+  TokMeta m;
+  LossPartial* parts;
+  size_t bytes;
+};
+LossWs carve_loss(void* base, const rft_tokens& tok, bool per_row) {
+  Carver c(base);
+  LossWs w;
+  w.m = carve_tokmeta(c, tok.T, tok.n_seq);
+  int64_t np = per_row ? tok.T : (tok.T + 255) / 256;
+  w.parts = c.take<LossPartial>(np > 0 ? np : 1);
+  w.bytes = c.bytes();
+  return w;
+}
+
+struct BwdWs {
+  TokMeta m;
+  uint16_t *hc, *wt, *dz, *dzt, *ht;  // bf16 path
+  float* dz32;                   // fp32 path
+  int64_t Tc, Vpad;
+  size_t bytes;
+};
+constexpr int64_t kBf16Align = 256;   // row chunk / vocabulary padding of the bf16 path
+constexpr int64_t kF32Align = 64;
+constexpr int64_t kRecommendTc = 32768;
+
+BwdWs carve_bwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dtype, int64_t Tc) {
+  Carver c(base);
+  BwdWs w = {};
+  w.m = carve_tokmeta(c, tok.T, tok.n_seq);
+  w.Tc = Tc;
+  if (dtype == RFT_BF16) {
+    w.Vpad = round_up(V, kBf16Align);
+    w.hc = c.take<uint16_t>((size_t)(tok.T > 0 ? tok.T : 1) * d);
+    w.wt = c.take<uint16_t>((size_t)d * w.Vpad);
+    w.dz = c.take<uint16_t>((size_t)Tc * w.Vpad);
+    w.dzt = c.take<uint16_t>((size_t)w.Vpad * Tc);
+    w.ht = c.take<uint16_t>((size_t)d * Tc);
+  } else {
+    w.Vpad = round_up(V, kF32Align);
+    w.dz32 = c.take<float>((size_t)Tc * w.Vpad);
+  }
+  w.bytes = c.bytes();
+  return w;
+}
+
+int64_t bwd_align(int dtype) { return dtype == RFT_BF16 ? kBf16Align : kF32Align; }
+
+int64_t bwd_tc_max(const rft_tokens& tok, int dtype) {
+  int64_t a = bwd_align(dtype);
+  int64_t t = round_up(tok.T > 0 ? tok.T : 1, a);
+  return t;
+}
+
+// largest row chunk (a multiple of the alignment) whose workspace fits, 0 if none
+int64_t bwd_tc_for(const rft_tokens& tok, int64_t d, int64_t V, int dtype, size_t ws_bytes) {
+  int64_t a = bwd_align(dtype);
+  int64_t kmax = bwd_tc_max(tok, dtype) / a;
+  if (carve_bwd(nullptr, tok, d, V, dtype, a).bytes > ws_bytes) return 0;
+  int64_t lo = 1, hi = kmax;  // invariant: chunk lo*a fits
+  while (lo < hi) {
+    int64_t mid = (lo + hi + 1) / 2;
+    if (carve_bwd(nullptr, tok, d, V, dtype, mid * a).bytes <= ws_bytes) lo = mid; else hi = mid - 1;
+  }
+  return lo * a;
+}
+
+}  // namespace
+
+// ================================================================== ABI ==
+extern "C" {
+
+int rft_abi_version(void) { return RFT_ABI_VERSION; }
+
+const char* rft_status_str(int s) {
+  switch (s) {
+    case RFT_OK: return "ok";
+    case RFT_E_NULL: return "null pointer";
+    case RFT_E_SHAPE: return "invalid shape";
+    case RFT_E_DTYPE: return "invalid dtype";
+    case RFT_E_PARAM: return "invalid parameter";
+    case RFT_E_WORKSPACE: return "workspace too small";
+    case RFT_E_UNSUPPORTED: return "unsupported";
+    case RFT_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* rft_last_error(void) { return g_err.c_str(); }
+
+size_t rft_workspace_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype) {
+  if (!tok || tok->T < 0 || tok->n_seq < 0 || V < 1) return 0;
+  switch (op) {
+    case RFT_OP_TOKEN_LOGPROBS:
+      if (dtype != RFT_F32 && dtype != RFT_BF16) return 0;
+      return carve_fwd(nullptr, *tok, d, V, dtype).bytes;
+    case RFT_OP_TOKEN_LOGPROBS_FROM_LOGITS:
+    case RFT_OP_PPO_BWD_LOGITS:
+      return 0;
+    case RFT_OP_PPO_FWD:
+      return carve_loss(nullptr, *tok, false).bytes;
+    case RFT_OP_PPO_FUSED_LOGITS:
+      return carve_loss(nullptr, *tok, true).bytes;
+    case RFT_OP_PPO_BWD: {
+      if ((dtype != RFT_F32 && dtype != RFT_BF16) || d < 1) return 0;
+      int64_t tc = bwd_tc_max(*tok, dtype);
+      if (tc > kRecommendTc) tc = kRecommendTc;
+      return carve_bwd(nullptr, *tok, d, V, dtype, tc).bytes;
+    }
+    default:
+      return 0;
+  }
+}
+
+size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype) {
+  if (op == RFT_OP_PPO_BWD) {
+    if (!tok || tok->T < 0 || tok->n_seq < 0 || V < 1 || d < 1) return 0;
+    if (dtype != RFT_F32 && dtype != RFT_BF16) return 0;
+    return carve_bwd(nullptr, *tok, d, V, dtype, bwd_align(dtype)).bytes;
+  }
+  return rft_workspace_bytes(op, tok, d, V, dtype);
+}
+
+rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t group_size,
+                                float eps, float* adv, void* stream) {
+  const char* fn = "rft_group_advantages";
+  if (n_groups < 0 || group_size < 1)
+    return fail(RFT_E_SHAPE, "%s: n_groups=%lld group_size=%d", fn, (long long)n_groups, group_size);
+  if (n_groups > 0 && (!rewards || !adv)) return fail(RFT_E_NULL, "%s: rewards / adv is NULL", fn);
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(RFT_E_PARAM, "%s: eps=%g", fn, (double)eps);
+  if (n_groups > 0 && rewards == adv) return fail(RFT_E_PARAM, "%s: adv may not alias rewards", fn);
+  RFT_HIP(launch_group_adv(rewards, n_groups, group_size, eps, adv, (hipStream_t)stream), fn);
+  return RFT_OK;
+}
+
+rft_status rft_token_logprobs(const rft_tokens* tok, const void* hidden, const void* weight,
+                              int dtype, int64_t d, int64_t V, float* logp, float* entropy,
+                              float* lse, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "rft_token_logprobs";
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if ((st = check_hw(fn, tok->T, hidden, weight, dtype, d, V))) return st;
+  if (tok->T > 0 && (!logp || !lse)) return fail(RFT_E_NULL, "%s: logp / lse is NULL", fn);
+  FwdWs w = carve_fwd(nullptr, *tok, d, V, dtype);
+  if ((st = check_ws(fn, ws, ws_bytes, w.bytes))) return st;
+  w = carve_fwd(ws, *tok, d, V, dtype);
+  hipStream_t s = (hipStream_t)stream;
+  if (tok->T == 0) return RFT_OK;
+  RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
+  if (dtype == RFT_BF16) {
+    RFT_HIP(launch_gather_rows16((const uint16_t*)hidden, d, w.m.rows, w.m.meta, tok->T, w.hc, s),
+            fn);
+    RFT_HIP(mfma_fwd_stats(w.hc, d, (const uint16_t*)weight, V, w.m.rows,
+                           tok->token_ids, w.m.meta, 0, tok->T, w.pm, w.ps, w.pu, w.ldp, w.zy, s),
+            fn);
+  } else {
+    RFT_HIP(simt_fwd_stats((const float*)hidden, d, (const float*)weight, V, w.m.rows,
+                           tok->token_ids, w.m.meta, tok->T, w.pm, w.ps, w.pu, w.ldp, w.zy, s),
+            fn);
+  }
+  RFT_HIP(launch_merge_rows(*tok, w.m, V, w.pm, w.ps, w.pu, w.ntiles, w.ldp, w.zy, logp, entropy,
+                            lse, s),
+          fn);
+  return RFT_OK;
+}
+
+rft_status rft_token_logprobs_from_logits(const rft_tokens* tok, const float* logits, int64_t V,
+                                          float* logp, float* entropy, float* lse,
+                                          float* gathered, void* ws, size_t ws_bytes,
+                                          void* stream) {
+  const char* fn = "rft_token_logprobs_from_logits";
+  (void)ws;
+  (void)ws_bytes;
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if (V < 1 || V > (int64_t)std::numeric_limits<int32_t>::max() / 2)
+    return fail(RFT_E_SHAPE, "%s: V=%lld", fn, (long long)V);
+  if (tok->T > 0 && (!logits || !logp || !lse)) return fail(RFT_E_NULL, "%s: logits / logp / lse is NULL", fn);
+  RFT_HIP(launch_logits_stats(logits, *tok, V, logp, entropy, lse, gathered, (hipStream_t)stream), fn);
+  return RFT_OK;
+}
+
+rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* logp,
+                                 const float* old_logp, const float* ref_logp, const float* adv,
+                                 const float* entropy, const rft_ppo_params* params,
+                                 float* grad_logp, rft_ppo_stats* stats, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  const char* fn = "rft_ppo_clip_loss_fwd";
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if ((st = check_params(params, fn))) return st;
+  if (V < 1) return fail(RFT_E_SHAPE, "%s: V=%lld", fn, (long long)V);
+  if (!stats) return fail(RFT_E_NULL, "%s: stats is NULL", fn);
+  if (tok->T > 0 && (!logp || !old_logp || !adv || !grad_logp))
+    return fail(RFT_E_NULL, "%s: logp / old_logp / adv / grad_logp is NULL", fn);
+  if (tok->T > 0 && params->kl_coef > 0.f && !ref_logp)
+    return fail(RFT_E_NULL, "%s: ref_logp is NULL with kl_coef > 0", fn);
+  LossWs w = carve_loss(nullptr, *tok, false);
+  if ((st = check_ws(fn, ws, ws_bytes, w.bytes))) return st;
+  w = carve_loss(ws, *tok, false);
+  hipStream_t s = (hipStream_t)stream;
+  RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
+  LossConst c = loss_const(params, V);
+  RFT_HIP(launch_loss_fwd(*tok, w.m, logp, old_logp, params->kl_coef > 0.f ? ref_logp : nullptr,
+                          adv, entropy, c, grad_logp, w.parts, stats, s),
+          fn);
+  return RFT_OK;
+}
+
+rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, const void* weight,
+                                 int dtype, int64_t d, int64_t V, const float* lse,
+                                 const float* grad_logp, float* d_hidden, float* d_weight,
+                                 int32_t accumulate_dw, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "rft_ppo_clip_loss_bwd";
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if ((st = check_hw(fn, tok->T, hidden, weight, dtype, d, V))) return st;
+  if (!d_weight) return fail(RFT_E_NULL, "%s: d_weight is NULL", fn);
+  if (tok->T > 0 && (!lse || !grad_logp || !d_hidden))
+    return fail(RFT_E_NULL, "%s: lse / grad_logp / d_hidden is NULL", fn);
+  size_t need = carve_bwd(nullptr, *tok, d, V, dtype, bwd_align(dtype)).bytes;
+  if ((st = check_ws(fn, ws, ws_bytes, need))) return st;
+  int64_t Tc = bwd_tc_for(*tok, d, V, dtype, ws_bytes);
+  if (Tc <= 0) return fail(RFT_E_WORKSPACE, "%s: workspace too small", fn);
+  BwdWs w = carve_bwd(ws, *tok, d, V, dtype, Tc);
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t T = tok->T;
+  if (T > 0) {
+    RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
+    RFT_HIP(launch_zero_masked_rows(tok->mask, T, d, d_hidden, s), fn);
+  }
+  int64_t nchunks = T > 0 ? (T + Tc - 1) / Tc : 0;
+  const int32_t* cnt = w.m.meta;
+  if (dtype == RFT_BF16) {
+    const uint16_t* H = (const uint16_t*)hidden;
+    const uint16_t* W = (const uint16_t*)weight;
+    if (nchunks > 0) {
+      RFT_HIP(launch_gather_rows16(H, d, w.m.rows, cnt, T, w.hc, s), fn);
+      RFT_HIP(launch_transpose_w(W, V, d, w.wt, w.Vpad, s), fn);
+    }
+    for (int64_t ci = 0; ci < nchunks; ++ci) {
+      int64_t c0 = ci * Tc;
+      RFT_HIP(mfma_dz(w.hc, d, W, V, w.Vpad, w.m.rows, tok->token_ids, lse, grad_logp, cnt, c0, Tc,
+                      w.dz, w.dzt, s),
+              fn);
+      // dH rows of this chunk: dZ [count, Vpad] . Wt[d, Vpad]^T, scattered to token rows
+      RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
+                              d_hidden, d, w.m.rows, c0, 0, s),
+              fn);
+      RFT_HIP(launch_transpose_hc(w.hc, d, cnt, c0, Tc, w.ht, Tc, s), fn);
+      // dW += dZt [V, count] . Ht[d, count]^T
+      RFT_HIP(mfma_gemm_store(w.dzt, Tc, w.ht, Tc, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight, d,
+                              nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s),
+              fn);
+    }
+    if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);
+  } else {
+    const float* H = (const float*)hidden;
+    const float* W = (const float*)weight;
+    for (int64_t ci = 0; ci < nchunks; ++ci) {
+      int64_t c0 = ci * Tc;
+      RFT_HIP(simt_dz(H, d, W, V, w.Vpad, w.m.rows, tok->token_ids, lse, grad_logp, cnt, c0, Tc,
+                      w.dz32, s),
+              fn);
+      // dH[m, j] = sum_v dZ[m, v] W[v, j]
+      RFT_HIP(simt_gemm_store(w.dz32, w.Vpad, 1, W, 1, d, nullptr, 0, Tc, d, V, cnt, c0, Tc, 1, 0,
+                              d_hidden, d, w.m.rows, c0, 0, s),
+              fn);
+      // dW[v, j] = sum_t dZ[t, v] H[rows[c0 + t], j]
+      RFT_HIP(simt_gemm_store(w.dz32, 1, w.Vpad, H, 1, d, w.m.rows, c0, V, d, Tc, cnt, c0, Tc, 0, 1,
+                              d_weight, d, nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s),
+              fn);
+    }
+    if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);
+  }
+  return RFT_OK;
+}
+
+rft_status rft_ppo_clip_loss_bwd_logits(const rft_tokens* tok, const float* logits, int64_t V,
+                                        const float* lse, const float* grad_logp,
+                                        float* d_logits, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "rft_ppo_clip_loss_bwd_logits";
+  (void)ws;
+  (void)ws_bytes;
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if (V < 1 || V > (int64_t)std::numeric_limits<int32_t>::max() / 2)
+    return fail(RFT_E_SHAPE, "%s: V=%lld", fn, (long long)V);
+  if (tok->T > 0 && (!logits || !lse || !grad_logp || !d_logits))
+    return fail(RFT_E_NULL, "%s: logits / lse / grad_logp / d_logits is NULL", fn);
+  RFT_HIP(launch_logits_bwd(logits, *tok, V, lse, grad_logp, d_logits, (hipStream_t)stream), fn);
+  return RFT_OK;
+}
+
+rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits, int64_t V,
+                                     const float* old_logp, const float* ref_logp,
+                                     const float* adv, const rft_ppo_params* params, float* logp,
+                                     float* entropy, float* lse, float* grad_logp,
+                                     float* d_logits, rft_ppo_stats* stats, void* ws,
+                                     size_t ws_bytes, void* stream) {
+  const char* fn = "rft_ppo_clip_fused_logits";
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if ((st = check_params(params, fn))) return st;
+  if (V < 1 || V > (int64_t)std::numeric_limits<int32_t>::max() / 2)
+    return fail(RFT_E_SHAPE, "%s: V=%lld", fn, (long long)V);
+  if (!stats) return fail(RFT_E_NULL, "%s: stats is NULL", fn);
+  if (tok->T > 0 && (!logits || !old_logp || !adv || !logp || !d_logits))
+    return fail(RFT_E_NULL, "%s: logits / old_logp / adv / logp / d_logits is NULL", fn);
+  if (tok->T > 0 && params->kl_coef > 0.f && !ref_logp)
+    return fail(RFT_E_NULL, "%s: ref_logp is NULL with kl_coef > 0", fn);
+  LossWs w = carve_loss(nullptr, *tok, true);
+  if ((st = check_ws(fn, ws, ws_bytes, w.bytes))) return st;
+  w = carve_loss(ws, *tok, true);
+  hipStream_t s = (hipStream_t)stream;
+  RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
+  LossConst c = loss_const(params, V);
+  RFT_HIP(launch_logits_fused(logits, *tok, w.m, V, old_logp,
+                              params->kl_coef > 0.f ? ref_logp : nullptr, adv, c, logp, entropy,
+                              lse, grad_logp, d_logits, w.parts, stats, s),
+          fn);
+  return RFT_OK;
+}
+
+}  // extern "C"

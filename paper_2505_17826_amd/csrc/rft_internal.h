@@ -1,0 +1,239 @@
+// Internal declarations shared by the HIP sources of librft (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <math.h>
+
+#include "rft.h"
+
+namespace rft {
+
+// ------------------------------------------------------------------ types --
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+// Round-to-nearest-even float -> bf16 bits (NaN stays a quiet NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// ------------------------------------------------------- wave reductions --
+// Butterfly reductions over the 32 lanes of each half-wave (lanes 0-31 and
+// 32-63 reduce separately) with DPP moves and one swizzle; every lane of the
+// half ends with the result.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float swz16_f(float v) {  // lane ^ 16 within 32
+  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F));
+}
+__device__ __forceinline__ float half_max(float v) {
+  v = fmaxf(v, dpp_f<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_f<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_f<0x141>(v));  // row_half_mirror
+  v = fmaxf(v, dpp_f<0x140>(v));  // row_mirror
+  v = fmaxf(v, swz16_f(v));
+  return v;
+}
+__device__ __forceinline__ float half_sum(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  v += swz16_f(v);
+  return v;
+}
+
+// Whole-wave (64 lanes) reductions via cross-lane shuffles.
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_sum_f(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max_f(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_min_f(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ long long wave_sum_ll(long long v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Merge of two online log-sum-exp partials (m: max, s: sum exp(z - m),
+// u: sum exp(z - m) z).  A partial with s == 0 is empty.
+__device__ __forceinline__ void lse_merge(float& m, float& s, float& u, float m2, float s2,
+                                          float u2) {
+  if (s2 == 0.f) return;
+  if (s == 0.f) { m = m2; s = s2; u = u2; return; }
+  float M = fmaxf(m, m2);
+  float a = exp2f((m - M) * kLog2e), b = exp2f((m2 - M) * kLog2e);
+  s = s * a + s2 * b;
+  u = u * a + u2 * b;
+  m = M;
+}
+
+// ----------------------------------------------------- token bookkeeping --
+// Compacted view of the masked rows, built on the device by the first kernels
+// of every call (the workspace holds it).
+struct TokMeta {
+  int32_t* rows;     // [T]  k-th valid row (k < N)
+  int32_t* row_seq;  // [T]  rollout of the k-th valid row
+  int32_t* kidx;     // [T]  compacted index of row t, -1 if masked
+  int32_t* n_i;      // [n_seq] valid tokens per rollout
+  int32_t* blk;      // [nblk] per-block counts, then offsets
+  int32_t* meta;     // [4]  N, S
+};
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base((char*)b) {}
+  template <class T>
+  T* take(size_t count) {
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? (T*)(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+  size_t bytes() const { return (off + 255) & ~size_t(255); }
+};
+
+constexpr int kK0Rows = 2048;  // rows per block of the compaction kernels
+
+TokMeta carve_tokmeta(Carver& c, int64_t T, int64_t n_seq);
+hipError_t launch_tokmeta(const rft_tokens& tok, const TokMeta& m, hipStream_t s);
+
+// ------------------------------------------------------------------ loss --
+struct LossConst {
+  float thr_lo, thr_hi;   // fp32 log(1 - eps_low), log(1 + eps_high)
+  float eps_low, eps_high, beta;
+  int agg;
+  double denom;           // 0 = use S or N
+  int64_t V;
+};
+
+// Per-token PPO-clip + k3 KL terms.  Returns false for an out-of-range id.
+struct TokLoss {
+  double w;     // aggregation weight
+  float pg, kl, rho, g;
+  bool clipped;
+};
+
+__device__ __forceinline__ TokLoss token_loss(float lp, float old, float ref, float A, int n_seq_i,
+                                              int N, int S, const LossConst& c) {
+  TokLoss r;
+  double den;
+  if (c.agg == RFT_AGG_SEQ_MEAN_TOKEN_MEAN) {
+    double Sd = c.denom > 0 ? c.denom : (double)S;
+    den = Sd * (double)n_seq_i;
+  } else {
+    den = c.denom > 0 ? c.denom : (double)N;
+  }
+  r.w = den > 0 ? 1.0 / den : 0.0;
+  float delta = lp - old;
+  r.rho = expf(delta);
+  float lo = 1.f - c.eps_low, hi = 1.f + c.eps_high;
+  float rb = fminf(fmaxf(r.rho, lo), hi);
+  r.pg = fmaxf(-A * r.rho, -A * rb);
+  r.clipped = (A > 0.f && delta > c.thr_hi) || (A < 0.f && delta < c.thr_lo);
+  float dk = ref - lp;
+  float em1 = expm1f(dk);
+  r.kl = em1 - dk;
+  r.g = (r.clipped ? 0.f : -A * r.rho) - c.beta * em1;
+  return r;
+}
+
+// Partial sums of one block of tokens, reduced in a fixed order.
+struct LossPartial {
+  double loss, pg, klw, kl, ent, ratio;
+  long long clipped, bad;
+};
+
+hipError_t launch_loss_final(const LossPartial* parts, int nparts, const int32_t* meta,
+                             rft_ppo_stats* stats, hipStream_t s);
+
+// ------------------------------------------------------------ launchers --
+hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, float* adv,
+                            hipStream_t s);
+hipError_t launch_loss_fwd(const rft_tokens& tok, const TokMeta& m, const float* logp,
+                           const float* old, const float* ref, const float* adv, const float* ent,
+                           const LossConst& c, float* grad, LossPartial* parts, rft_ppo_stats* st,
+                           hipStream_t s);
+hipError_t launch_merge_rows(const rft_tokens& tok, const TokMeta& m, int64_t V, const float* pm,
+                             const float* ps, const float* pu, int ntiles, int64_t ld,
+                             const float* zy, float* logp, float* ent, float* lse, hipStream_t s);
+hipError_t mfma_fwd_stats(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V,
+                          const int32_t* rows, const int32_t* ids, const int32_t* cnt,
+                          int64_t rows_off, int64_t cap, float* pm, float* ps, float* pu,
+                          int64_t ldp, float* zy, hipStream_t s);
+hipError_t mfma_dz(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
+                   const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
+                   const int32_t* cnt, int64_t c0, int64_t Tc, uint16_t* dz, uint16_t* dzt,
+                   hipStream_t s);
+hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
+                           int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
+                           int64_t cnt_cap, int m_from_cnt, int k_from_cnt, float* C, int64_t ldc,
+                           const int32_t* rows, int64_t rows_off, int accumulate, hipStream_t s);
+hipError_t simt_fwd_stats(const float* H, int64_t d, const float* W, int64_t V, const int32_t* rows,
+                          const int32_t* ids, const int32_t* cnt, int64_t cap, float* pm, float* ps,
+                          float* pu, int64_t ldp, float* zy, hipStream_t s);
+hipError_t simt_dz(const float* H, int64_t d, const float* W, int64_t V, int64_t Vpad,
+                   const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
+                   const int32_t* cnt, int64_t c0, int64_t Tc, float* dz, hipStream_t s);
+hipError_t simt_gemm_store(const float* A, int64_t sam, int64_t sak, const float* B, int64_t sbn,
+                           int64_t sbk, const int32_t* b_map, int64_t b_koff, int64_t M, int64_t N,
+                           int64_t K, const int32_t* cnt, int64_t cnt_off, int64_t cnt_cap,
+                           int m_from_cnt, int k_from_cnt, float* C, int64_t ldc,
+                           const int32_t* rows, int64_t rows_off, int accumulate, hipStream_t s);
+hipError_t launch_transpose_w(const uint16_t* W, int64_t V, int64_t d, uint16_t* Wt, int64_t ldt,
+                              hipStream_t s);
+hipError_t launch_gather_rows16(const uint16_t* H, int64_t d, const int32_t* rows,
+                                const int32_t* cnt, int64_t cap, uint16_t* Hc, hipStream_t s);
+hipError_t launch_transpose_hc(const uint16_t* Hc, int64_t d, const int32_t* cnt, int64_t c0,
+                               int64_t Tc, uint16_t* Ht, int64_t ldt, hipStream_t s);
+hipError_t launch_fill_zero(float* out, int64_t n, hipStream_t s);
+hipError_t launch_zero_masked_rows(const uint8_t* mask, int64_t T, int64_t width, float* out,
+                                   hipStream_t s);
+hipError_t launch_logits_stats(const float* logits, const rft_tokens& tok, int64_t V, float* logp,
+                               float* ent, float* lse, float* gathered, hipStream_t s);
+hipError_t launch_logits_bwd(const float* logits, const rft_tokens& tok, int64_t V,
+                             const float* lse, const float* grad, float* dl, hipStream_t s);
+hipError_t launch_logits_fused(const float* logits, const rft_tokens& tok, const TokMeta& m,
+                               int64_t V, const float* old, const float* ref, const float* adv,
+                               const LossConst& c, float* logp, float* ent, float* lse,
+                               float* grad, float* dl, LossPartial* parts, rft_ppo_stats* st,
+                               hipStream_t s);
+
+constexpr int kMfmaTileN = 256;  // vocabulary columns per forward tile (bf16 path)
+constexpr int kSimtTileN = 64;   // (fp32 path)
+
+}  // namespace rft

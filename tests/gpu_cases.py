@@ -1,0 +1,114 @@
+"""Shared helpers of the GPU parity tests: run the HIP path through the C ABI
+binding and the float64 oracle on the same seeded inputs."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2505_17826_amd as R
+from gen import synth
+from oracle import rft_oracle as O
+
+requires_gpu = pytest.mark.skipif(not torch.cuda.is_available(), reason="needs an MI355X")
+
+# tolerances (spec bars, plus the derived ones)
+TOL_LOGP = 2e-3          # absolute, log-probs (also entropy and lse)
+TOL_LOSS_REL = 1e-3      # relative, loss ...
+TOL_LOSS_ABS = 1e-6      # ... with an absolute floor (zero-mean advantages cancel)
+TOL_GRAD_FRO = 2e-2      # relative Frobenius, dH / dW / dlogits
+TOL_ADV = 1e-5           # absolute, advantages
+
+
+def f32(x):
+    return float(np.float32(x))
+
+
+def rel_fro(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    nb = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)
+
+
+def cpu(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def tokens_of(b: synth.Batch) -> R.Tokens:
+    dev = torch.device("cuda")
+    return R.Tokens(b.seq_start.to(dev).contiguous(), b.mask.to(dev).contiguous(),
+                    b.ids.to(dev).contiguous())
+
+
+def params_of(cfg: synth.Config, denom=0.0, agg=None) -> R.rft_ppo_params:
+    return R.ppo_params(cfg.eps_low, cfg.eps_high, cfg.beta, cfg.agg if agg is None else agg, denom)
+
+
+def oracle_eps(cfg):
+    """The float32 values the library receives, as the oracle's fp64 inputs."""
+    return f32(cfg.eps_low), f32(cfg.eps_high), f32(cfg.beta)
+
+
+def perturbed_logprobs(logp_fp64, batch: synth.Batch):
+    """Old / reference log-probs = given log-probs + the batch's noise, as fp32."""
+    m = batch.mask.cpu().numpy() != 0
+    old = np.where(m, logp_fp64 + batch.old_noise.cpu().numpy(), 0.0).astype(np.float32)
+    ref = np.where(m, logp_fp64 + batch.ref_noise.cpu().numpy(), 0.0).astype(np.float32)
+    return old, ref
+
+
+def gpu_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bwd_bytes=None):
+    """adv -> log-probs -> loss -> backward through the binding; CPU results."""
+    dev = torch.device("cuda")
+    cfg = b.cfg
+    tok = tokens_of(b)
+    H, W = b.H.to(dev).contiguous(), b.W.to(dev).contiguous()
+    adv = R.rft_group_advantages(b.rewards.to(dev), cfg.group)
+    logp, ent, lse = R.rft_token_logprobs(tok, H, W)
+    old = torch.from_numpy(old32).to(dev)
+    ref = torch.from_numpy(ref32).to(dev)
+    grad, st = R.rft_ppo_clip_loss_fwd(tok, cfg.V, logp, old, ref, adv, params_of(cfg, denom),
+                                       entropy=ent)
+    ws = None
+    if ws_bwd_bytes is not None:
+        ws = torch.empty(ws_bwd_bytes, dtype=torch.uint8, device=dev)
+    dH, dW = R.rft_ppo_clip_loss_bwd(tok, H, W, lse, grad, ws=ws)
+    torch.cuda.synchronize()
+    return {"adv": cpu(adv), "logp": cpu(logp), "entropy": cpu(ent), "lse": cpu(lse),
+            "grad_logp": cpu(grad), "stats": R.stats_to_dict(st), "dH": cpu(dH), "dW": cpu(dW)}
+
+
+def oracle_step(b: synth.Batch, old32, ref32, denom=0.0):
+    cfg = b.cfg
+    el, eh, be = oracle_eps(cfg)
+    return O.trainer_step(b.H, b.W, b.ids, b.mask, b.seq_start, b.rewards, cfg.group,
+                          old32.astype(np.float64), ref32.astype(np.float64), el, eh, be, cfg.agg,
+                          denom)
+
+
+def compare_step(g, o, b: synth.Batch, check_bwd=True):
+    m = b.mask.cpu().numpy() != 0
+    np.testing.assert_allclose(g["adv"], o["adv"], atol=TOL_ADV, rtol=0)
+    for k in ("logp", "entropy", "lse"):
+        assert np.all(g[k][~m] == 0.0), f"{k}: masked rows must be exactly 0"
+        err = np.abs(g[k][m] - o[k][m]).max() if m.any() else 0.0
+        assert err <= TOL_LOGP, f"{k}: max abs err {err}"
+    st, of = g["stats"], o["fwd"]
+    assert st["n_valid"] == of["n_valid"] and st["n_seq_valid"] == of["n_seq_valid"]
+    assert abs(st["loss"] - of["loss"]) <= TOL_LOSS_REL * abs(of["loss"]) + TOL_LOSS_ABS, \
+        (st["loss"], of["loss"])
+    assert np.all(g["grad_logp"][~m] == 0.0)
+    # per-token gradient, leaving out tokens within 1e-4 of a clip bound
+    # (there the two sides may take different, equally valid branches)
+    rows = of["weights_rows"]
+    keep = of["margin"] >= 1e-4
+    gr, orr = g["grad_logp"][rows][keep], of["grad_logp"][rows][keep]
+    scale = np.abs(orr).max() if orr.size else 0.0
+    bad = np.abs(gr - orr) > 1e-3 * np.abs(orr) + 1e-7 * scale
+    assert not bad.any(), f"grad_logp: {bad.sum()} tokens off"
+    assert abs(st["n_clipped"] - of["n_clipped"]) <= int((~keep).sum())
+    if check_bwd:
+        assert np.all(g["dH"][~m] == 0.0), "dH masked rows must be exactly 0"
+        assert rel_fro(g["dH"], o["dH"]) <= TOL_GRAD_FRO, rel_fro(g["dH"], o["dH"])
+        assert rel_fro(g["dW"], o["dW"]) <= TOL_GRAD_FRO, rel_fro(g["dW"], o["dW"])

@@ -1,0 +1,134 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every entry point the header declares, and rejects invalid arguments with
+status codes before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import paper_2505_17826_amd as R
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rft.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(rft_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = R.lib()
+    names = _declared()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(R._SIGS), "binding signatures must cover the header exactly"
+
+
+def test_version_and_status_strings():
+    L = R.lib()
+    assert L.rft_abi_version() == 1
+    for s in range(8):
+        assert L.rft_status_str(s)
+    assert L.rft_status_str(99) == b"unknown status"
+
+
+def _tok(T=8, n_seq=2, null=False):
+    # pointers are never dereferenced on the host; argument checks return first
+    fake = 0 if null else 0x1000
+    return R.rft_tokens(T, n_seq, fake, fake, fake)
+
+
+def test_workspace_sizes_are_consistent():
+    L = R.lib()
+    tk = _tok(T=4096, n_seq=8)
+    a = L.rft_workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, ctypes.byref(tk), 256, 5000, R.RFT_BF16)
+    b = L.rft_workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, ctypes.byref(tk), 256, 10000, R.RFT_BF16)
+    assert 0 < a < b
+    m = L.rft_workspace_min_bytes(R.RFT_OP_PPO_BWD, ctypes.byref(tk), 256, 5000, R.RFT_BF16)
+    r = L.rft_workspace_bytes(R.RFT_OP_PPO_BWD, ctypes.byref(tk), 256, 5000, R.RFT_BF16)
+    assert 0 < m <= r
+    assert L.rft_workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS_FROM_LOGITS, ctypes.byref(tk), 0, 5, 0) == 0
+    assert L.rft_workspace_bytes(R.RFT_OP_PPO_FWD, ctypes.byref(tk), 0, 5, 0) > 0
+    assert L.rft_workspace_bytes(R.RFT_OP_PPO_BWD, ctypes.byref(tk), 256, 5000, 9) == 0
+    assert L.rft_workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, None, 256, 5000, R.RFT_BF16) == 0
+
+
+def test_argument_validation_returns_codes():
+    L = R.lib()
+    s = None
+    fake = ctypes.c_void_p(0x1000)
+    # advantages
+    assert L.rft_group_advantages(fake, -1, 8, 1e-6, fake, s) == R.RFT_E_SHAPE
+    assert L.rft_group_advantages(fake, 4, 0, 1e-6, fake, s) == R.RFT_E_SHAPE
+    assert L.rft_group_advantages(None, 4, 8, 1e-6, fake, s) == R.RFT_E_NULL
+    assert L.rft_group_advantages(fake, 4, 8, -1.0, ctypes.c_void_p(0x2000), s) == R.RFT_E_PARAM
+    assert L.rft_group_advantages(fake, 4, 8, 1e-6, fake, s) == R.RFT_E_PARAM  # aliasing
+    assert b"alias" in L.rft_last_error()
+    # log-probs
+    tk = _tok()
+    args = (fake, fake, R.RFT_BF16, 64, 100, fake, fake, fake, fake, 1 << 30, s)
+    assert L.rft_token_logprobs(None, *args) == R.RFT_E_NULL
+    bad = R.rft_tokens(-1, 2, 0x1000, 0x1000, 0x1000)
+    assert L.rft_token_logprobs(ctypes.byref(bad), *args) == R.RFT_E_SHAPE
+    nos = R.rft_tokens(8, 0, 0x1000, 0x1000, 0x1000)
+    assert L.rft_token_logprobs(ctypes.byref(nos), *args) == R.RFT_E_SHAPE
+    assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, 7, 64, 100, fake, fake, fake, fake,
+                                1 << 30, s) == R.RFT_E_DTYPE
+    assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, R.RFT_BF16, 60, 100, fake, fake,
+                                fake, fake, 1 << 30, s) == R.RFT_E_SHAPE      # d % 8
+    assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 0, fake, fake, fake,
+                                fake, 1 << 30, s) == R.RFT_E_SHAPE
+    assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
+                                fake, fake, 16, s) == R.RFT_E_WORKSPACE
+    assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
+                                fake, None, 1 << 30, s) == R.RFT_E_WORKSPACE
+    assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, None, fake,
+                                fake, fake, 1 << 30, s) == R.RFT_E_NULL
+    # loss parameters
+    P = R.ppo_params
+    base = (ctypes.byref(tk), 100, fake, fake, fake, fake, None)
+    tail = (fake, fake, fake, 1 << 30, s)
+    for p, code in [(P(eps_low=-0.1), R.RFT_E_PARAM), (P(eps_low=1.5), R.RFT_E_PARAM),
+                    (P(eps_high=-1.0), R.RFT_E_PARAM), (P(eps_high=float("nan")), R.RFT_E_PARAM),
+                    (P(kl_coef=-1.0), R.RFT_E_PARAM), (P(kl_coef=float("inf")), R.RFT_E_PARAM),
+                    (P(agg=5), R.RFT_E_PARAM), (P(denom_override=-2.0), R.RFT_E_PARAM)]:
+        assert L.rft_ppo_clip_loss_fwd(*base, ctypes.byref(p), *tail) == code
+    assert L.rft_ppo_clip_loss_fwd(*base, None, *tail) == R.RFT_E_NULL
+    # KL requested without reference log-probs
+    assert L.rft_ppo_clip_loss_fwd(ctypes.byref(tk), 100, fake, fake, None, fake, None,
+                                   ctypes.byref(P(kl_coef=0.1)), *tail) == R.RFT_E_NULL
+    # stats pointer
+    assert L.rft_ppo_clip_loss_fwd(ctypes.byref(tk), 100, fake, fake, fake, fake, None,
+                                   ctypes.byref(P()), fake, None, fake, 1 << 30, s) == R.RFT_E_NULL
+    # backward: workspace below the minimum
+    m = L.rft_workspace_min_bytes(R.RFT_OP_PPO_BWD, ctypes.byref(tk), 64, 100, R.RFT_BF16)
+    assert L.rft_ppo_clip_loss_bwd(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
+                                   fake, fake, 0, fake, m - 1, s) == R.RFT_E_WORKSPACE
+    assert L.rft_ppo_clip_loss_bwd(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
+                                   fake, None, 0, fake, m, s) == R.RFT_E_NULL
+    # logits paths
+    assert L.rft_token_logprobs_from_logits(ctypes.byref(tk), fake, 0, fake, fake, fake, None,
+                                            None, 0, s) == R.RFT_E_SHAPE
+    assert L.rft_ppo_clip_loss_bwd_logits(ctypes.byref(tk), None, 10, fake, fake, fake, None, 0,
+                                          s) == R.RFT_E_NULL
+    assert L.rft_ppo_clip_fused_logits(ctypes.byref(tk), fake, 10, fake, fake, fake,
+                                       ctypes.byref(P(eps_low=2.0)), fake, fake, fake, fake, fake,
+                                       fake, fake, 1 << 30, s) == R.RFT_E_PARAM
+
+
+def test_binding_refuses_cpu_tensors():
+    with pytest.raises(RuntimeError, match="device tensors"):
+        R.rft_group_advantages(torch.zeros(8), 8)
+
+
+def test_header_documents_every_entry_point():
+    src = open(HEADER).read()
+    for n in _declared():
+        # every prototype is preceded by a comment block
+        i = src.rindex(n + "(")
+        assert "*/" in src[max(0, i - 2000):i], n
