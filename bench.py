@@ -76,6 +76,7 @@ def cpu_baseline(batch, target_s, extra):
     if cfg.dtype != "logits":
         extra["W_cpu"] = batch.W.cpu()
     n0 = 32
+    run(n0)                      # warm-up (first touches of the weight)
     t0 = run(n0)
     n = int(min(valid.size, max(n0, n0 * target_s / max(t0, 1e-3))))
     t = run(n) if n > n0 else t0

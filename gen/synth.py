@@ -173,13 +173,15 @@ def _gumbel_argmax(z: torch.Tensor, g: torch.Generator) -> torch.Tensor:
 
 
 def make_batch(cfg: Config, device="cpu", poison: bool = False, seed_key=None,
-               chunk_rows: int = 4096) -> Batch:
+               chunk_rows: int = 4096, layout_only: bool = False) -> Batch:
     """Build the synthetic batch of ``cfg`` on ``device``.
 
     ``seed_key`` (a tuple of ints) selects the random streams; it defaults to
     ``(cfg.cid,)`` so each named workload has one fixed batch.  With
     ``poison=True`` masked rows of H / logits are NaN and their token ids are
-    out of range, which a correct consumer never reads.
+    out of range, which a correct consumer never reads.  ``layout_only=True``
+    skips H, W and logits and draws the token ids uniformly (for kernels that
+    only need the layout, ids, rewards and noise).
     """
     key = tuple(seed_key) if seed_key is not None else (cfg.cid,)
     dev = torch.device(device)
@@ -192,7 +194,11 @@ def make_batch(cfg: Config, device="cpu", poison: bool = False, seed_key=None,
     ids = torch.zeros(T, dtype=torch.int64, device=dev)
     g_samp = _torch_gen(key, "sampling", dev)
     valid_rows = torch.from_numpy(np.nonzero(valid_np)[0]).to(dev)
-    if cfg.dtype in ("f32", "bf16"):
+    if layout_only:
+        u = _np_rng(key, "sampling").integers(0, cfg.V, size=T)
+        ids = torch.from_numpy(u).to(dev)
+        ids[~valid] = 0
+    elif cfg.dtype in ("f32", "bf16"):
         tdt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
         gH = _torch_gen(key, "H", dev)
         H = torch.empty((T, cfg.d), dtype=tdt, device=dev)
