@@ -1,7 +1,8 @@
 // bf16 MFMA "NT" GEMM core for gfx950 with the trainer-step epilogues:
 //   C[m, n] = sum_k A[m, k] * B[n, k]   (both operands K-contiguous, bf16)
-// 256x256 workgroup tile, BK = 64, four wavefronts each owning 128x128 of C
-// as 4x4 v_mfma_f32_32x32x16_bf16 tiles (fp32 accumulators).  Operands go
+// 256x256 workgroup tile, BK = 64, eight wavefronts (two per SIMD, so one
+// wave's LDS and barrier waits overlap the other's MFMAs), each owning 64x128
+// of C as 2x4 v_mfma_f32_32x32x16_bf16 tiles (fp32 accumulators).  Operands go
 // straight from HBM/L2 into LDS with buffer_load_dwordx4 ... lds (no staging
 // registers); the buffer descriptor covers only the tile's valid rows, so rows
 // past the end and the K tail read as zeros without branches.  LDS holds
@@ -24,7 +25,7 @@
 namespace rft {
 namespace mf {
 
-constexpr int BM = 256, BN = 256, BK = 64, NT = 256;
+constexpr int BM = 256, BN = 256, BK = 64, NT = 512;
 constexpr int A_BYTES = BM * BK * 2;
 constexpr int B_BYTES = BN * BK * 2;
 constexpr int STAGE = A_BYTES + B_BYTES;  // 64 KiB
@@ -71,8 +72,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int64
   return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), 0, nr, 0x00020000);
 }
 
-// Stage loader: wave w fills rows [w*64, w*64+64) of the A and B tiles with
-// 8 instructions of 8 rows each.  Lane l writes LDS slot l of an instruction
+// Stage loader: wave w fills rows [w*32, w*32+32) of the A and B tiles with
+// 4 instructions of 8 rows each.  Lane l writes LDS slot l of an instruction
 // (row l/8, physical chunk l%8), so it loads logical chunk (l%8) ^ (row & 7)
 // of its row; chunks at or past K are read from outside the descriptor (0).
 __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB,
@@ -82,7 +83,7 @@ __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_b
   const uint32_t va = kin ? voffA + (uint32_t)k0 * 2u : 0x80000000u;
   const uint32_t vb = kin ? voffB + (uint32_t)k0 * 2u : 0x80000000u;
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
+  for (int p = 0; p < 4; ++p) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_ptr)(dst + p * 1024), 16,
                                              va + (uint32_t)p * strideA8, 0, 0, 0);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES + p * 1024), 16,
@@ -100,12 +101,20 @@ __device__ __forceinline__ void tile_of(int L, int nTm, int nTn, int& mt, int& n
   nt = r / gsz;
 }
 
+// Workgroup barrier without the implicit wait for outstanding loads; the
+// empty asm statements keep the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void barrier_lds() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 template <int EPI>
 __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   __shared__ __attribute__((aligned(16))) char lds[LDS_TOTAL];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wid >> 1, wn = wid & 1;
+  const int wm = wid >> 1, wn = wid & 1;  // 4 x 2 waves, wave tile 64 x 128
 
   int M = g.M, K = g.K;
   if (g.cnt) {
@@ -128,8 +137,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   if ((int)(blockIdx.x >> 3) >= per_xcd || L >= total) return;
   const int nk = (K + BK - 1) / BK;
 
-  // per-lane load geometry (see gload): row w*64 + p*8 + (lane>>3), chunk below
-  const int ld_row = wid * 64 + (lane >> 3);
+  // per-lane load geometry (see load_stage): row w*32 + p*8 + (lane>>3)
+  const int ld_row = wid * 32 + (lane >> 3);
   const int ld_chunk = (lane & 7) ^ ((lane >> 3) & 7);
   const uint32_t voffA = (uint32_t)(ld_row * g.lda * 2 + ld_chunk * 16);
   const uint32_t voffB = (uint32_t)(ld_row * g.ldb * 2 + ld_chunk * 16);
@@ -153,8 +162,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(g.A + (int64_t)m0 * g.lda, rowsA * g.lda * 2);
     const __amdgpu_buffer_rsrc_t rB = make_rsrc(g.B + (int64_t)nb0 * g.ldb, rowsB * g.ldb * 2);
 
-    // per-row epilogue parameters for this tile
-    {
+    // per-row epilogue parameters for this tile (threads 0..255, one row each)
+    if (tid < BM) {
       int m = m0 + tid;
       bool v = m < M;
       if (EPI == EPI_STATS) {
@@ -178,45 +187,44 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       }
     }
 
-    floatx16 acc[4][4];
+    floatx16 acc[2][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
+    char* const ldsw = lds + wid * 32 * 128;
     if (nk > 0)
-      load_stage(rA, rB, lds + wid * 64 * 128, 0, K, ld_chunk, voffA, voffB, strideA8, strideB8);
-    wait_vm();
-    __syncthreads();
+      load_stage(rA, rB, ldsw, 0, K, ld_chunk, voffA, voffB, strideA8, strideB8);
+    __syncthreads();  // first stage and the per-row parameters are visible to every wave
     for (int kt = 0; kt < nk; ++kt) {
       if (kt + 1 < nk)
-        load_stage(rA, rB, lds + ((kt + 1) & 1) * STAGE + wid * 64 * 128, (kt + 1) * BK, K,
-                   ld_chunk, voffA, voffB, strideA8, strideB8);
+        load_stage(rA, rB, ldsw + ((kt + 1) & 1) * STAGE, (kt + 1) * BK, K, ld_chunk, voffA,
+                   voffB, strideA8, strideB8);
       const char* As = lds + (kt & 1) * STAGE;
       const char* Bs = As + A_BYTES;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int ch = ((ks * 2 + fh) ^ (fr & 7)) << 4;
-        bf16x8 a[4], b[4];
+        bf16x8 a[2], b[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          a[i] = *(const bf16x8*)(As + (wm * 128 + i * 32 + fr) * 128 + ch);
-          b[i] = *(const bf16x8*)(Bs + (wn * 128 + i * 32 + fr) * 128 + ch);
-        }
+        for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(As + (wm * 64 + i * 32 + fr) * 128 + ch);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Bs + (wn * 128 + j * 32 + fr) * 128 + ch);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int j = 0; j < 4; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
       }
       wait_vm();
-      __syncthreads();
+      barrier_lds();
     }
 
     // ------------------------------------------------------------ epilogue
-    // accumulator element e of tile (i, j): row = wm*128 + i*32 + (e>>2)*8 + fh*4 + (e&3),
+    // accumulator element e of tile (i, j): row = wm*64 + i*32 + (e>>2)*8 + fh*4 + (e&3),
     //                                       col = wn*128 + j*32 + fr
     const int colb = n0 + wn * 128 + fr;
     if (EPI == EPI_STATS) {
@@ -225,7 +233,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) cv[j] = colb + j * 32 < N;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < 2; ++i) {
         __builtin_amdgcn_sched_barrier(0);  // keep the accumulator reads of one tile row together
         float mx[16], sm[16], um[16];
 #pragma unroll
@@ -259,7 +267,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
         // logit of the sampled token
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          int rl = wm * 128 + i * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
+          int rl = wm * 64 + i * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
           int y = rp_i[rl];
           int yl = y - (n0 + wn * 128);
           if (yl >= 0 && yl < 128 && (yl & 31) == fr) {
@@ -278,7 +286,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
           ou = sel ? um[e] : ou;
         }
         const int e_own = fr & 15;
-        const int rl = wm * 128 + i * 32 + (e_own >> 2) * 8 + fh * 4 + (e_own & 3);
+        const int rl = wm * 64 + i * 32 + (e_own >> 2) * 8 + fh * 4 + (e_own & 3);
         if (wn == 1 && fr < 16) {
           xm[rl * 3 + 0] = om;
           xm[rl * 3 + 1] = os;
@@ -299,11 +307,11 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       }
     } else if (EPI == EPI_DZ) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < 2; ++i) {
 #pragma unroll
         for (int e4 = 0; e4 < 4; ++e4) {
           __builtin_amdgcn_sched_barrier(0);
-          const int rl0 = wm * 128 + i * 32 + e4 * 8 + fh * 4;
+          const int rl0 = wm * 64 + i * 32 + e4 * 8 + fh * 4;
           float Lr[4], cr[4];
           int yr[4];
 #pragma unroll
@@ -335,11 +343,11 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       }
     } else {  // EPI_STORE
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < 2; ++i) {
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int rl = wm * 128 + i * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
+          const int rl = wm * 64 + i * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
           const int m = m0 + rl;
           if (m >= M) continue;
           const int64_t dst = (int64_t)rp_i[rl] * g.ldc;
