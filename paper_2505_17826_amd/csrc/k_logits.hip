@@ -1,18 +1,20 @@
 // Loss-only path from given fp32 logits [T, V]: one workgroup per row.
 //   pass 1: stream the row (16-byte loads) keeping per-thread online
-//           (max, sum exp, sum exp*z), reduce over the workgroup;
+//           (max, sum exp, sum exp*z), reduce over the workgroup in a fixed
+//           order;
 //   row terms: lse, entropy, logp = z_y - lse, the PPO-clip/KL loss terms
 //           and c_t = d loss / d logp;
-//   pass 2: re-read the row and write d_logits = c_t (onehot - exp(z - lse))
-//           with non-temporal stores.
-// One workgroup per CU (the kernel reserves most of the LDS) keeps the rows in
-// flight small enough that the pass-2 re-read is served by the cache.
+//   pass 2: d_logits = c_t (onehot - exp(z - lse)) with non-temporal stores.
+// The fused kernel keeps the row on chip between the passes (registers, then
+// LDS) so that a row of up to about 600 KB is read from HBM once.  Every kernel
+// here gives each thread the same chunks of the row in the same order, so the
+// statistics-only, d_logits-only and fused kernels agree bit for bit.
 #include "rft_internal.h"
 
 namespace rft {
 namespace lg {
 
-constexpr int NT = 1024;
+constexpr int NT = 512;
 constexpr int UNROLL = 4;
 
 struct RowStats {
@@ -47,6 +49,7 @@ __device__ __forceinline__ void acc1(RowStats& r, float z) {
 }
 
 // Workgroup reduction of the per-thread online partials, in a fixed order.
+template <int NTH = NT>
 __device__ RowStats block_stats(RowStats r, RowStats* sh) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   float M = wave_max_f(r.m);
@@ -56,11 +59,11 @@ __device__ RowStats block_stats(RowStats r, RowStats* sh) {
   __syncthreads();
   if (threadIdx.x == 0) {
     float m = -INFINITY, ss = 0.f, uu = 0.f;
-    for (int i = 0; i < NT / 64; ++i) lse_merge(m, ss, uu, sh[i].m, sh[i].s, sh[i].u);
-    sh[NT / 64] = RowStats{m, ss, uu};
+    for (int i = 0; i < NTH / 64; ++i) lse_merge(m, ss, uu, sh[i].m, sh[i].s, sh[i].u);
+    sh[NTH / 64] = RowStats{m, ss, uu};
   }
   __syncthreads();
-  RowStats out = sh[NT / 64];
+  RowStats out = sh[NTH / 64];
   __syncthreads();
   return out;
 }
@@ -113,14 +116,14 @@ __device__ void row_pass2(const float* __restrict__ z, int64_t V, float lse, flo
   }
 }
 
-template <bool VEC>
+template <bool VEC, int NTH = NT>
 __device__ void zero_row(float* __restrict__ out, int64_t V) {
   if (VEC) {
     floatx4* o4 = (floatx4*)out;
     floatx4 zz = {0.f, 0.f, 0.f, 0.f};
-    for (int64_t j = threadIdx.x; j < (V >> 2); j += NT) __builtin_nontemporal_store(zz, o4 + j);
+    for (int64_t j = threadIdx.x; j < (V >> 2); j += NTH) __builtin_nontemporal_store(zz, o4 + j);
   } else {
-    for (int64_t j = threadIdx.x; j < V; j += NT) out[j] = 0.f;
+    for (int64_t j = threadIdx.x; j < V; j += NTH) out[j] = 0.f;
   }
 }
 
@@ -243,6 +246,151 @@ __global__ void __launch_bounds__(NT) k_logits_fused(
   row_pass2<VEC>(z, V, L, c, (y >= 0 && (int64_t)y < V) ? y : -1, out);
 }
 
+// ---- fused, with the row kept on chip: the first REG*NTC float4 of the row
+// stay in registers and the next LCAP float4 in LDS between the two passes;
+// only the remainder is read twice.
+typedef int v4i __attribute__((ext_vector_type(4)));
+constexpr int NTC = NT;                  // 2 waves per SIMD
+constexpr int REG = 56;                  // float4 per thread held in registers
+constexpr int LCAP = 18 * NTC;           // float4 held in LDS (144 KiB)
+constexpr size_t kCachedLds = (size_t)LCAP * 16;
+
+__device__ __forceinline__ floatx4 dlogit4(floatx4 q, float lk, float c, int64_t j, int y) {
+  floatx4 d;
+  d[0] = -c * exp2f(fmaf(q[0], kLog2e, -lk));
+  d[1] = -c * exp2f(fmaf(q[1], kLog2e, -lk));
+  d[2] = -c * exp2f(fmaf(q[2], kLog2e, -lk));
+  d[3] = -c * exp2f(fmaf(q[3], kLog2e, -lk));
+  if ((y >> 2) == j) d[y & 3] += c;
+  return d;
+}
+
+__device__ __forceinline__ void acc4v(RowStats& r, floatx4 q) {
+  acc4(r, make_float4(q[0], q[1], q[2], q[3]));
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* p, int64_t bytes) {
+  uint64_t a = (uint64_t)p;
+  uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  int nr = __builtin_amdgcn_readfirstlane((int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), 0, nr, 0x00020000);
+}
+
+__global__ void __launch_bounds__(NTC) k_logits_fused_cached(
+    const float* __restrict__ logits, int64_t T, int64_t V, const uint8_t* __restrict__ mask,
+    const int32_t* __restrict__ ids, const int32_t* __restrict__ kidx,
+    const int32_t* __restrict__ row_seq, const int32_t* __restrict__ n_i,
+    const int32_t* __restrict__ meta, const float* __restrict__ old, const float* __restrict__ ref,
+    const float* __restrict__ adv, LossConst cst, float* __restrict__ logp,
+    float* __restrict__ ent, float* __restrict__ lse_out, float* __restrict__ grad_out,
+    float* __restrict__ dl, LossPartial* __restrict__ parts) {
+  extern __shared__ floatx4 row_lds[];  // LCAP float4
+  __shared__ RowStats sh[NTC / 64 + 1];
+  __shared__ float row_c;
+  const int tid = threadIdx.x;
+  const int64_t t = blockIdx.x;
+  float* out = dl + t * V;
+  const int k = kidx[t];
+  // one row is V * 4 bytes (at most 1 GiB, checked by the launcher)
+  const __amdgpu_buffer_rsrc_t rin = row_rsrc(logits + t * V, V * 4);
+  const __amdgpu_buffer_rsrc_t rout = row_rsrc(out, V * 4);
+  const uint32_t vo = (uint32_t)tid * 16u;
+  constexpr uint32_t SU = (uint32_t)NTC * 16u;  // bytes between a thread's chunks
+  const int64_t n4 = V >> 2;
+  if (k < 0) {
+    const floatx4 zz = {0.f, 0.f, 0.f, 0.f};
+    for (int64_t j = tid, o = vo; j < n4; j += NTC, o += SU)
+      __builtin_amdgcn_raw_buffer_store_b128((v4i)zz, rout, (uint32_t)o, 0, 2);
+    if (tid == 0) {
+      logp[t] = 0.f;
+      if (ent) ent[t] = 0.f;
+      if (lse_out) lse_out[t] = 0.f;
+      if (grad_out) grad_out[t] = 0.f;
+      parts[t] = LossPartial{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+    return;
+  }
+  // pass 1: registers, then LDS, then the rest (chunks past the row read as 0
+  // and are left out of the statistics)
+  const int u_full = (int)min((int64_t)REG, n4 / NTC);  // chunks complete for every thread
+  // a lane whose chunk lies past the row takes a vector offset of 2^31, out of
+  // range for the descriptor whether or not the scalar offset is counted
+  const int nv = (int)min((int64_t)REG, (n4 - tid + NTC - 1) / NTC);  // this lane's chunks
+  floatx4 regs[REG];
+#pragma unroll
+  for (int u = 0; u < REG; ++u)
+    regs[u] = (floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, u < nv ? vo : 0x80000000u,
+                                                             (uint32_t)u * SU, 2);
+  RowStats r = {-INFINITY, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < REG; ++u) {
+    if (u < u_full || (u == u_full && tid + (int64_t)u * NTC < n4)) acc4v(r, regs[u]);
+  }
+  const int64_t j_lds = (int64_t)REG * NTC, j_rest = j_lds + LCAP;
+  for (int64_t j = j_lds + tid, s_ = tid; j < n4 && s_ < LCAP; j += NTC, s_ += NTC) {
+    floatx4 q = (floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, (uint32_t)(j * 16), 0, 2);
+    row_lds[s_] = q;
+    acc4v(r, q);
+  }
+  for (int64_t j = j_rest + tid; j < n4; j += NTC)
+    acc4v(r, (floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, (uint32_t)(j * 16), 0, 0));
+  r = block_stats<NTC>(r, sh);
+  const float* z = logits + t * V;
+  if (tid == 0) {
+    float L = r.m + logf(r.s);
+    float H = L - r.u / r.s;
+    int y = ids[t];
+    bool ok = y >= 0 && (int64_t)y < V;
+    float lp = ok ? z[y] - L : __int_as_float(0x7fc00000);
+    logp[t] = lp;
+    if (ent) ent[t] = H;
+    if (lse_out) lse_out[t] = L;
+    LossPartial p = {0, 0, 0, 0, 0, 0, 0, 0};
+    float c = 0.f;
+    if (!ok) {
+      p.bad = 1;
+    } else {
+      int i = row_seq[k];
+      float rf = ref ? ref[t] : lp;
+      TokLoss Lt = token_loss(lp, old[t], rf, adv[i], n_i[i], meta[0], meta[1], cst);
+      p.loss = Lt.w * ((double)Lt.pg + (double)cst.beta * (double)Lt.kl);
+      p.pg = Lt.w * (double)Lt.pg;
+      p.klw = Lt.w * (double)cst.beta * (double)Lt.kl;
+      p.kl = (double)Lt.kl;
+      p.ratio = (double)Lt.rho;
+      p.ent = (double)H;
+      p.clipped = Lt.clipped ? 1 : 0;
+      c = (float)(Lt.w * (double)Lt.g);
+    }
+    if (grad_out) grad_out[t] = c;
+    parts[t] = p;
+    row_c = c;
+    sh[NTC / 64].m = L;
+  }
+  __syncthreads();
+  const float c = row_c, lk = sh[NTC / 64].m * kLog2e;
+  int y = ids[t];
+  y = (y >= 0 && (int64_t)y < V) ? y : -1;
+  // pass 2: same three regions; stores past the row are dropped by the descriptor
+  uint32_t vo2 = vo;
+  int nv2 = nv;
+  asm volatile("" : "+v"(vo2), "+v"(nv2));  // recomputed here, not held through pass 1
+#pragma unroll
+  for (int u = 0; u < REG; ++u)
+    __builtin_amdgcn_raw_buffer_store_b128(
+        (v4i)dlogit4(regs[u], lk, c, tid + (int64_t)u * NTC, y), rout,
+        u < nv2 ? vo2 : 0x80000000u, (uint32_t)u * SU, 2);
+  for (int64_t j = j_lds + tid, s_ = tid; j < n4 && s_ < LCAP; j += NTC, s_ += NTC)
+    __builtin_amdgcn_raw_buffer_store_b128((v4i)dlogit4(row_lds[s_], lk, c, j, y), rout,
+                                           (uint32_t)(j * 16), 0, 2);
+  for (int64_t j = j_rest + tid; j < n4; j += NTC)
+    __builtin_amdgcn_raw_buffer_store_b128(
+        (v4i)dlogit4((floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, (uint32_t)(j * 16), 0, 0),
+                     lk, c, j, y),
+        rout, (uint32_t)(j * 16), 0, 2);
+}
+
 }  // namespace lg
 
 static bool vec_ok(const void* p, int64_t V) {
@@ -281,12 +429,13 @@ hipError_t launch_logits_fused(const float* logits, const rft_tokens& tok, const
                                float* grad, float* dl, LossPartial* parts, rft_ppo_stats* st,
                                hipStream_t s) {
   if (tok.T > 0) {
-    if (vec_ok(logits, V) && vec_ok(dl, V)) {
-      hipError_t e = hipFuncSetAttribute((const void*)lg::k_logits_fused<true>,
+    // buffer descriptors span one row: 32-bit byte offsets
+    if (vec_ok(logits, V) && vec_ok(dl, V) && V <= ((int64_t)1 << 28)) {
+      hipError_t e = hipFuncSetAttribute((const void*)lg::k_logits_fused_cached,
                                          hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         (int)kFusedReserve);
+                                         (int)lg::kCachedLds);
       if (e != hipSuccess) return e;
-      lg::k_logits_fused<true><<<(unsigned)tok.T, lg::NT, kFusedReserve, s>>>(
+      lg::k_logits_fused_cached<<<(unsigned)tok.T, lg::NTC, lg::kCachedLds, s>>>(
           logits, tok.T, V, tok.mask, tok.token_ids, m.kidx, m.row_seq, m.n_i, m.meta, old, ref,
           adv, c, logp, ent, lse, grad, dl, parts);
     } else {
