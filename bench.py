@@ -26,6 +26,30 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 WORKLOADS = {"tiny": 0, "1.5b": 1, "7b": 2, "longcot": 3, "lossonly": 4}
 
+# HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE (one run each), scaled by what the same counters read for a plain
+# copy of known size (read x2.0, write x1.0).  Valid only for the kernel
+# sources they were taken with: a changed source reports null.
+TRAFFIC = {
+    "7b": {"sources": {"k_gemm_mfma.hip": "e8a653268855e3b2", "rft_internal.h": "aa6e4ef7f573c667"},
+           "bytes": 218364953.8 * 1024 * 2.0 + 1174457.5 * 1024 * 1.0},
+    "lossonly": {"sources": {"k_logits.hip": "4aa7d762e0d14af6", "rft_internal.h": "aa6e4ef7f573c667"},
+                 "bytes": 8759344.9 * 1024 * 2.0 + 19461397.0 * 1024 * 1.0},
+}
+
+
+def traffic_gb(workload):
+    import hashlib
+    t = TRAFFIC.get(workload)
+    if t is None:
+        return None
+    csrc = os.path.join(ROOT, "paper_2505_17826_amd", "csrc")
+    for f, h in t["sources"].items():
+        with open(os.path.join(csrc, f), "rb") as fh:
+            if hashlib.sha256(fh.read()).hexdigest()[:16] != h:
+                return None
+    return t["bytes"] / 1e9
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -36,7 +60,28 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GB",
+                    help="only run a plain device copy of GB gigabytes (the known-size kernel "
+                         "that scales the HBM byte counters) and exit")
     return ap.parse_args()
+
+
+def copy_probe(gb):
+    """A plain fp32 device-to-device copy of a known size, three launches."""
+    import torch
+    n = int(gb * 1e9) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(3):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 3
+    print(json.dumps({"copy_probe_bytes_each_way": n * 4, "ms_per_copy": ms,
+                      "GB_per_s_read_plus_write": 2 * n * 4 / ms / 1e6}), flush=True)
 
 
 def cpu_baseline(batch, target_s, extra):
@@ -88,6 +133,9 @@ def cpu_baseline(batch, target_s, extra):
 
 def main():
     args = parse()
+    if args.copy_probe > 0:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "the path would shard by whole GRPO groups (see the design notes)", file=sys.stderr)
@@ -144,7 +192,7 @@ def main():
                                         stats=stats, ws=ws_f)
             if ev is not None:
                 ev[1].record()
-        dom_name = "k_logits_fused (one workgroup per row: stats, loss, d_logits)"
+        dom_name = "k_logits_fused_cached (one workgroup per row: stats, loss, d_logits)"
         # algorithmic bytes: read every valid row once, write every row of d_logits once
         dom_work = (N * V * 4 + T * V * 4) / 1e9  # GB
         bound = "hbm"
@@ -210,13 +258,15 @@ def main():
     if bound == "hbm":
         ach = dom_work / (dom_ms / 1e3)
         out["roofline"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                           "frac": ach / PEAK_HBM_GBS, "traffic": None, "kernel": dom_name,
+                           "frac": ach / PEAK_HBM_GBS, "traffic": traffic_gb(args.workload),
+                           "traffic_unit": "GB per launch", "kernel": dom_name,
                            "ms_per_launch": dom_ms}
     else:
         ach = dom_work / (dom_ms / 1e3)
         peak = PEAK_BF16_TFLOPS if bound == "mfma" else 157.3
         out["roofline"] = {"bound": bound, "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                           "frac": ach / peak, "traffic": None, "kernel": dom_name,
+                           "frac": ach / peak, "traffic": traffic_gb(args.workload),
+                           "traffic_unit": "GB per launch", "kernel": dom_name,
                            "ms_per_launch": dom_ms}
         alg = 6.0 * N * cfg.d * V / 1e12
         out["step_mfma"] = {"algorithmic_tflop": alg, "algorithmic_tflops": alg / (ms / 1e3),
