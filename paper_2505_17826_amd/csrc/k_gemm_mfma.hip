@@ -4,13 +4,14 @@
 // wave's LDS and barrier waits overlap the other's MFMAs), each owning 64x128
 // of C as 2x4 v_mfma_f32_32x32x16_bf16 tiles (fp32 accumulators).  Operands go
 // straight from HBM/L2 into LDS with buffer_load_dwordx4 ... lds (no staging
-// registers); the buffer descriptor covers only the tile's valid rows, so rows
+// registers), issued by four of the eight waves; the buffer descriptor covers only the tile's valid rows, so rows
 // past the end and the K tail read as zeros without branches.  LDS holds
-// 16-byte chunks XOR-swizzled by row (conflict-free ds_read_b128 of MFMA
-// fragments) in two stages.  Workgroups map to tiles so that the ones resident
-// on one XCD work on neighbouring tiles (shared L2), and the number of rows
-// can come from a device counter, so the host never waits for the count of
-// valid tokens.
+// 16-byte chunks XOR-swizzled by row pair (conflict-free ds_read_b128 of MFMA
+// fragments in the 64-bank LDS) in two stages.  Workgroups map to tiles so
+// that the ones resident on one XCD work on neighbouring tiles (shared L2)
+// and all XCDs sweep the same B columns together (shared last-level cache).
+// The number of rows can come from a device counter, so the host never waits
+// for the count of valid tokens.
 //
 // Epilogues:
 //   EPI_STATS  forward of the policy head: per row and 256-column vocabulary
@@ -72,33 +73,81 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int64
   return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), 0, nr, 0x00020000);
 }
 
-// Stage loader: wave w fills rows [w*32, w*32+32) of the A and B tiles with
-// 4 instructions of 8 rows each.  Lane l writes LDS slot l of an instruction
-// (row l/8, physical chunk l%8), so it loads logical chunk (l%8) ^ (row & 7)
-// of its row; chunks at or past K are read from outside the descriptor (0).
+// LDS layout of a stage: rows of BK bf16 (128 B), 16-byte chunk c of row r
+// stored at chunk c ^ ((r >> 1) & 7).  The LDS serves 256 B per clock in 64
+// banks, i.e. two 128-byte rows; a ds_read_b128 of an MFMA fragment (32 rows,
+// one logical chunk) then touches 16 distinct 16-byte bank groups in every
+// group of 16 lanes, so fragment reads are conflict free.
+//
+// Stage loader: waves 0-3 issue the loads, wave w fills rows [w*64, w*64+64)
+// of the A tile and then of the B tile with 8 + 8 instructions of 8 rows each;
+// waves 4-7 only compute.  (Measured on gfx950: four loader waves issuing A
+// and B in two separate runs keep the L2 round trip of the direct-to-LDS
+// loads markedly shorter than eight waves or interleaved A/B loads.)  Lane l
+// writes LDS slot l of an instruction (row p*8 + l/8 of the wave's rows,
+// physical chunk l%8), so it loads logical chunk
+// (l%8) ^ (((p*8 + l/8) >> 1) & 7) = (l%8) ^ (l/16) ^ 4*(p&1); the two
+// parities of p take the offsets vA[0|1], vB[0|1].  Chunks at or past K are
+// read from outside the descriptor (0).
+constexpr int NLOAD = 4;
+struct LoadGeom {
+  uint32_t vA[2], vB[2];  // per-lane byte offsets for even / odd p (k0 = 0)
+  int kc[2];              // logical chunk * 8 (first element) for even / odd p
+  uint32_t sA, sB;        // bytes between instructions (8 rows)
+};
+
 __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB,
-                                           char* dst, int k0, int K, int ld_chunk, uint32_t voffA,
-                                           uint32_t voffB, uint32_t strideA8, uint32_t strideB8) {
-  const bool kin = k0 + ld_chunk * 8 < K;
-  const uint32_t va = kin ? voffA + (uint32_t)k0 * 2u : 0x80000000u;
-  const uint32_t vb = kin ? voffB + (uint32_t)k0 * 2u : 0x80000000u;
+                                           char* dst, int k0, int K, const LoadGeom& lg) {
+  constexpr int NI = 32 / NLOAD;  // instructions per operand per loader wave
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
+  for (int p = 0; p < NI; ++p) {
+    const int q = p & 1;
+    const uint32_t va = k0 + lg.kc[q] < K ? lg.vA[q] + (uint32_t)k0 * 2u : 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_ptr)(dst + p * 1024), 16,
-                                             va + (uint32_t)p * strideA8, 0, 0, 0);
+                                             va + (uint32_t)p * lg.sA, 0, 0, 0);
+  }
+#pragma unroll
+  for (int p = 0; p < NI; ++p) {
+    const int q = p & 1;
+    const uint32_t vb = k0 + lg.kc[q] < K ? lg.vB[q] + (uint32_t)k0 * 2u : 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES + p * 1024), 16,
-                                             vb + (uint32_t)p * strideB8, 0, 0, 0);
+                                             vb + (uint32_t)p * lg.sB, 0, 0, 0);
   }
 }
 
-__device__ __forceinline__ void tile_of(int L, int nTm, int nTn, int& mt, int& nt) {
-  constexpr int GM = 8;
-  int per = GM * nTn;
-  int g = L / per, r = L - g * per;
-  int m_first = g * GM;
-  int gsz = min(nTm - m_first, GM);
-  mt = m_first + r % gsz;
-  nt = r / gsz;
+// Tile order.  Workgroup b runs on XCD x = b % 8 as the j = b / 8-th
+// workgroup dispatched there.  M-tiles are taken in super-groups of 64: XCD x
+// owns M-tiles [64 s + 8 x, 64 s + 8 x + 8) of super-group s and walks them
+// eight at a time along N, so the 32 workgroups resident on one XCD cover
+// 8 M-tiles x 4 N-tiles (A and B slabs shared in that XCD's L2) and all XCDs
+// read the same B columns at the same time (shared in the last-level cache).
+// M-tiles past the last full super-group are dealt round-robin over the XCDs.
+// Returns false for workgroups with no tile.
+constexpr int SG = 8;
+__device__ __forceinline__ bool tile_of(int b, int nTm, int nTn, int& mt, int& nt) {
+  const int x = b & 7, j = b >> 3;
+  const int full = nTm / (8 * SG);
+  const int per = SG * nTn;  // tiles per XCD per super-group
+  if (j < full * per) {
+    const int s_ = j / per, r = j - s_ * per;
+    mt = s_ * 8 * SG + x * SG + r % SG;
+    nt = r / SG;
+    return true;
+  }
+  const int R = nTm - full * 8 * SG;
+  const int t = (j - full * per) * 8 + x;
+  if (t >= R * nTn) return false;
+  mt = full * 8 * SG + t % R;
+  nt = t / R;
+  return true;
+}
+
+// Workgroups needed for nTm x nTn tiles in that order (non-decreasing in
+// nTm, so a grid sized for the largest M covers every smaller M).
+inline int64_t grid_tiles(int64_t nTm, int64_t nTn) {
+  const int64_t full = nTm / (8 * SG);
+  const int64_t R = nTm - full * 8 * SG;
+  return 8 * (full * SG * nTn + (R * nTn + 7) / 8);
 }
 
 // Workgroup barrier without the implicit wait for outstanding loads; the
@@ -127,22 +176,27 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   const int NB = g.NB > 0 ? g.NB : N;
   if (EPI == EPI_STORE && g.k_from_cnt && K == 0 && g.accumulate) return;  // nothing to add
   const int nTm = (M + BM - 1) / BM, nTn = (N + BN - 1) / BN;
-  const int total = nTm * nTn;
-  // Workgroup b runs on XCD b % 8: give each XCD a contiguous run of tiles so
-  // the workgroups resident on one XCD share operand tiles in its L2.  The
-  // grid is sized for the largest possible M; workgroups past the device
-  // count exit at once (they are dispatched last).
-  const int per_xcd = (total + 7) >> 3;
-  const int L = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if ((int)(blockIdx.x >> 3) >= per_xcd || L >= total) return;
+  // The grid is sized for the largest possible M; workgroups without a tile
+  // for the device count exit at once.
+  int mt, nt;
+  if (!tile_of((int)blockIdx.x, nTm, nTn, mt, nt)) return;
   const int nk = (K + BK - 1) / BK;
 
-  // per-lane load geometry (see load_stage): row w*32 + p*8 + (lane>>3)
-  const int ld_row = wid * 32 + (lane >> 3);
-  const int ld_chunk = (lane & 7) ^ ((lane >> 3) & 7);
-  const uint32_t voffA = (uint32_t)(ld_row * g.lda * 2 + ld_chunk * 16);
-  const uint32_t voffB = (uint32_t)(ld_row * g.ldb * 2 + ld_chunk * 16);
-  const uint32_t strideA8 = (uint32_t)(8 * g.lda * 2), strideB8 = (uint32_t)(8 * g.ldb * 2);
+  // per-lane load geometry (see load_stage): row w*64 + p*8 + (lane>>3)
+  const bool loader = wid < NLOAD;
+  LoadGeom lg;
+  {
+    const int ld_row = (wid % NLOAD) * (256 / NLOAD) + (lane >> 3);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int ch = (lane & 7) ^ (lane >> 4) ^ (q * 4);
+      lg.kc[q] = ch * 8;
+      lg.vA[q] = (uint32_t)(ld_row * g.lda * 2 + ch * 16);
+      lg.vB[q] = (uint32_t)(ld_row * g.ldb * 2 + ch * 16);
+    }
+    lg.sA = (uint32_t)(8 * g.lda * 2);
+    lg.sB = (uint32_t)(8 * g.ldb * 2);
+  }
   // per-lane MFMA operand offsets (row = base + (lane&31), chunk = ks*2 + (lane>>5))
   const int fr = lane & 31, fh = lane >> 5;
 
@@ -151,8 +205,6 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   float* rp_b = (float*)(lds + 2 * STAGE + BM * 8);
 
   {
-    int mt, nt;
-    tile_of(L, nTm, nTn, mt, nt);
     const int m0 = mt * BM, n0 = nt * BN;
 
     // buffer descriptors over the tile's valid rows: everything else reads 0
@@ -195,19 +247,18 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    char* const ldsw = lds + wid * 32 * 128;
-    if (nk > 0)
-      load_stage(rA, rB, ldsw, 0, K, ld_chunk, voffA, voffB, strideA8, strideB8);
+    char* const ldsw = lds + (wid % NLOAD) * (256 / NLOAD) * 128;
+    if (nk > 0 && loader)
+      load_stage(rA, rB, ldsw, 0, K, lg);
     __syncthreads();  // first stage and the per-row parameters are visible to every wave
     for (int kt = 0; kt < nk; ++kt) {
-      if (kt + 1 < nk)
-        load_stage(rA, rB, ldsw + ((kt + 1) & 1) * STAGE, (kt + 1) * BK, K, ld_chunk, voffA,
-                   voffB, strideA8, strideB8);
+      if (kt + 1 < nk && loader)
+        load_stage(rA, rB, ldsw + ((kt + 1) & 1) * STAGE, (kt + 1) * BK, K, lg);
       const char* As = lds + (kt & 1) * STAGE;
       const char* Bs = As + A_BYTES;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const int ch = ((ks * 2 + fh) ^ (fr & 7)) << 4;
+        const int ch = ((ks * 2 + fh) ^ ((fr >> 1) & 7)) << 4;
         bf16x8 a[2], b[4];
 #pragma unroll
         for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(As + (wm * 64 + i * 32 + fr) * 128 + ch);
@@ -370,8 +421,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 
 // ------------------------------------------------------------ launchers ----
 static unsigned grid_for(int64_t M_cap, int64_t N) {
-  int64_t tiles = ((M_cap + mf::BM - 1) / mf::BM) * ((N + mf::BN - 1) / mf::BN);
-  return (unsigned)((tiles + 7) / 8 * 8);
+  return (unsigned)mf::grid_tiles((M_cap + mf::BM - 1) / mf::BM, (N + mf::BN - 1) / mf::BN);
 }
 
 // Forward of the policy head over the compacted hidden rows Hc [rows_off, rows_off + cap):
