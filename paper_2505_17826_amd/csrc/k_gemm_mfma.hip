@@ -31,7 +31,11 @@ constexpr int A_BYTES = BM * BK * 2;
 constexpr int B_BYTES = BN * BK * 2;
 constexpr int STAGE = A_BYTES + B_BYTES;  // 64 KiB
 constexpr int ROWP = BM * 16;             // per-row epilogue parameters
-constexpr int LDS_TOTAL = 2 * STAGE + ROWP;
+// dZ epilogue: one 256x256 bf16 tile staged in LDS, rows padded to 528 bytes
+// (conflict-free 2- and 8-byte writes, contiguous 16-byte reads)
+constexpr int STG_PITCH = 528;
+constexpr int STG_BYTES = 256 * STG_PITCH;
+constexpr int LDS_TOTAL = 2 * STAGE + ROWP > STG_BYTES ? 2 * STAGE + ROWP : STG_BYTES;
 
 enum { EPI_STATS = 0, EPI_DZ = 1, EPI_STORE = 2 };
 
@@ -357,6 +361,9 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
         __syncthreads();
       }
     } else if (EPI == EPI_DZ) {
+      // d = c (onehot - p) in bf16, packed per lane as four consecutive rows
+      // of one column
+      uint2 hv[2][4][4];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
 #pragma unroll
@@ -375,23 +382,59 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
           for (int j = 0; j < 4; ++j) {
             const int col = colb + j * 32;
             const bool cvalid = col < g.Vvalid;
-            uint16_t hb[4];
+            uint32_t hb[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               float z = acc[i][j][e4 * 4 + q];
               float p = exp2f(z * kLog2e - Lr[q]);
               float d = cr[q] * ((col == yr[q] ? 1.f : 0.f) - p);
-              d = cvalid ? d : 0.f;
-              hb[q] = f32_to_bf16(d);
-              g.dz[(int64_t)(m0 + rl0 + q) * g.ldz + col] = hb[q];
+              hb[q] = f32_to_bf16(cvalid ? d : 0.f);
             }
-            uint2 pk;
-            pk.x = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
-            pk.y = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
-            *(uint2*)(g.dzt + (int64_t)col * g.ldzt + m0 + rl0) = pk;
+            hv[i][j][e4].x = hb[0] | (hb[1] << 16);
+            hv[i][j][e4].y = hb[2] | (hb[3] << 16);
           }
         }
       }
+      // Stage each layout through LDS and write it with 16-byte stores that
+      // cover whole lines: a wave writes two 512-byte rows per instruction.
+      char* const st = lds;
+      auto copy_out = [&](uint16_t* dst, int64_t ld) {
+#pragma unroll 4
+        for (int it = 0; it < 16; ++it) {
+          const int c = it * NT + tid, row = c >> 5, ch = c & 31;
+          const uint4 v = *(const uint4*)(st + row * STG_PITCH + ch * 16);
+          *(uint4*)(dst + (int64_t)row * ld + ch * 8) = v;
+        }
+      };
+      __syncthreads();  // every wave is done with the stages and the row parameters
+      // dZ [rows, Vpad]: element (row, col) at byte row * pitch + col * 2
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4) {
+            char* q0 = st + (wm * 64 + i * 32 + e4 * 8 + fh * 4) * STG_PITCH +
+                       (wn * 128 + j * 32 + fr) * 2;
+            *(uint16_t*)(q0) = (uint16_t)hv[i][j][e4].x;
+            *(uint16_t*)(q0 + STG_PITCH) = (uint16_t)(hv[i][j][e4].x >> 16);
+            *(uint16_t*)(q0 + 2 * STG_PITCH) = (uint16_t)hv[i][j][e4].y;
+            *(uint16_t*)(q0 + 3 * STG_PITCH) = (uint16_t)(hv[i][j][e4].y >> 16);
+          }
+      __syncthreads();
+      copy_out(g.dz + (int64_t)m0 * g.ldz + n0, g.ldz);
+      __syncthreads();
+      // dZ^T [Vpad, rows]: element (col, row) at byte col * pitch + row * 2
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4)
+            *(uint2*)(st + (wn * 128 + j * 32 + fr) * STG_PITCH +
+                      (wm * 64 + i * 32 + e4 * 8 + fh * 4) * 2) = hv[i][j][e4];
+      __syncthreads();
+      copy_out(g.dzt + (int64_t)n0 * g.ldzt + m0, g.ldzt);
     } else {  // EPI_STORE
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
