@@ -3,11 +3,11 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 7b|1.5b|longcot|lossonly|tiny]
 
 One step is one pass of the whole hot path over one synthetic batch that is
-already resident in HBM: group advantages, per-token log-probs and entropy
-through the lm_head (online log-sum-exp, no stored logits), the PPO-clip/KL
-loss, and the backward to the hidden states and the lm_head weight (the
-loss-only workload: log-softmax statistics, loss and d_logits from given
-logits).  Prints one JSON line.
+already resident in HBM: group advantages, then rft_ppo_clip_step - per-token
+log-probs and entropy through the lm_head (online log-sum-exp, logits kept only
+for one chunk of rows), the PPO-clip/KL loss, and the backward to the hidden
+states and the lm_head weight (the loss-only workload: log-softmax statistics,
+loss and d_logits from given logits in one fused call).  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -203,10 +203,9 @@ def main():
         dW = torch.empty((V, d), **f32)
         ws_fwd = torch.empty(R.workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, tok, d, V, dt),
                              dtype=torch.uint8, device=dev)
-        ws_loss = torch.empty(R.workspace_bytes(R.RFT_OP_PPO_FWD, tok, d, V, dt),
+        ws_step = torch.empty(R.workspace_bytes(R.RFT_OP_PPO_STEP, tok, d, V, dt),
                               dtype=torch.uint8, device=dev)
-        ws_bwd = torch.empty(R.workspace_bytes(R.RFT_OP_PPO_BWD, tok, d, V, dt),
-                             dtype=torch.uint8, device=dev)
+        # rollout-side log-probs for the old / reference policies (setup, untimed)
         R.rft_token_logprobs(tok, b.H, b.W, logp=logp, entropy=ent, lse=lse, ws=ws_fwd)
         old = torch.where(b.mask.bool(), logp + b.old_noise, torch.zeros_like(logp))
         ref = torch.where(b.mask.bool(), logp + b.ref_noise, torch.zeros_like(logp))
@@ -215,15 +214,27 @@ def main():
             R.rft_group_advantages(b.rewards, cfg.group, out=adv)
             if ev is not None:
                 ev[0].record()
-            R.rft_token_logprobs(tok, b.H, b.W, logp=logp, entropy=ent, lse=lse, ws=ws_fwd)
+            R.rft_ppo_clip_step(tok, b.H, b.W, old, ref, adv, params, logp=logp, entropy=ent,
+                                lse=lse, grad_logp=grad, d_hidden=dH, d_weight=dW, stats=stats,
+                                ws=ws_step)
             if ev is not None:
                 ev[1].record()
-            R.rft_ppo_clip_loss_fwd(tok, V, logp, old, ref, adv, params, entropy=ent,
-                                    grad_logp=grad, stats=stats, ws=ws_loss)
-            R.rft_ppo_clip_loss_bwd(tok, b.H, b.W, lse, grad, d_hidden=dH, d_weight=dW,
-                                    ws=ws_bwd)
-        dom_name = "rft_token_logprobs (MFMA lm_head forward + online LSE), 2*N*d*V per call"
-        dom_work = 2.0 * N * d * V / 1e12  # TFLOP
+
+        def fwd_kernel_ms(reps=3):
+            """The forward GEMM with online log-sum-exp alone (rft_token_logprobs), timed
+            after the benchmark: its per-launch rate is the kernel-level roofline."""
+            e = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                 for _ in range(reps)]
+            for a, z in e:
+                a.record()
+                R.rft_token_logprobs(tok, b.H, b.W, logp=logp, entropy=ent, lse=lse, ws=ws_fwd)
+                z.record()
+            torch.cuda.synchronize()
+            return float(np.mean([a.elapsed_time(z) for a, z in e]))
+        dom_name = ("rft_ppo_clip_step: every MFMA GEMM of the step (forward with online LSE "
+                    "and fp16 logit store, dH, dW) plus the dZ pass; 6*N*d*V algorithmic flops "
+                    "per call")
+        dom_work = 6.0 * N * d * V / 1e12  # TFLOP
         bound = "mfma" if cfg.dtype == "bf16" else "alu"
 
     torch.cuda.synchronize()
@@ -265,13 +276,20 @@ def main():
         ach = dom_work / (dom_ms / 1e3)
         peak = PEAK_BF16_TFLOPS if bound == "mfma" else 157.3
         out["roofline"] = {"bound": bound, "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                           "frac": ach / peak, "traffic": traffic_gb(args.workload),
+                           "frac": ach / peak, "traffic": traffic_gb("step_" + args.workload),
                            "traffic_unit": "GB per launch", "kernel": dom_name,
                            "ms_per_launch": dom_ms}
         alg = 6.0 * N * cfg.d * V / 1e12
         out["step_mfma"] = {"algorithmic_tflop": alg, "algorithmic_tflops": alg / (ms / 1e3),
                             "frac_algorithmic": alg / (ms / 1e3) / peak,
-                            "frac_executed": (8.0 * N * cfg.d * V / 1e12) / (ms / 1e3) / peak}
+                            "executed_flop_per_token": "6dV (logits formed once, not recomputed)"}
+        fms = fwd_kernel_ms()
+        fw = 2.0 * N * cfg.d * V / 1e12
+        out["roofline_fwd_kernel"] = {
+            "kernel": "k_gemm<EPI_STATS> via rft_token_logprobs (timed after the benchmark)",
+            "bound": bound, "achieved": fw / (fms / 1e3), "peak": peak, "unit": "TFLOP/s",
+            "frac": fw / (fms / 1e3) / peak, "ms_per_launch": fms,
+            "traffic": traffic_gb(args.workload), "traffic_unit": "GB per launch"}
     out["loss"] = st["loss"]
     out["clipfrac"] = st["clipfrac"]
     if not args.no_cpu_baseline:

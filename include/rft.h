@@ -76,7 +76,8 @@ typedef enum {
   RFT_OP_PPO_FWD = 2,
   RFT_OP_PPO_BWD = 3,
   RFT_OP_PPO_BWD_LOGITS = 4,
-  RFT_OP_PPO_FUSED_LOGITS = 5
+  RFT_OP_PPO_FUSED_LOGITS = 5,
+  RFT_OP_PPO_STEP = 6
 } rft_op;
 
 /* (host struct holding device pointers) */
@@ -123,9 +124,10 @@ const char* rft_status_str(int status);
 const char* rft_last_error(void);
 
 /* Workspace bytes the operation `op` needs for this layout and sizes (d and V
- * as in the call; dtype of hidden/weight).  For RFT_OP_PPO_BWD the value is
- * the recommended size; any size >= rft_workspace_min_bytes() works, a larger
- * workspace processes more rows per backward chunk.  Returns 0 for invalid
+ * as in the call; dtype of hidden/weight).  For RFT_OP_PPO_BWD and
+ * RFT_OP_PPO_STEP the value is the recommended size; any size >=
+ * rft_workspace_min_bytes() works, a larger workspace processes more rows per
+ * chunk.  Returns 0 for invalid
  * arguments. */
 size_t rft_workspace_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
 size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
@@ -210,8 +212,8 @@ rft_status rft_ppo_clip_loss_bwd_logits(const rft_tokens* tok, const float* logi
 
 /* The loss-only path in one pass per row: log-softmax statistics of the given
  * logits, the PPO-clip/KL loss and metrics, and d_logits, reading each valid
- * logits row once from HBM (a second read of the row is served from cache)
- * and writing d_logits once.  Outputs as rft_token_logprobs_from_logits,
+ * logits row once from HBM (the row stays on chip between the statistics and
+ * the gradient) and writing d_logits once.  Outputs as rft_token_logprobs_from_logits,
  * rft_ppo_clip_loss_fwd and rft_ppo_clip_loss_bwd_logits (entropy may be
  * NULL; lse and grad_logp may be NULL). */
 rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits, int64_t V,
@@ -220,6 +222,30 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
                                      float* entropy, float* lse, float* grad_logp,
                                      float* d_logits, rft_ppo_stats* stats, void* ws,
                                      size_t ws_bytes, void* stream);
+
+/* The whole trainer-side step of the policy head in one call (Sec. 3: the
+ * trainer's update with the PPO-clip surrogate, k3 KL to the reference model
+ * and GRPO advantages, over the masked response tokens): the outputs of
+ * rft_token_logprobs (logp, entropy, lse), of rft_ppo_clip_loss_fwd
+ * (grad_logp, *stats) and of rft_ppo_clip_loss_bwd (d_hidden, d_weight), for
+ * the same inputs and with the same conventions (masked rows 0, bad ids,
+ * accumulate_dw).  adv is [n_seq] (e.g. from rft_group_advantages).
+ * The rows are processed in chunks sized by the workspace.  For bf16 inputs
+ * the chunk's forward GEMM keeps, next to the log-sum-exp partials, each
+ * logit minus its row's maximum over a 256-column tile in fp16 in the
+ * workspace, and the backward forms dZ from it instead of recomputing the
+ * logits (6 N d V flops instead of 8 N d V); logp, entropy, lse, grad_logp
+ * and the stats equal those of the separate calls bit for bit, d_hidden and
+ * d_weight agree to the rounding of dZ.  For fp32 inputs the call runs the
+ * three separate calls in order.  logits are never stored beyond one chunk.
+ * Errors: as rft_token_logprobs and rft_ppo_clip_loss_fwd. */
+rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const void* weight,
+                             int dtype, int64_t d, int64_t V, const float* old_logp,
+                             const float* ref_logp, const float* adv,
+                             const rft_ppo_params* params, float* logp, float* entropy,
+                             float* lse, float* grad_logp, float* d_hidden, float* d_weight,
+                             int32_t accumulate_dw, rft_ppo_stats* stats, void* ws,
+                             size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -23,7 +23,7 @@ RFT_OK, RFT_E_NULL, RFT_E_SHAPE, RFT_E_DTYPE, RFT_E_PARAM, RFT_E_WORKSPACE, \
 RFT_F32, RFT_BF16 = 0, 1
 RFT_AGG_SEQ_MEAN_TOKEN_MEAN, RFT_AGG_TOKEN_MEAN = 0, 1
 (RFT_OP_TOKEN_LOGPROBS, RFT_OP_TOKEN_LOGPROBS_FROM_LOGITS, RFT_OP_PPO_FWD, RFT_OP_PPO_BWD,
- RFT_OP_PPO_BWD_LOGITS, RFT_OP_PPO_FUSED_LOGITS) = range(6)
+ RFT_OP_PPO_BWD_LOGITS, RFT_OP_PPO_FUSED_LOGITS, RFT_OP_PPO_STEP) = range(7)
 
 _p = ctypes.c_void_p
 _i64 = ctypes.c_int64
@@ -75,6 +75,10 @@ _SIGS = {
     "rft_ppo_clip_fused_logits": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _i64, _p, _p, _p,
                                                  ctypes.POINTER(rft_ppo_params), _p, _p, _p, _p,
                                                  _p, _p, _p, ctypes.c_size_t, _p]),
+    "rft_ppo_clip_step": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _p, ctypes.c_int, _i64,
+                                         _i64, _p, _p, _p, ctypes.POINTER(rft_ppo_params), _p, _p,
+                                         _p, _p, _p, _p, ctypes.c_int32, _p, _p, ctypes.c_size_t,
+                                         _p]),
 }
 
 _LIB = None
@@ -287,6 +291,33 @@ def rft_ppo_clip_fused_logits(tokens: Tokens, logits, old_logp, ref_logp, adv, p
                                            _ptr(d_logits), _ptr(stats), _ptr(ws), nb,
                                            _stream(stream)))
     return logp, d_logits, stats
+
+
+def rft_ppo_clip_step(tokens: Tokens, hidden, weight, old_logp, ref_logp, adv, params,
+                      logp=None, entropy=None, lse=None, grad_logp=None, d_hidden=None,
+                      d_weight=None, accumulate_dw=False, stats=None, ws=None, stream=None):
+    """Returns (logp, entropy, lse, grad_logp, d_hidden, d_weight, stats)."""
+    _need_gpu(hidden, weight, old_logp, adv)
+    dev = hidden.device
+    T, d, V = tokens.T, hidden.shape[1], weight.shape[0]
+    dt = _dtype_code(hidden)
+    f32 = dict(dtype=torch.float32, device=dev)
+    logp = torch.empty(T, **f32) if logp is None else logp
+    entropy = torch.empty(T, **f32) if entropy is None else entropy
+    lse = torch.empty(T, **f32) if lse is None else lse
+    grad_logp = torch.empty(T, **f32) if grad_logp is None else grad_logp
+    d_hidden = torch.empty((T, d), **f32) if d_hidden is None else d_hidden
+    d_weight = torch.empty((V, d), **f32) if d_weight is None else d_weight
+    stats = torch.zeros(STATS_BYTES, dtype=torch.uint8, device=dev) if stats is None else stats
+    need = workspace_bytes(RFT_OP_PPO_STEP, tokens, d, V, dt)
+    ws, nb = _workspace(need, dev, ws)
+    tk = tokens.c()
+    _check(lib().rft_ppo_clip_step(ctypes.byref(tk), _ptr(hidden), _ptr(weight), dt, d, V,
+                                   _ptr(old_logp), _ptr(ref_logp), _ptr(adv), ctypes.byref(params),
+                                   _ptr(logp), _ptr(entropy), _ptr(lse), _ptr(grad_logp),
+                                   _ptr(d_hidden), _ptr(d_weight), 1 if accumulate_dw else 0,
+                                   _ptr(stats), _ptr(ws), nb, _stream(stream)))
+    return logp, entropy, lse, grad_logp, d_hidden, d_weight, stats
 
 
 def loaded_library_path() -> str:

@@ -17,6 +17,9 @@
 //   EPI_STATS  forward of the policy head: per row and 256-column vocabulary
 //              tile, online log-sum-exp partials (max, sum exp, sum exp*z) and
 //              the logit of the sampled token.  Logits are never stored.
+//   EPI_STATS_Y  EPI_STATS, and also z minus the row's maximum over the
+//              tile, rounded to fp16, row-major [rows, Vpad] (the backward
+//              then forms dZ from it instead of recomputing z).
 //   EPI_DZ     backward recompute: dZ = c (onehot(y) - exp(z - lse)) in bf16,
 //              written row-major [rows, Vpad] and transposed [Vpad, rows].
 //   EPI_STORE  fp32 result, optionally scattered to rows through a map and
@@ -37,7 +40,7 @@ constexpr int STG_PITCH = 528;
 constexpr int STG_BYTES = 256 * STG_PITCH;
 constexpr int LDS_TOTAL = 2 * STAGE + ROWP > STG_BYTES ? 2 * STAGE + ROWP : STG_BYTES;
 
-enum { EPI_STATS = 0, EPI_DZ = 1, EPI_STORE = 2 };
+enum { EPI_STATS = 0, EPI_DZ = 1, EPI_STORE = 2, EPI_STATS_Y = 3 };
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
@@ -63,7 +66,9 @@ struct Args {
   const int32_t* ids;
   const float* lse;
   const float* cgrad;
-  float* pm; float* ps; float* pu; int64_t ldp; float* zy;  // EPI_STATS (index rows_off + m)
+  float* pm; float* ps; float* pu; int64_t ldp; float* zy;  // EPI_STATS: partials at p_off + m,
+  int64_t p_off;                                            //   zy at rows_off + m
+  uint16_t* y; int64_t ldy;                                 // EPI_STATS_Y: fp16 z - tile max
   uint16_t* dz; int64_t ldz; uint16_t* dzt; int64_t ldzt; int64_t Vvalid;  // EPI_DZ
   float* C; int64_t ldc; int accumulate; int c_scatter;  // EPI_STORE
 };
@@ -162,8 +167,34 @@ __device__ __forceinline__ void barrier_lds() {
   asm volatile("" ::: "memory");
 }
 
+// Copy a staged 256 x 256 tile of 16-bit values (rows STG_PITCH bytes apart in
+// LDS) to dst with row stride ld: each instruction of a wave writes two
+// 512-byte rows with 16-byte stores.
+__device__ __forceinline__ void stage_copy_out(const char* st, uint16_t* dst, int64_t ld, int tid) {
+#pragma unroll 4
+  for (int it = 0; it < 16; ++it) {
+    const int c = it * NT + tid, row = c >> 5, ch = c & 31;
+    const uint4 v = *(const uint4*)(st + row * STG_PITCH + ch * 16);
+    *(uint4*)(dst + (int64_t)row * ld + ch * 8) = v;
+  }
+}
+
+// Write four 16-bit values (rows r..r+3 of one column, packed in v) into the
+// row-major staging tile.
+__device__ __forceinline__ void stage_col4(char* q0, uint2 v) {
+  *(uint16_t*)(q0) = (uint16_t)v.x;
+  *(uint16_t*)(q0 + STG_PITCH) = (uint16_t)(v.x >> 16);
+  *(uint16_t*)(q0 + 2 * STG_PITCH) = (uint16_t)v.y;
+  *(uint16_t*)(q0 + 3 * STG_PITCH) = (uint16_t)(v.y >> 16);
+}
+
+__device__ __forceinline__ uint32_t f16_bits(float f) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
+}
+
 template <int EPI>
 __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
+  constexpr bool kStats = EPI == EPI_STATS || EPI == EPI_STATS_Y;
   __shared__ __attribute__((aligned(16))) char lds[LDS_TOTAL];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -222,7 +253,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     if (tid < BM) {
       int m = m0 + tid;
       bool v = m < M;
-      if (EPI == EPI_STATS) {
+      if (kStats) {
         int y = -1;
         if (v) y = g.ids[g.rows[g.rows_off + m]];
         rp_i[tid] = y;
@@ -282,8 +313,9 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     // accumulator element e of tile (i, j): row = wm*64 + i*32 + (e>>2)*8 + fh*4 + (e&3),
     //                                       col = wn*128 + j*32 + fr
     const int colb = n0 + wn * 128 + fr;
-    if (EPI == EPI_STATS) {
-      float* xm = (float*)lds;  // cross-wave exchange [256 rows][3]
+    if (kStats) {
+      float* xm = (float*)lds;           // cross-wave exchange [256 rows][3]
+      float* mrow = (float*)(lds + 3072);  // row maximum over the tile [256]
       bool cv[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) cv[j] = colb + j * 32 < N;
@@ -350,15 +382,52 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
         __syncthreads();
         if (wn == 0 && fr < 16) {
           int m = m0 + rl;
+          float mt = 0.f;
           if (m < M) {
             lse_merge(om, os, ou, xm[rl * 3 + 0], xm[rl * 3 + 1], xm[rl * 3 + 2]);
-            int64_t o = (int64_t)nt * g.ldp + g.rows_off + m;
+            int64_t o = (int64_t)nt * g.ldp + g.p_off + m;
             g.pm[o] = om;
             g.ps[o] = os;
             g.pu[o] = ou;
+            mt = om;
           }
+          if (EPI == EPI_STATS_Y) mrow[rl] = mt;
         }
         __syncthreads();
+      }
+      if (EPI == EPI_STATS_Y) {
+        // y = z - (row maximum over the tile) <= 0, rounded to fp16; rows past
+        // M and columns past N hold values the backward never uses
+        uint2 hv[2][4][4];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4) {
+            const int rl0 = wm * 64 + i * 32 + e4 * 8 + fh * 4;
+            float mr[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) mr[q] = mrow[rl0 + q];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              uint32_t hb[4];
+#pragma unroll
+              for (int q = 0; q < 4; ++q) hb[q] = f16_bits(acc[i][j][e4 * 4 + q] - mr[q]);
+              hv[i][j][e4].x = hb[0] | (hb[1] << 16);
+              hv[i][j][e4].y = hb[2] | (hb[3] << 16);
+            }
+          }
+        __syncthreads();  // the staging tile overlaps xm and mrow
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e4 = 0; e4 < 4; ++e4)
+              stage_col4(lds + (wm * 64 + i * 32 + e4 * 8 + fh * 4) * STG_PITCH +
+                             (wn * 128 + j * 32 + fr) * 2,
+                         hv[i][j][e4]);
+        __syncthreads();
+        stage_copy_out(lds, g.y + (int64_t)m0 * g.ldy + n0, g.ldy, tid);
       }
     } else if (EPI == EPI_DZ) {
       // d = c (onehot - p) in bf16, packed per lane as four consecutive rows
@@ -398,14 +467,6 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       // Stage each layout through LDS and write it with 16-byte stores that
       // cover whole lines: a wave writes two 512-byte rows per instruction.
       char* const st = lds;
-      auto copy_out = [&](uint16_t* dst, int64_t ld) {
-#pragma unroll 4
-        for (int it = 0; it < 16; ++it) {
-          const int c = it * NT + tid, row = c >> 5, ch = c & 31;
-          const uint4 v = *(const uint4*)(st + row * STG_PITCH + ch * 16);
-          *(uint4*)(dst + (int64_t)row * ld + ch * 8) = v;
-        }
-      };
       __syncthreads();  // every wave is done with the stages and the row parameters
       // dZ [rows, Vpad]: element (row, col) at byte row * pitch + col * 2
 #pragma unroll
@@ -413,16 +474,12 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4) {
-            char* q0 = st + (wm * 64 + i * 32 + e4 * 8 + fh * 4) * STG_PITCH +
-                       (wn * 128 + j * 32 + fr) * 2;
-            *(uint16_t*)(q0) = (uint16_t)hv[i][j][e4].x;
-            *(uint16_t*)(q0 + STG_PITCH) = (uint16_t)(hv[i][j][e4].x >> 16);
-            *(uint16_t*)(q0 + 2 * STG_PITCH) = (uint16_t)hv[i][j][e4].y;
-            *(uint16_t*)(q0 + 3 * STG_PITCH) = (uint16_t)(hv[i][j][e4].y >> 16);
-          }
+          for (int e4 = 0; e4 < 4; ++e4)
+            stage_col4(st + (wm * 64 + i * 32 + e4 * 8 + fh * 4) * STG_PITCH +
+                           (wn * 128 + j * 32 + fr) * 2,
+                       hv[i][j][e4]);
       __syncthreads();
-      copy_out(g.dz + (int64_t)m0 * g.ldz + n0, g.ldz);
+      stage_copy_out(st, g.dz + (int64_t)m0 * g.ldz + n0, g.ldz, tid);
       __syncthreads();
       // dZ^T [Vpad, rows]: element (col, row) at byte col * pitch + row * 2
 #pragma unroll
@@ -434,7 +491,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
             *(uint2*)(st + (wn * 128 + j * 32 + fr) * STG_PITCH +
                       (wm * 64 + i * 32 + e4 * 8 + fh * 4) * 2) = hv[i][j][e4];
       __syncthreads();
-      copy_out(g.dzt + (int64_t)n0 * g.ldzt + m0, g.ldzt);
+      stage_copy_out(st, g.dzt + (int64_t)n0 * g.ldzt + m0, g.ldzt, tid);
     } else {  // EPI_STORE
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -479,8 +536,27 @@ hipError_t mfma_fwd_stats(const uint16_t* Hc, int64_t d, const uint16_t* W, int6
   a.M = (int)cap; a.N = (int)V; a.K = (int)d;
   a.cnt = cnt; a.cnt_off = rows_off; a.cnt_cap = cap; a.m_from_cnt = 1;
   a.rows = rows; a.rows_off = rows_off; a.ids = ids;
-  a.pm = pm; a.ps = ps; a.pu = pu; a.ldp = ldp; a.zy = zy;
+  a.pm = pm; a.ps = ps; a.pu = pu; a.ldp = ldp; a.zy = zy; a.p_off = rows_off;
   mf::k_gemm<mf::EPI_STATS><<<grid_for(cap, V), mf::NT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+// Forward of one chunk of compacted rows [c0, c0 + Tc) for the fused step:
+// partials [ntiles][Tc] indexed by the chunk row, zy by the compacted row, and
+// y = z - (row maximum over the tile) in fp16 into y [Tc, ldy] (ldy = Vpad).
+hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V,
+                            int64_t Vpad, const int32_t* rows, const int32_t* ids,
+                            const int32_t* cnt, int64_t c0, int64_t Tc, float* pm, float* ps,
+                            float* pu, float* zy, uint16_t* y, hipStream_t s) {
+  mf::Args a = {};
+  a.A = Hc + c0 * d; a.lda = d;
+  a.B = W; a.ldb = d;
+  a.M = (int)Tc; a.N = (int)V; a.K = (int)d;
+  a.cnt = cnt; a.cnt_off = c0; a.cnt_cap = Tc; a.m_from_cnt = 1;
+  a.rows = rows; a.rows_off = c0; a.ids = ids;
+  a.pm = pm; a.ps = ps; a.pu = pu; a.ldp = Tc; a.zy = zy; a.p_off = 0;
+  a.y = y; a.ldy = Vpad;
+  mf::k_gemm<mf::EPI_STATS_Y><<<grid_for(Tc, V), mf::NT, 0, s>>>(a);
   return hipGetLastError();
 }
 

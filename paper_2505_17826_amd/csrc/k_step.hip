@@ -1,0 +1,175 @@
+// Kernels of the fused trainer step (rft_ppo_clip_step), per chunk of
+// compacted rows [c0, c0 + Tc):
+//   k_step_rows   merge the chunk's log-sum-exp partials into lse, entropy and
+//                 logp, and form the per-token loss gradient c_t = dL/dlogp
+//                 (PPO-clip surrogate with the k3 KL term, Sec. 3 of the paper);
+//   k_dz_from_y   dZ = c_t (onehot(y_t) - exp(z - lse_t)) from the fp16
+//                 y = z - (row maximum over the 256-column tile) that the
+//                 forward GEMM stored, written in place as bf16 [Tc, Vpad] and
+//                 transposed [Vpad, Tc] for the weight-gradient GEMM.
+// The arithmetic of k_step_rows is that of k_merge_rows and k_loss_fwd (same
+// merge order, same per-token formula), so the step and the separate calls
+// give the same log-probs and gradients bit for bit.
+#include "rft_internal.h"
+
+namespace rft {
+
+__global__ void __launch_bounds__(256) k_step_rows(
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ row_seq,
+    const int32_t* __restrict__ n_i, const int32_t* __restrict__ meta,
+    const int32_t* __restrict__ ids, int64_t V, int64_t c0, int64_t Tc,
+    const float* __restrict__ pm, const float* __restrict__ ps, const float* __restrict__ pu,
+    int ntiles, const float* __restrict__ zy, const float* __restrict__ old,
+    const float* __restrict__ ref, const float* __restrict__ adv, LossConst c,
+    float* __restrict__ logp, float* __restrict__ ent, float* __restrict__ lse,
+    float* __restrict__ grad) {
+  const int64_t kl = (int64_t)blockIdx.x * 256 + threadIdx.x;  // row within the chunk
+  const int64_t k = c0 + kl;                                    // compacted row
+  if (kl >= Tc || k >= (int64_t)meta[0]) return;
+  const int t = rows[k];
+  float m = -INFINITY, sm = 0.f, u = 0.f;
+  for (int j = 0; j < ntiles; ++j) {
+    const int64_t o = (int64_t)j * Tc + kl;
+    lse_merge(m, sm, u, pm[o], ps[o], pu[o]);
+  }
+  const float L = m + logf(sm);
+  lse[t] = L;
+  if (ent) ent[t] = L - u / sm;
+  const int y = ids[t];
+  const bool ok = y >= 0 && (int64_t)y < V;
+  const float lp = ok ? zy[k] - L : __int_as_float(0x7fc00000);
+  logp[t] = lp;
+  float gout = 0.f;
+  if (ok) {
+    const int i = row_seq[k];
+    const float rf = ref ? ref[t] : lp;
+    TokLoss Lt = token_loss(lp, old[t], rf, adv[i], n_i[i], meta[0], meta[1], c);
+    gout = (float)(Lt.w * (double)Lt.g);
+  }
+  grad[t] = gout;
+}
+
+// One 512-thread workgroup per 256 x 256 tile of the chunk.  Thread tid owns
+// the 8 x 8 blocks (row block rb, column block cb) with cb = tid % 32 and
+// rb = tid / 32 and tid / 32 + 16: it reads eight 16-byte row pieces (a wave
+// reads two 512-byte rows per instruction), writes dZ back in place, and
+// writes each of its eight columns (eight rows = 16 bytes) into the transposed
+// LDS tile, rows of 512 bytes whose 16-byte chunk k sits at k ^ ((row/8) % 16)
+// (conflict-free 16-byte writes and reads).  Tiles wholly past the chunk's
+// count are skipped: the weight-gradient GEMM reads dZ^T only up to the count
+// rounded to 64, which the tile holding the count covers with zeros.
+constexpr int kDzT = 512;
+
+__device__ __forceinline__ uint32_t bf16_bits(float f) { return (uint32_t)f32_to_bf16(f); }
+
+__global__ void __launch_bounds__(kDzT) k_dz_from_y(
+    uint16_t* __restrict__ yz, int64_t Vpad, uint16_t* __restrict__ dzt, int64_t Tc, int64_t V,
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ ids,
+    const int32_t* __restrict__ meta, int64_t c0, const float* __restrict__ pm,
+    const float* __restrict__ lse, const float* __restrict__ grad, int ntc) {
+  __shared__ __attribute__((aligned(16))) char st[256 * 512];
+  __shared__ float rL[256], rC[256], rM[256];
+  __shared__ int rY[256];
+  const int tid = threadIdx.x;
+  const int nt = (int)(blockIdx.x % ntc), mt = (int)(blockIdx.x / ntc);
+  int64_t count = (int64_t)meta[0] - c0;
+  count = count < 0 ? 0 : (count > Tc ? Tc : count);
+  const int64_t r0 = (int64_t)mt * 256;
+  if (r0 >= count) return;
+  const int64_t n0 = (int64_t)nt * 256;
+  if (tid < 256) {
+    const int64_t r = r0 + tid;
+    float L_ = 0.f, C_ = 0.f, M_ = 0.f;
+    int Y_ = -1;
+    if (r < count) {
+      const int t = rows[c0 + r];
+      L_ = lse[t];
+      C_ = grad[t];
+      Y_ = ids[t];
+      M_ = pm[(int64_t)nt * Tc + r];
+    }
+    rL[tid] = L_ * kLog2e;
+    rC[tid] = C_;
+    rM[tid] = M_ * kLog2e;
+    rY[tid] = Y_;
+  }
+  __syncthreads();
+  const int cb = tid & 31;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int rb = (tid >> 5) + 16 * h;
+    uint16_t* src = yz + (r0 + rb * 8) * Vpad + n0 + cb * 8;
+    uint4 in[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) in[r] = *(const uint4*)(src + r * Vpad);
+    uint32_t out[8][4];  // [row][column pair], bf16 pairs
+    uint16_t colv[8][8];  // [column][row], bf16
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int rl = rb * 8 + r;
+      const float Lk = rL[rl], Ck = rC[rl], Mk = rM[rl];
+      const int Yk = rY[rl];
+      const bool rv = r0 + rl < count;
+      const uint32_t w[4] = {in[r].x, in[r].y, in[r].z, in[r].w};
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int64_t col = n0 + cb * 8 + q;
+        const uint16_t hb = (uint16_t)(w[q >> 1] >> ((q & 1) * 16));
+        const float yv = (float)__builtin_bit_cast(_Float16, hb);
+        const float p = exp2f(fmaf(yv, kLog2e, Mk - Lk));
+        float d = Ck * ((col == (int64_t)Yk ? 1.f : 0.f) - p);
+        d = (rv && col < V) ? d : 0.f;
+        colv[q][r] = (uint16_t)bf16_bits(d);
+      }
+#pragma unroll
+      for (int q2 = 0; q2 < 4; ++q2)
+        out[r][q2] = (uint32_t)colv[2 * q2][r] | ((uint32_t)colv[2 * q2 + 1][r] << 16);
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+      *(uint4*)(src + r * Vpad) = make_uint4(out[r][0], out[r][1], out[r][2], out[r][3]);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int row = cb * 8 + q;  // column of dZ = row of dZ^T
+      const int phys = rb ^ (cb & 15);
+      uint4 v;
+      v.x = (uint32_t)colv[q][0] | ((uint32_t)colv[q][1] << 16);
+      v.y = (uint32_t)colv[q][2] | ((uint32_t)colv[q][3] << 16);
+      v.z = (uint32_t)colv[q][4] | ((uint32_t)colv[q][5] << 16);
+      v.w = (uint32_t)colv[q][6] | ((uint32_t)colv[q][7] << 16);
+      *(uint4*)(st + row * 512 + phys * 16) = v;
+    }
+  }
+  __syncthreads();
+  // dZ^T rows n0 .. n0 + 255, columns r0 .. r0 + 255
+#pragma unroll 4
+  for (int it = 0; it < 16; ++it) {
+    const int c = it * kDzT + tid, row = c >> 5, k = c & 31;
+    const uint4 v = *(const uint4*)(st + row * 512 + ((k ^ ((row >> 3) & 15)) * 16));
+    *(uint4*)(dzt + (n0 + row) * Tc + r0 + k * 8) = v;
+  }
+}
+
+hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int64_t c0,
+                            int64_t Tc, const float* pm, const float* ps, const float* pu,
+                            int ntiles, const float* zy, const float* old, const float* ref,
+                            const float* adv, const LossConst& c, float* logp, float* ent,
+                            float* lse, float* grad, hipStream_t s) {
+  const int nb = (int)((Tc + 255) / 256);
+  k_step_rows<<<nb, 256, 0, s>>>(m.rows, m.row_seq, m.n_i, m.meta, ids, V, c0, Tc, pm, ps, pu,
+                                 ntiles, zy, old, ref, adv, c, logp, ent, lse, grad);
+  return hipGetLastError();
+}
+
+hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, uint16_t* dzt, int64_t Tc, int64_t V,
+                            const int32_t* rows, const int32_t* ids, const int32_t* meta,
+                            int64_t c0, const float* pm, const float* lse, const float* grad,
+                            hipStream_t s) {
+  const int ntc = (int)(Vpad / 256);
+  const int64_t nb = (Tc / 256) * ntc;
+  k_dz_from_y<<<(unsigned)nb, kDzT, 0, s>>>(yz, Vpad, dzt, Tc, V, rows, ids, meta, c0, pm, lse,
+                                            grad, ntc);
+  return hipGetLastError();
+}
+
+}  // namespace rft

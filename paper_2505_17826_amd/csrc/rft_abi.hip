@@ -5,6 +5,7 @@
 #include <stdio.h>
 
 #include <cmath>
+#include <algorithm>
 #include <limits>
 #include <string>
 
@@ -199,6 +200,60 @@ int64_t bwd_tc_for(const rft_tokens& tok, int64_t d, int64_t V, int dtype, size_
   return lo * a;
 }
 
+// Fused step (bf16): compacted hidden rows, transposed weight, per-chunk
+// log-sum-exp partials, the sampled logits, the loss partials and the chunk
+// buffers (fp16 y, then bf16 dZ, in dz).
+struct StepWs {
+  TokMeta m;
+  uint16_t *hc, *wt, *dz, *dzt, *ht;
+  float *pm, *ps, *pu, *zy;
+  LossPartial* parts;
+  int ntiles;
+  int64_t Tc, Vpad;
+  size_t bytes;
+};
+StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
+  Carver c(base);
+  StepWs w = {};
+  const int64_t T1 = tok.T > 0 ? tok.T : 1;
+  w.m = carve_tokmeta(c, tok.T, tok.n_seq);
+  w.Tc = Tc;
+  w.Vpad = round_up(V, kBf16Align);
+  w.ntiles = (int)(w.Vpad / kMfmaTileN);
+  w.hc = c.take<uint16_t>((size_t)T1 * d);
+  w.wt = c.take<uint16_t>((size_t)d * w.Vpad);
+  w.pm = c.take<float>((size_t)w.ntiles * Tc);
+  w.ps = c.take<float>((size_t)w.ntiles * Tc);
+  w.pu = c.take<float>((size_t)w.ntiles * Tc);
+  w.zy = c.take<float>((size_t)T1);
+  w.parts = c.take<LossPartial>((size_t)((T1 + 255) / 256));
+  w.dz = c.take<uint16_t>((size_t)Tc * w.Vpad);
+  w.dzt = c.take<uint16_t>((size_t)w.Vpad * Tc);
+  w.ht = c.take<uint16_t>((size_t)d * Tc);
+  w.bytes = c.bytes();
+  return w;
+}
+
+// largest row chunk (a multiple of 256) whose step workspace fits, 0 if none
+int64_t step_tc_for(const rft_tokens& tok, int64_t d, int64_t V, size_t ws_bytes) {
+  const int64_t a = kBf16Align;
+  const int64_t kmax = bwd_tc_max(tok, RFT_BF16) / a;
+  if (carve_step(nullptr, tok, d, V, a).bytes > ws_bytes) return 0;
+  int64_t lo = 1, hi = kmax;
+  while (lo < hi) {
+    int64_t mid = (lo + hi + 1) / 2;
+    if (carve_step(nullptr, tok, d, V, mid * a).bytes <= ws_bytes) lo = mid; else hi = mid - 1;
+  }
+  return lo * a;
+}
+
+size_t step_f32_bytes(const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
+  size_t a = carve_fwd(nullptr, tok, d, V, RFT_F32).bytes;
+  size_t b = carve_loss(nullptr, tok, false).bytes;
+  size_t c = carve_bwd(nullptr, tok, d, V, RFT_F32, Tc).bytes;
+  return std::max(a, std::max(b, c));
+}
+
 }  // namespace
 
 // ================================================================== ABI ==
@@ -241,15 +296,25 @@ size_t rft_workspace_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, 
       if (tc > kRecommendTc) tc = kRecommendTc;
       return carve_bwd(nullptr, *tok, d, V, dtype, tc).bytes;
     }
+    case RFT_OP_PPO_STEP: {
+      if ((dtype != RFT_F32 && dtype != RFT_BF16) || d < 1) return 0;
+      int64_t tc = bwd_tc_max(*tok, dtype);
+      if (tc > kRecommendTc) tc = kRecommendTc;
+      return dtype == RFT_BF16 ? carve_step(nullptr, *tok, d, V, tc).bytes
+                               : step_f32_bytes(*tok, d, V, tc);
+    }
     default:
       return 0;
   }
 }
 
 size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype) {
-  if (op == RFT_OP_PPO_BWD) {
+  if (op == RFT_OP_PPO_BWD || op == RFT_OP_PPO_STEP) {
     if (!tok || tok->T < 0 || tok->n_seq < 0 || V < 1 || d < 1) return 0;
     if (dtype != RFT_F32 && dtype != RFT_BF16) return 0;
+    if (op == RFT_OP_PPO_STEP)
+      return dtype == RFT_BF16 ? carve_step(nullptr, *tok, d, V, kBf16Align).bytes
+                               : step_f32_bytes(*tok, d, V, bwd_align(dtype));
     return carve_bwd(nullptr, *tok, d, V, dtype, bwd_align(dtype)).bytes;
   }
   return rft_workspace_bytes(op, tok, d, V, dtype);
@@ -359,8 +424,8 @@ rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, cons
   BwdWs w = carve_bwd(ws, *tok, d, V, dtype, Tc);
   hipStream_t s = (hipStream_t)stream;
   const int64_t T = tok->T;
+  RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
   if (T > 0) {
-    RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
     RFT_HIP(launch_zero_masked_rows(tok->mask, T, d, d_hidden, s), fn);
   }
   int64_t nchunks = T > 0 ? (T + Tc - 1) / Tc : 0;
@@ -452,6 +517,85 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
   RFT_HIP(launch_logits_fused(logits, *tok, w.m, V, old_logp,
                               params->kl_coef > 0.f ? ref_logp : nullptr, adv, c, logp, entropy,
                               lse, grad_logp, d_logits, w.parts, stats, s),
+          fn);
+  return RFT_OK;
+}
+
+rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const void* weight,
+                             int dtype, int64_t d, int64_t V, const float* old_logp,
+                             const float* ref_logp, const float* adv,
+                             const rft_ppo_params* params, float* logp, float* entropy,
+                             float* lse, float* grad_logp, float* d_hidden, float* d_weight,
+                             int32_t accumulate_dw, rft_ppo_stats* stats, void* ws,
+                             size_t ws_bytes, void* stream) {
+  const char* fn = "rft_ppo_clip_step";
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if ((st = check_hw(fn, tok->T, hidden, weight, dtype, d, V))) return st;
+  if ((st = check_params(params, fn))) return st;
+  if (!stats || !d_weight) return fail(RFT_E_NULL, "%s: stats / d_weight is NULL", fn);
+  if (tok->T > 0 && (!old_logp || !adv || !logp || !lse || !grad_logp || !d_hidden))
+    return fail(RFT_E_NULL, "%s: old_logp / adv / logp / lse / grad_logp / d_hidden is NULL", fn);
+  if (tok->T > 0 && params->kl_coef > 0.f && !ref_logp)
+    return fail(RFT_E_NULL, "%s: ref_logp is NULL with kl_coef > 0", fn);
+  const float* ref = params->kl_coef > 0.f ? ref_logp : nullptr;
+  if (dtype == RFT_F32) {
+    if ((st = check_ws(fn, ws, ws_bytes, step_f32_bytes(*tok, d, V, bwd_align(dtype))))) return st;
+    if ((st = rft_token_logprobs(tok, hidden, weight, dtype, d, V, logp, entropy, lse, ws,
+                                 ws_bytes, stream)))
+      return st;
+    if ((st = rft_ppo_clip_loss_fwd(tok, V, logp, old_logp, ref, adv, entropy, params, grad_logp,
+                                    stats, ws, ws_bytes, stream)))
+      return st;
+    return rft_ppo_clip_loss_bwd(tok, hidden, weight, dtype, d, V, lse, grad_logp, d_hidden,
+                                 d_weight, accumulate_dw, ws, ws_bytes, stream);
+  }
+  if ((st = check_ws(fn, ws, ws_bytes, carve_step(nullptr, *tok, d, V, kBf16Align).bytes)))
+    return st;
+  const int64_t Tc = step_tc_for(*tok, d, V, ws_bytes);
+  if (Tc <= 0) return fail(RFT_E_WORKSPACE, "%s: workspace too small", fn);
+  StepWs w = carve_step(ws, *tok, d, V, Tc);
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t T = tok->T;
+  const LossConst c = loss_const(params, V);
+  const uint16_t* H = (const uint16_t*)hidden;
+  const uint16_t* W = (const uint16_t*)weight;
+  const int64_t nchunks = T > 0 ? (T + Tc - 1) / Tc : 0;
+  const int32_t* cnt = w.m.meta;
+  RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
+  if (T > 0) {
+    RFT_HIP(launch_zero_masked_rows(tok->mask, T, d, d_hidden, s), fn);
+    // masked rows of the per-token outputs are 0; the chunks fill the valid rows
+    RFT_HIP(launch_fill_zero(logp, T, s), fn);
+    RFT_HIP(launch_fill_zero(lse, T, s), fn);
+    if (entropy) RFT_HIP(launch_fill_zero(entropy, T, s), fn);
+    RFT_HIP(launch_gather_rows16(H, d, w.m.rows, cnt, T, w.hc, s), fn);
+    RFT_HIP(launch_transpose_w(W, V, d, w.wt, w.Vpad, s), fn);
+  }
+  for (int64_t ci = 0; ci < nchunks; ++ci) {
+    const int64_t c0 = ci * Tc;
+    RFT_HIP(mfma_fwd_stats_y(w.hc, d, W, V, w.Vpad, w.m.rows, tok->token_ids, cnt, c0, Tc, w.pm,
+                             w.ps, w.pu, w.zy, w.dz, s),
+            fn);
+    RFT_HIP(launch_step_rows(w.m, tok->token_ids, V, c0, Tc, w.pm, w.ps, w.pu, w.ntiles, w.zy,
+                             old_logp, ref, adv, c, logp, entropy, lse, grad_logp, s),
+            fn);
+    RFT_HIP(launch_dz_from_y(w.dz, w.Vpad, w.dzt, Tc, V, w.m.rows, tok->token_ids, cnt, c0, w.pm,
+                             lse, grad_logp, s),
+            fn);
+    RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
+                            d_hidden, d, w.m.rows, c0, 0, s),
+            fn);
+    RFT_HIP(launch_transpose_hc(w.hc, d, cnt, c0, Tc, w.ht, Tc, s), fn);
+    RFT_HIP(mfma_gemm_store(w.dzt, Tc, w.ht, Tc, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight, d,
+                            nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s),
+            fn);
+  }
+  if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);
+  // loss and metrics over every row (rewrites grad_logp with the same values
+  // and 0 on masked rows)
+  RFT_HIP(launch_loss_fwd(*tok, w.m, logp, old_logp, ref, adv, entropy, c, grad_logp, w.parts,
+                          stats, s),
           fn);
   return RFT_OK;
 }

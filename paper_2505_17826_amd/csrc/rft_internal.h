@@ -195,6 +195,19 @@ hipError_t mfma_fwd_stats(const uint16_t* H, int64_t d, const uint16_t* W, int64
                           const int32_t* rows, const int32_t* ids, const int32_t* cnt,
                           int64_t rows_off, int64_t cap, float* pm, float* ps, float* pu,
                           int64_t ldp, float* zy, hipStream_t s);
+hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V,
+                            int64_t Vpad, const int32_t* rows, const int32_t* ids,
+                            const int32_t* cnt, int64_t c0, int64_t Tc, float* pm, float* ps,
+                            float* pu, float* zy, uint16_t* y, hipStream_t s);
+hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int64_t c0,
+                            int64_t Tc, const float* pm, const float* ps, const float* pu,
+                            int ntiles, const float* zy, const float* old, const float* ref,
+                            const float* adv, const LossConst& c, float* logp, float* ent,
+                            float* lse, float* grad, hipStream_t s);
+hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, uint16_t* dzt, int64_t Tc, int64_t V,
+                            const int32_t* rows, const int32_t* ids, const int32_t* meta,
+                            int64_t c0, const float* pm, const float* lse, const float* grad,
+                            hipStream_t s);
 hipError_t mfma_dz(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
                    const int32_t* cnt, int64_t c0, int64_t Tc, uint16_t* dz, uint16_t* dzt,

@@ -79,6 +79,27 @@ def gpu_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bwd_bytes=None):
             "grad_logp": cpu(grad), "stats": R.stats_to_dict(st), "dH": cpu(dH), "dW": cpu(dW)}
 
 
+def gpu_fused_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bytes=None, dW_init=None):
+    """adv -> rft_ppo_clip_step (the whole step in one call); CPU results."""
+    dev = torch.device("cuda")
+    cfg = b.cfg
+    tok = tokens_of(b)
+    H, W = b.H.to(dev).contiguous(), b.W.to(dev).contiguous()
+    adv = R.rft_group_advantages(b.rewards.to(dev), cfg.group)
+    old = torch.from_numpy(old32).to(dev)
+    ref = torch.from_numpy(ref32).to(dev)
+    ws = None
+    if ws_bytes is not None:
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    dW = None if dW_init is None else torch.from_numpy(dW_init).to(dev)
+    logp, ent, lse, grad, dH, dW, st = R.rft_ppo_clip_step(
+        tok, H, W, old, ref, adv, params_of(cfg, denom), d_weight=dW,
+        accumulate_dw=dW_init is not None, ws=ws)
+    torch.cuda.synchronize()
+    return {"adv": cpu(adv), "logp": cpu(logp), "entropy": cpu(ent), "lse": cpu(lse),
+            "grad_logp": cpu(grad), "stats": R.stats_to_dict(st), "dH": cpu(dH), "dW": cpu(dW)}
+
+
 def oracle_step(b: synth.Batch, old32, ref32, denom=0.0):
     cfg = b.cfg
     el, eh, be = oracle_eps(cfg)
