@@ -162,3 +162,61 @@ def test_fullsize_loss_only():
     assert e <= TOL_GRAD_FRO, e
     masked = np.nonzero(~mk)[0][:16]
     assert torch.all(dl[torch.as_tensor(masked, device=DEV)] == 0)
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3])
+def test_fullsize_step(cid):
+    """The fused step at full size in the benchmark's configuration.  old / ref
+    log-probs are synthetic (independent of the HIP path); the oracle computes
+    sampled rows of logp / entropy / lse, their per-token gradient and their
+    rows of dH on its own; dW is checked by its zero column sums and against
+    the separate backward call of the library on the step's own lse and
+    gradient (a consistency check between the two formulations)."""
+    cfg = synth.config(cid)
+    print(f"[fullsize-step] {cfg.name}", flush=True)
+    b = synth.make_batch(cfg, DEV)
+    tok = R.Tokens(b.seq_start, b.mask, b.ids)
+    T, d, V = b.T, cfg.d, cfg.V
+    m = b.mask.bool()
+    lp0 = -math.log(V)
+    old = torch.where(m, lp0 + synth.extra_normal(T, (cid, 3), DEV, std=1.0), torch.zeros(T, device=DEV))
+    ref = torch.where(m, old + synth.extra_normal(T, (cid, 4), DEV, std=0.1), torch.zeros(T, device=DEV))
+    adv = R.rft_group_advantages(b.rewards, cfg.group)
+    ws = _ws(R.RFT_OP_PPO_STEP, tok, d, V, R.RFT_BF16)
+    logp, ent, lse, grad, dH, dW, st = R.rft_ppo_clip_step(tok, b.H, b.W, old, ref, adv,
+                                                           params_of(cfg), ws=ws)
+    torch.cuda.synchronize()
+    s = R.stats_to_dict(st)
+    cnt = O.token_counts(b.mask, b.seq_start)
+    assert s["n_valid"] == cnt["N"] and s["n_seq_valid"] == cnt["S"] and s["n_bad_ids"] == 0
+    assert math.isfinite(s["loss"])
+    assert torch.all(logp[~m] == 0) and torch.all(grad[~m] == 0) and torch.all(dH[~m] == 0)
+    rows = _sample_rows(b.mask, 24, cid + 20)
+    olp, oent, olse = O.token_logprobs(b.H, b.W, b.ids, b.mask, rows=rows)
+    for name, g, o in (("logp", logp, olp), ("entropy", ent, oent), ("lse", lse, olse)):
+        err = np.abs(cpu(g)[rows] - o[rows]).max()
+        assert err <= TOL_LOGP, (name, err)
+    el, eh, be = oracle_eps(cfg)
+    advo = O.group_advantages(b.rewards.cpu().numpy(), cfg.group)
+    of = O.ppo_clip_loss_fwd(olp, cpu(old), cpu(ref), advo, b.mask, b.seq_start, b.ids, V, el, eh,
+                             be, cfg.agg)
+    pos = np.searchsorted(of["weights_rows"], rows)
+    keep = of["margin"][pos] >= 1e-4
+    go, gg = of["grad_logp"][rows][keep], cpu(grad)[rows][keep]
+    np.testing.assert_allclose(gg, go, rtol=1e-3, atol=1e-7 * np.abs(go).max())
+    hrows = rows[keep][:12]
+    odH, _ = O.ppo_clip_loss_bwd(b.H, b.W, olse, of["grad_logp"], b.ids, b.mask, rows=hrows,
+                                 want_dw=False)
+    e1 = rel_fro(cpu(dH)[hrows], odH[hrows])
+    dWn = dW.double()
+    colsum = dWn.sum(dim=0).norm().item()
+    assert colsum <= 2e-2 * dWn.norm().item(), (colsum, dWn.norm().item())
+    del dWn
+    dH2, dW2 = R.rft_ppo_clip_loss_bwd(tok, b.H, b.W, lse, grad,
+                                       ws=_ws(R.RFT_OP_PPO_BWD, tok, d, V, R.RFT_BF16))
+    torch.cuda.synchronize()
+    e2 = (torch.linalg.norm(dW - dW2) / torch.linalg.norm(dW2)).item()
+    e3 = (torch.linalg.norm(dH - dH2) / torch.linalg.norm(dH2)).item()
+    print(f"[fullsize-step] {cfg.name}: dH sampled rel {e1:.2e}; step vs separate backward "
+          f"dW {e2:.2e} dH {e3:.2e}", flush=True)
+    assert e1 <= TOL_GRAD_FRO and e2 <= 5e-3 and e3 <= 5e-3
