@@ -67,6 +67,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--ws-gb", type=float, default=0.0,
+                    help="workspace of the fused step in GB (default: the library's "
+                         "recommended size); a larger workspace means fewer row chunks")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GB",
                     help="only run a plain device copy of GB gigabytes (the known-size kernel "
                          "that scales the HBM byte counters) and exit")
@@ -210,8 +213,9 @@ def main():
         dW = torch.empty((V, d), **f32)
         ws_fwd = torch.empty(R.workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, tok, d, V, dt),
                              dtype=torch.uint8, device=dev)
-        ws_step = torch.empty(R.workspace_bytes(R.RFT_OP_PPO_STEP, tok, d, V, dt),
-                              dtype=torch.uint8, device=dev)
+        ws_step_bytes = (int(args.ws_gb * 1e9) if args.ws_gb > 0
+                         else R.workspace_bytes(R.RFT_OP_PPO_STEP, tok, d, V, dt))
+        ws_step = torch.empty(ws_step_bytes, dtype=torch.uint8, device=dev)
         # rollout-side log-probs for the old / reference policies (setup, untimed)
         R.rft_token_logprobs(tok, b.H, b.W, logp=logp, entropy=ent, lse=lse, ws=ws_fwd)
         old = torch.where(b.mask.bool(), logp + b.old_noise, torch.zeros_like(logp))
@@ -270,6 +274,7 @@ def main():
         "dtype": {"bf16": "bf16", "f32": "f32", "logits": "f32"}[cfg.dtype],
         "data": "synthetic (seeded; shapes and distributions of the workload, no dataset)",
         "config": {"workload": cfg.name, "n_seq": n_seq, "group": cfg.group, "T": T,
+                   "workspace_bytes": (ws_step_bytes if cfg.dtype != "logits" else None),
                    "valid_tokens": N, "V": V, "d": cfg.d, "eps": [cfg.eps_low, cfg.eps_high],
                    "kl_coef": cfg.beta, "agg": cfg.agg},
     }

@@ -157,7 +157,7 @@ struct BwdWs {
 };
 constexpr int64_t kBf16Align = 256;   // row chunk / vocabulary padding of the bf16 path
 constexpr int64_t kF32Align = 64;
-constexpr int64_t kRecommendTc = 32768;
+constexpr int64_t kRecommendTc = 65536;
 
 BwdWs carve_bwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dtype, int64_t Tc) {
   Carver c(base);
