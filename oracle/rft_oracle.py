@@ -44,6 +44,13 @@ Readings where the paper is silent (it prints no formula):
      nothing to the loss, its metrics or its gradient (they still count in N
      and n_i).
   R6 N = 0 gives loss 0 and zero gradients.
+  R10 MIX (the paper's example of a new algorithm, Sec. 4, combining online
+     GRPO with SFT on expert trajectories, mu = 0.1 by default): with
+     per-rollout expert flags the loss is (1 - mu) * (the GRPO loss of the
+     non-expert rollouts, computed on that sub-batch with its own counts) +
+     mu * (the SFT loss of the expert rollouts: the mean of -logp over their
+     valid tokens).  The GRPO metrics come from the sub-batch; the entropy
+     mean, N, S and the bad-id count cover every valid token.
 """
 from __future__ import annotations
 
@@ -193,7 +200,64 @@ def clip_thresholds(eps_low, eps_high):
 
 def ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids=None, V=None,
                       eps_low=0.2, eps_high=0.2, beta=0.0, agg=AGG_SEQ_MEAN_TOKEN_MEAN,
-                      denom_override=0.0, entropy=None):
+                      denom_override=0.0, entropy=None, is_expert=None, mix_mu=0.0):
+    if is_expert is not None:
+        return _mix_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, eps_low,
+                             eps_high, beta, agg, denom_override, entropy, is_expert, mix_mu)
+    return _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, eps_low,
+                          eps_high, beta, agg, denom_override, entropy)
+
+
+def _mix_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, eps_low, eps_high,
+                  beta, agg, denom_override, entropy, is_expert, mu):
+    """MIX loss (reading R10): the GRPO loss of the non-expert rollouts and the
+    SFT loss of the expert rollouts, weighted 1 - mu and mu."""
+    m = _int(mask) != 0
+    ss = _int(seq_start)
+    ex = _int(is_expert) != 0
+    T = m.size
+    row_expert = np.zeros(T, dtype=bool)
+    for i in range(ex.size):
+        a, b = max(0, min(ss[i], T)), max(0, min(ss[i + 1], T))
+        row_expert[a:b] = ex[i]
+    # GRPO on the sub-batch of non-expert rollouts (expert rows masked out)
+    g = _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, m & ~row_expert, seq_start, ids, V,
+                       eps_low, eps_high, beta, agg, denom_override, None)
+    # SFT on the expert rollouts: mean of -logp over their valid tokens
+    lp = _f64(logp)
+    er = np.nonzero(m & row_expert)[0]
+    good_e = np.ones(er.size, dtype=bool)
+    if ids is not None and V is not None:
+        yy = _int(ids)[er]
+        good_e = (yy >= 0) & (yy < V)
+    Ne = er.size
+    sft = float(-lp[er][good_e].sum() / Ne) if Ne else 0.0
+    grad = (1.0 - mu) * g["grad_logp"]
+    if Ne:
+        grad[er[good_e]] = -mu / Ne
+    cnt = token_counts(m, seq_start)
+    N = cnt["N"]
+    out = dict(g)
+    out.update({
+        "loss": (1.0 - mu) * g["loss"] + mu * sft,
+        "sft_loss": sft, "n_expert": Ne, "n_valid": N, "n_seq_valid": cnt["S"],
+        "n_bad_ids": g["n_bad_ids"] + int((~good_e).sum()),
+        "grad_logp": grad, "expert_rows": er[good_e],
+    })
+    if entropy is not None:
+        rows = cnt["rows"]
+        good = np.ones(rows.size, dtype=bool)
+        if ids is not None and V is not None:
+            yy = _int(ids)[rows]
+            good = (yy >= 0) & (yy < V)
+        out["entropy_mean"] = float(_f64(entropy)[rows][good].sum() / N) if N else 0.0
+    else:
+        out["entropy_mean"] = 0.0
+    return out
+
+
+def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, eps_low,
+                   eps_high, beta, agg, denom_override, entropy):
     """Clipped PPO surrogate with a k3 KL term toward the reference policy,
     aggregated over the masked tokens (Sec. 3.3.2 clip 1 +/- 0.2 and KL; Sec. 3.2
     Listing 4 loss-function call shape returning the loss and its metrics;
@@ -255,6 +319,7 @@ def ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids=No
         "ratio_mean": float(rho_s.sum() / N) if N else 0.0,
         "clipfrac": float(clipped.sum() / N) if N else 0.0,
         "n_valid": N, "n_seq_valid": S, "n_clipped": int(clipped.sum()), "n_bad_ids": n_bad,
+        "sft_loss": 0.0, "n_expert": 0,
         "grad_logp": grad, "weights_rows": rows, "weights": w,
         "clipped_rows": rows[clipped],
         "margin": np.minimum(np.abs(d32.astype(np.float64) - float(hi32)),
@@ -346,26 +411,30 @@ def bwd_logits(logits, lse, grad_logp, ids, mask, rows=None, block=256):
 
 # ------------------------------------------------------------ whole step ----
 def trainer_step(H, W, ids, mask, seq_start, rewards, group_size, old_logp, ref_logp,
-                 eps_low, eps_high, beta, agg, denom_override=0.0, adv_eps=1e-6, want_dw=True):
+                 eps_low, eps_high, beta, agg, denom_override=0.0, adv_eps=1e-6, want_dw=True,
+                 is_expert=None, mix_mu=0.0):
     """One pass of the whole path: advantages, log-probs/entropy, loss and the
     gradients to H and W."""
     adv = group_advantages(rewards, group_size, adv_eps)
     logp, ent, lse = token_logprobs(H, W, ids, mask)
     V = _f64(W).shape[0]
     fw = ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv, mask, seq_start, ids, V,
-                           eps_low, eps_high, beta, agg, denom_override, entropy=ent)
+                           eps_low, eps_high, beta, agg, denom_override, entropy=ent,
+                           is_expert=is_expert, mix_mu=mix_mu)
     dH, dW = ppo_clip_loss_bwd(H, W, lse, fw["grad_logp"], ids, mask, want_dw=want_dw)
     return {"adv": adv, "logp": logp, "entropy": ent, "lse": lse, "fwd": fw, "dH": dH, "dW": dW}
 
 
 def loss_only_step(logits, ids, mask, seq_start, rewards, group_size, old_logp, ref_logp,
-                   eps_low, eps_high, beta, agg, denom_override=0.0, adv_eps=1e-6, rows=None):
+                   eps_low, eps_high, beta, agg, denom_override=0.0, adv_eps=1e-6, rows=None,
+                   is_expert=None, mix_mu=0.0):
     """The loss-only path from given logits: log-probs, entropy, loss, dlogits.
     ``rows`` samples the dlogits rows returned; the loss always uses every row."""
     adv = group_advantages(rewards, group_size, adv_eps)
     logp, ent, lse = token_logprobs_from_logits(logits, ids, mask)
     V = logits.shape[1]
     fw = ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv, mask, seq_start, ids, V,
-                           eps_low, eps_high, beta, agg, denom_override, entropy=ent)
+                           eps_low, eps_high, beta, agg, denom_override, entropy=ent,
+                           is_expert=is_expert, mix_mu=mix_mu)
     dl = bwd_logits(logits, lse, fw["grad_logp"], ids, mask, rows=rows)
     return {"adv": adv, "logp": logp, "entropy": ent, "lse": lse, "fwd": fw, "dlogits": dl}

@@ -515,3 +515,92 @@ def test_whole_step_composition():
     # ratio 1, no KL: loss = -mean advantage over rollouts with tokens
     a = O.group_advantages(r, 2)
     assert out["fwd"]["loss"] == pytest.approx(-a.mean(), abs=1e-14)
+
+
+# ------------------------------------------------------------ MIX (R10) ----
+def test_mix_without_experts_scales_grpo():
+    """No expert rollout: the MIX loss is (1 - mu) times the GRPO loss, its
+    gradient likewise, and the GRPO metrics are the plain ones."""
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=21)
+    mu = 0.3
+    plain = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.28, 0.05, 0)
+    mix = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.28, 0.05, 0,
+                              is_expert=np.zeros(adv.size, np.uint8), mix_mu=mu)
+    assert mix["loss"] == pytest.approx((1 - mu) * plain["loss"], rel=1e-13)
+    np.testing.assert_allclose(mix["grad_logp"], (1 - mu) * plain["grad_logp"], rtol=1e-13)
+    for k in ("pg_loss", "kl_loss", "kl_mean", "ratio_mean", "clipfrac", "n_clipped"):
+        assert mix[k] == plain[k], k
+    assert mix["sft_loss"] == 0.0 and mix["n_expert"] == 0
+
+
+def test_mix_all_experts_is_sft():
+    """Every rollout is an expert one and mu = 1: the loss is the mean of -logp
+    over the valid tokens (pure-Python sum) and every valid token's gradient
+    is -1/N."""
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=22)
+    out = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.1, 0,
+                              is_expert=np.ones(adv.size, np.uint8), mix_mu=1.0)
+    vals = [-float(logp[t]) for t in range(mask.size) if mask[t]]
+    assert out["loss"] == pytest.approx(sum(vals) / len(vals), rel=1e-13)
+    assert out["sft_loss"] == pytest.approx(sum(vals) / len(vals), rel=1e-13)
+    g = out["grad_logp"]
+    assert np.all(g[mask == 0] == 0)
+    np.testing.assert_allclose(g[mask != 0], -1.0 / len(vals), rtol=1e-15)
+    assert out["n_expert"] == len(vals) and out["n_clipped"] == 0
+
+
+def test_mix_equals_two_separate_batches():
+    """A mixed batch gives (1 - mu) * the GRPO loss of its non-expert rollouts,
+    computed as a separate batch with its own counts, + mu * the mean -logp of
+    its expert rollouts, also taken apart; likewise the per-token gradient."""
+    rng = np.random.default_rng(23)
+    pad, V, mu = 9, 40, 0.1
+    lens = np.array([9, 4, 0, 7, 9, 2, 5, 8])
+    ex = np.array([0, 1, 0, 0, 1, 0, 1, 0], np.uint8)
+    ss, mask = _layout(lens, pad)
+    T = mask.size
+    logp = -rng.random(T) * 4
+    old = logp + rng.standard_normal(T) * 0.4
+    ref = logp + rng.standard_normal(T) * 0.2
+    adv = rng.standard_normal(lens.size)
+    ids = rng.integers(0, V, size=T)
+    for agg in (0, 1):
+        out = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.02, agg,
+                                  is_expert=ex, mix_mu=mu)
+        keep = np.nonzero(ex == 0)[0]
+        rows_g = np.concatenate([np.arange(i * pad, (i + 1) * pad) for i in keep])
+        ss_g, mask_g = _layout(lens[keep], pad)
+        sub = O.ppo_clip_loss_fwd(logp[rows_g], old[rows_g], ref[rows_g], adv[keep], mask_g, ss_g,
+                                  ids[rows_g], V, 0.2, 0.2, 0.02, agg)
+        rows_e = [t for i in np.nonzero(ex)[0] for t in range(i * pad, i * pad + lens[i])]
+        sft = -sum(float(logp[t]) for t in rows_e) / len(rows_e)
+        assert out["loss"] == pytest.approx((1 - mu) * sub["loss"] + mu * sft, rel=1e-12)
+        assert out["pg_loss"] == pytest.approx(sub["pg_loss"], rel=1e-12)
+        np.testing.assert_allclose(out["grad_logp"][rows_g], (1 - mu) * sub["grad_logp"],
+                                   rtol=1e-12, atol=1e-300)
+        np.testing.assert_allclose(out["grad_logp"][rows_e], -mu / len(rows_e), rtol=1e-14)
+        assert out["n_valid"] == int(lens.sum()) and out["n_expert"] == len(rows_e)
+
+
+def test_mix_finite_difference():
+    """Central differences of the MIX loss with respect to each valid logp
+    (tokens near a clip bound skipped)."""
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=24)
+    ex = (np.arange(adv.size) % 3 == 1).astype(np.uint8)
+    args = (old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.03, 0)
+    kw = dict(is_expert=ex, mix_mu=0.25)
+    out = O.ppo_clip_loss_fwd(logp, *args, **kw)
+    h = 1e-6
+    checked = 0
+    for t in np.nonzero(mask)[0]:
+        d = logp[t] - old[t]
+        if min(abs(d - math.log(1.2)), abs(d - math.log(0.8))) < 1e-3:
+            continue
+        lp1, lp2 = logp.copy(), logp.copy()
+        lp1[t] += h
+        lp2[t] -= h
+        fd = (O.ppo_clip_loss_fwd(lp1, *args, **kw)["loss"] -
+              O.ppo_clip_loss_fwd(lp2, *args, **kw)["loss"]) / (2 * h)
+        assert fd == pytest.approx(out["grad_logp"][t], rel=1e-6, abs=1e-9), t
+        checked += 1
+    assert checked > 10
