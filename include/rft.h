@@ -33,6 +33,12 @@
  *    hidden states or logits and give 0 in every per-row output.  The
  *    contents of seq_start are not validated; an invalid layout gives
  *    unspecified values but every access stays in bounds.
+ *  - Expert rollouts (MIX, Sec. 4 example of a new algorithm: online GRPO
+ *    mixed with SFT on expert trajectories).  rft_tokens.is_expert may be
+ *    NULL (every rollout is an on-policy rollout) or point to n_seq flags;
+ *    with flags the loss is (1 - mix_mu) * GRPO loss over the other rollouts
+ *    (their own normalisers) + mix_mu * SFT loss over the expert rollouts
+ *    (mean of -logp over their valid tokens).
  *  - Matrices are row-major.  hidden is [T, d], weight is [V, d] (the
  *    nn.Linear layout; logits z_t = weight . hidden_t), logits are [T, V].
  *    bf16 data requires d % 8 == 0.
@@ -47,7 +53,7 @@
 extern "C" {
 #endif
 
-#define RFT_ABI_VERSION 1
+#define RFT_ABI_VERSION 2
 
 typedef enum {
   RFT_OK = 0,
@@ -87,6 +93,7 @@ typedef struct {
   const int32_t* seq_start;  /* [n_seq + 1] row offsets                          */
   const uint8_t* mask;       /* [T] 1 = token in the objective                   */
   const int32_t* token_ids;  /* [T] sampled ids; valid rows should be in [0, V)  */
+  const uint8_t* is_expert;  /* [n_seq] 1 = expert rollout (MIX), or NULL        */
 } rft_tokens;
 
 /* (host struct) PPO-clip / KL parameters. */
@@ -97,21 +104,28 @@ typedef struct {
   int32_t agg;            /* rft_agg                                                */
   double denom_override;  /* 0: use the call's own S (or N); > 0: use this value,
                              e.g. the global count across micro-batches             */
+  float mix_mu;           /* weight of the SFT loss on expert rollouts, 0 <= mu <= 1;
+                             used only when tokens.is_expert != NULL               */
 } rft_ppo_params;
 
-/* (device struct) loss value and metrics written by the loss calls. */
+/* (device struct) loss value and metrics written by the loss calls.  With
+ * expert rollouts (MIX), pg_loss, kl_loss, kl_mean, ratio_mean and clipfrac
+ * cover the on-policy tokens (N - n_expert of them) and
+ * loss = (1 - mix_mu) * (pg_loss + kl_loss) + mix_mu * sft_loss. */
 typedef struct {
-  double loss;          /* pg_loss + kl_loss                          */
+  double loss;          /* pg_loss + kl_loss (MIX: see above)        */
   double pg_loss;       /* sum_t w_t * clipped surrogate              */
   double kl_loss;       /* sum_t w_t * beta * kl_t                    */
-  double kl_mean;       /* mean over valid tokens of kl_t             */
+  double kl_mean;       /* mean over on-policy tokens of kl_t         */
   double entropy_mean;  /* mean over valid tokens of entropy (0 if no entropy given) */
-  double ratio_mean;    /* mean over valid tokens of exp(logp - old)  */
-  double clipfrac;      /* n_clipped / N                              */
+  double ratio_mean;    /* mean over on-policy tokens of exp(logp - old) */
+  double clipfrac;      /* n_clipped / on-policy tokens               */
   int64_t n_valid;      /* N                                          */
   int64_t n_seq_valid;  /* S                                          */
   int64_t n_clipped;
   int64_t n_bad_ids;
+  double sft_loss;      /* mean of -logp over expert tokens (0 without) */
+  int64_t n_expert;     /* valid tokens of expert rollouts            */
 } rft_ppo_stats;
 
 /* Version of this ABI (RFT_ABI_VERSION). */

@@ -31,13 +31,13 @@ _i64 = ctypes.c_int64
 
 class rft_tokens(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int64), ("n_seq", ctypes.c_int64), ("seq_start", _p),
-                ("mask", _p), ("token_ids", _p)]
+                ("mask", _p), ("token_ids", _p), ("is_expert", _p)]
 
 
 class rft_ppo_params(ctypes.Structure):
     _fields_ = [("eps_low", ctypes.c_float), ("eps_high", ctypes.c_float),
                 ("kl_coef", ctypes.c_float), ("agg", ctypes.c_int32),
-                ("denom_override", ctypes.c_double)]
+                ("denom_override", ctypes.c_double), ("mix_mu", ctypes.c_float)]
 
 
 class rft_ppo_stats(ctypes.Structure):
@@ -46,7 +46,8 @@ class rft_ppo_stats(ctypes.Structure):
                 ("entropy_mean", ctypes.c_double), ("ratio_mean", ctypes.c_double),
                 ("clipfrac", ctypes.c_double), ("n_valid", ctypes.c_int64),
                 ("n_seq_valid", ctypes.c_int64), ("n_clipped", ctypes.c_int64),
-                ("n_bad_ids", ctypes.c_int64)]
+                ("n_bad_ids", ctypes.c_int64), ("sft_loss", ctypes.c_double),
+                ("n_expert", ctypes.c_int64)]
 
 
 STATS_BYTES = ctypes.sizeof(rft_ppo_stats)
@@ -136,10 +137,12 @@ def _dtype_code(t):
 
 @dataclass
 class Tokens:
-    """Token layout of one batch: rollout row offsets, action mask, sampled ids."""
+    """Token layout of one batch: rollout row offsets, action mask, sampled ids,
+    and optionally per-rollout expert flags (MIX)."""
     seq_start: torch.Tensor   # int32 [n_seq + 1]
     mask: torch.Tensor        # uint8 [T]
     token_ids: torch.Tensor   # int32 [T]
+    is_expert: torch.Tensor = None  # uint8 [n_seq] or None
 
     @property
     def T(self):
@@ -154,13 +157,19 @@ class Tokens:
                       (self.token_ids, torch.int32)):
             if t.dtype != dt or not t.is_contiguous():
                 raise TypeError("tokens: seq_start int32, mask uint8, token_ids int32, contiguous")
+        ex = None
+        if self.is_expert is not None:
+            if (self.is_expert.dtype != torch.uint8 or not self.is_expert.is_contiguous()
+                    or self.is_expert.numel() != self.n_seq):
+                raise TypeError("tokens: is_expert must be contiguous uint8 [n_seq]")
+            ex = self.is_expert.data_ptr()
         return rft_tokens(self.T, self.n_seq, self.seq_start.data_ptr(), self.mask.data_ptr(),
-                          self.token_ids.data_ptr())
+                          self.token_ids.data_ptr(), ex)
 
 
 def ppo_params(eps_low=0.2, eps_high=0.2, kl_coef=0.0, agg=RFT_AGG_SEQ_MEAN_TOKEN_MEAN,
-               denom_override=0.0) -> rft_ppo_params:
-    return rft_ppo_params(eps_low, eps_high, kl_coef, agg, denom_override)
+               denom_override=0.0, mix_mu=0.0) -> rft_ppo_params:
+    return rft_ppo_params(eps_low, eps_high, kl_coef, agg, denom_override, mix_mu)
 
 
 def stats_to_dict(buf: torch.Tensor) -> dict:

@@ -54,15 +54,18 @@ __device__ void block_reduce_partial(LossPartial& p, LossPartial* out) {
   p.kl = wave_sum_d(p.kl);
   p.ent = wave_sum_d(p.ent);
   p.ratio = wave_sum_d(p.ratio);
+  p.sft = wave_sum_d(p.sft);
   p.clipped = wave_sum_ll(p.clipped);
   p.bad = wave_sum_ll(p.bad);
+  p.expert = wave_sum_ll(p.expert);
   if (lane == 0) sh[w] = p;
   __syncthreads();
   if (threadIdx.x == 0) {
     LossPartial t = sh[0];
     for (int i = 1; i < (int)(blockDim.x >> 6); ++i) {
       t.loss += sh[i].loss; t.pg += sh[i].pg; t.klw += sh[i].klw; t.kl += sh[i].kl;
-      t.ent += sh[i].ent; t.ratio += sh[i].ratio; t.clipped += sh[i].clipped; t.bad += sh[i].bad;
+      t.ent += sh[i].ent; t.ratio += sh[i].ratio; t.sft += sh[i].sft;
+      t.clipped += sh[i].clipped; t.bad += sh[i].bad; t.expert += sh[i].expert;
     }
     *out = t;
   }
@@ -72,11 +75,12 @@ __device__ void block_reduce_partial(LossPartial& p, LossPartial* out) {
 __global__ void __launch_bounds__(256) k_loss_fwd(
     const uint8_t* __restrict__ mask, const int32_t* __restrict__ ids, const int32_t* __restrict__ kidx,
     const int32_t* __restrict__ row_seq, const int32_t* __restrict__ n_i, const int32_t* __restrict__ meta,
-    int64_t T, const float* __restrict__ logp, const float* __restrict__ old,
-    const float* __restrict__ ref, const float* __restrict__ adv, const float* __restrict__ ent,
-    LossConst c, float* __restrict__ grad, LossPartial* __restrict__ parts) {
+    int64_t T, const float* __restrict__ logp,
+    const float* __restrict__ old, const float* __restrict__ ref, const float* __restrict__ adv,
+    const float* __restrict__ ent, LossConst c, float* __restrict__ grad,
+    LossPartial* __restrict__ parts) {
   int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  LossPartial p = {0, 0, 0, 0, 0, 0, 0, 0};
+  LossPartial p = RFT_ZERO_PARTIAL;
   if (t < T) {
     int k = kidx[t];
     float gout = 0.f;
@@ -88,16 +92,9 @@ __global__ void __launch_bounds__(256) k_loss_fwd(
       } else {
         float lp = logp[t];
         float rf = ref ? ref[t] : lp;
-        TokLoss L = token_loss(lp, old[t], rf, adv[i], n_i[i], meta[0], meta[1], c);
-        double ell = (double)L.pg + (double)c.beta * (double)L.kl;
-        p.loss = L.w * ell;
-        p.pg = L.w * (double)L.pg;
-        p.klw = L.w * (double)c.beta * (double)L.kl;
-        p.kl = (double)L.kl;
-        p.ratio = (double)L.rho;
-        p.ent = ent ? (double)ent[t] : 0.0;
-        p.clipped = L.clipped ? 1 : 0;
-        gout = (float)(L.w * (double)L.g);
+        const bool ex = c.is_expert && c.is_expert[i];
+        gout = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, ent ? (double)ent[t] : 0.0, c,
+                        p);
       }
     }
     grad[t] = gout;
@@ -109,31 +106,35 @@ __global__ void __launch_bounds__(256) k_loss_fwd(
 __global__ void __launch_bounds__(1024) k_loss_final(const LossPartial* __restrict__ parts, int n,
                                                      const int32_t* __restrict__ meta,
                                                      rft_ppo_stats* __restrict__ st) {
-  LossPartial p = {0, 0, 0, 0, 0, 0, 0, 0};
+  LossPartial p = RFT_ZERO_PARTIAL;
   // each thread sums a contiguous run, in order
   int per = (n + 1023) / 1024;
   int a = threadIdx.x * per, b = min(n, a + per);
   for (int i = a; i < b; ++i) {
     p.loss += parts[i].loss; p.pg += parts[i].pg; p.klw += parts[i].klw; p.kl += parts[i].kl;
-    p.ent += parts[i].ent; p.ratio += parts[i].ratio; p.clipped += parts[i].clipped; p.bad += parts[i].bad;
+    p.ent += parts[i].ent; p.ratio += parts[i].ratio; p.sft += parts[i].sft;
+    p.clipped += parts[i].clipped; p.bad += parts[i].bad; p.expert += parts[i].expert;
   }
   __shared__ LossPartial out;
   block_reduce_partial(p, &out);
   __syncthreads();
   if (threadIdx.x == 0) {
-    int N = meta[0], S = meta[1];
-    double inv = N > 0 ? 1.0 / (double)N : 0.0;
+    const int N = meta[0], S = meta[1], Ne = meta[2], Ng = N - Ne;
+    const double inv = N > 0 ? 1.0 / (double)N : 0.0;
+    const double invg = Ng > 0 ? 1.0 / (double)Ng : 0.0;
     st->loss = N > 0 ? out.loss : 0.0;
     st->pg_loss = N > 0 ? out.pg : 0.0;
     st->kl_loss = N > 0 ? out.klw : 0.0;
-    st->kl_mean = out.kl * inv;
+    st->kl_mean = out.kl * invg;
     st->entropy_mean = out.ent * inv;
-    st->ratio_mean = out.ratio * inv;
-    st->clipfrac = (double)out.clipped * inv;
+    st->ratio_mean = out.ratio * invg;
+    st->clipfrac = (double)out.clipped * invg;
     st->n_valid = N;
     st->n_seq_valid = S;
     st->n_clipped = out.clipped;
     st->n_bad_ids = out.bad;
+    st->sft_loss = Ne > 0 ? out.sft / (double)Ne : 0.0;
+    st->n_expert = Ne;
   }
 }
 
@@ -149,8 +150,8 @@ hipError_t launch_loss_fwd(const rft_tokens& tok, const TokMeta& m, const float*
                            hipStream_t s) {
   int nb = (int)((tok.T + 255) / 256);
   if (nb > 0)
-    k_loss_fwd<<<nb, 256, 0, s>>>(tok.mask, tok.token_ids, m.kidx, m.row_seq, m.n_i, m.meta, tok.T,
-                                  logp, old, ref, adv, ent, c, grad, parts);
+    k_loss_fwd<<<nb, 256, 0, s>>>(tok.mask, tok.token_ids, m.kidx, m.row_seq, m.n_i, m.meta,
+                                  tok.T, logp, old, ref, adv, ent, c, grad, parts);
   return launch_loss_final(parts, nb, m.meta, st, s);
 }
 

@@ -203,7 +203,7 @@ __global__ void __launch_bounds__(NT) k_logits_fused(
       if (ent) ent[t] = 0.f;
       if (lse_out) lse_out[t] = 0.f;
       if (grad_out) grad_out[t] = 0.f;
-      parts[t] = LossPartial{0, 0, 0, 0, 0, 0, 0, 0};
+      parts[t] = RFT_ZERO_PARTIAL;
     }
     return;
   }
@@ -218,22 +218,15 @@ __global__ void __launch_bounds__(NT) k_logits_fused(
     logp[t] = lp;
     if (ent) ent[t] = H;
     if (lse_out) lse_out[t] = L;
-    LossPartial p = {0, 0, 0, 0, 0, 0, 0, 0};
+    LossPartial p = RFT_ZERO_PARTIAL;
     float c = 0.f;
     if (!ok) {
       p.bad = 1;
     } else {
       int i = row_seq[k];
       float rf = ref ? ref[t] : lp;
-      TokLoss Lt = token_loss(lp, old[t], rf, adv[i], n_i[i], meta[0], meta[1], cst);
-      p.loss = Lt.w * ((double)Lt.pg + (double)cst.beta * (double)Lt.kl);
-      p.pg = Lt.w * (double)Lt.pg;
-      p.klw = Lt.w * (double)cst.beta * (double)Lt.kl;
-      p.kl = (double)Lt.kl;
-      p.ratio = (double)Lt.rho;
-      p.ent = (double)H;
-      p.clipped = Lt.clipped ? 1 : 0;
-      c = (float)(Lt.w * (double)Lt.g);
+      const bool ex = cst.is_expert && cst.is_expert[i];
+      c = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, (double)H, cst, p);
     }
     if (grad_out) grad_out[t] = c;
     parts[t] = p;
@@ -307,7 +300,7 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
       if (ent) ent[t] = 0.f;
       if (lse_out) lse_out[t] = 0.f;
       if (grad_out) grad_out[t] = 0.f;
-      parts[t] = LossPartial{0, 0, 0, 0, 0, 0, 0, 0};
+      parts[t] = RFT_ZERO_PARTIAL;
     }
     return;
   }
@@ -346,22 +339,15 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
     logp[t] = lp;
     if (ent) ent[t] = H;
     if (lse_out) lse_out[t] = L;
-    LossPartial p = {0, 0, 0, 0, 0, 0, 0, 0};
+    LossPartial p = RFT_ZERO_PARTIAL;
     float c = 0.f;
     if (!ok) {
       p.bad = 1;
     } else {
       int i = row_seq[k];
       float rf = ref ? ref[t] : lp;
-      TokLoss Lt = token_loss(lp, old[t], rf, adv[i], n_i[i], meta[0], meta[1], cst);
-      p.loss = Lt.w * ((double)Lt.pg + (double)cst.beta * (double)Lt.kl);
-      p.pg = Lt.w * (double)Lt.pg;
-      p.klw = Lt.w * (double)cst.beta * (double)Lt.kl;
-      p.kl = (double)Lt.kl;
-      p.ratio = (double)Lt.rho;
-      p.ent = (double)H;
-      p.clipped = Lt.clipped ? 1 : 0;
-      c = (float)(Lt.w * (double)Lt.g);
+      const bool ex = cst.is_expert && cst.is_expert[i];
+      c = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, (double)H, cst, p);
     }
     if (grad_out) grad_out[t] = c;
     parts[t] = p;

@@ -2,7 +2,8 @@
 // compacted rows [c0, c0 + Tc):
 //   k_step_rows   merge the chunk's log-sum-exp partials into lse, entropy and
 //                 logp, and form the per-token loss gradient c_t = dL/dlogp
-//                 (PPO-clip surrogate with the k3 KL term, Sec. 3 of the paper);
+//                 (PPO-clip surrogate with the k3 KL term, Sec. 3 of the paper,
+//                 and the on-policy / expert split of the MIX loss);
 //   k_dz_from_y   dZ = c_t (onehot(y_t) - exp(z - lse_t)) from the fp16
 //                 y = z - (row maximum over the 256-column tile) that the
 //                 forward GEMM stored, written in place as bf16 [Tc, Vpad] and
@@ -43,8 +44,9 @@ __global__ void __launch_bounds__(256) k_step_rows(
   if (ok) {
     const int i = row_seq[k];
     const float rf = ref ? ref[t] : lp;
-    TokLoss Lt = token_loss(lp, old[t], rf, adv[i], n_i[i], meta[0], meta[1], c);
-    gout = (float)(Lt.w * (double)Lt.g);
+    const bool ex = c.is_expert && c.is_expert[i];
+    LossPartial p = RFT_ZERO_PARTIAL;
+    gout = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, 0.0, c, p);
   }
   grad[t] = gout;
 }

@@ -68,6 +68,7 @@ __global__ void __launch_bounds__(kThreads) k_seq_count(const uint8_t* __restric
 // One block: block counts -> exclusive offsets (in place), N and S.
 __global__ void __launch_bounds__(kThreads) k_scan(int32_t* __restrict__ blk, int nblk,
                                                    const int32_t* __restrict__ n_i, int64_t n_seq,
+                                                   const uint8_t* __restrict__ is_expert,
                                                    int32_t* __restrict__ meta) {
   __shared__ int sh[kThreads];
   __shared__ int red[4];
@@ -79,14 +80,22 @@ __global__ void __launch_bounds__(kThreads) k_scan(int32_t* __restrict__ blk, in
     if (b < nblk) blk[b] = carry + ex;
     carry += block_sum_int(v, red);
   }
-  int s = 0;
-  for (int64_t i = threadIdx.x; i < n_seq; i += kThreads) s += n_i[i] > 0 ? 1 : 0;
+  int s = 0, ne = 0, se = 0;
+  for (int64_t i = threadIdx.x; i < n_seq; i += kThreads) {
+    s += n_i[i] > 0 ? 1 : 0;
+    if (is_expert && is_expert[i]) {
+      ne += n_i[i];
+      se += n_i[i] > 0 ? 1 : 0;
+    }
+  }
   s = block_sum_int(s, red);
+  ne = block_sum_int(ne, red);
+  se = block_sum_int(se, red);
   if (threadIdx.x == 0) {
     meta[0] = carry;
     meta[1] = s;
-    meta[2] = 0;
-    meta[3] = 0;
+    meta[2] = ne;
+    meta[3] = se;
   }
 }
 
@@ -151,7 +160,7 @@ hipError_t launch_tokmeta(const rft_tokens& tok, const TokMeta& m, hipStream_t s
   int nblk = (int)((T + kK0Rows - 1) / kK0Rows);
   if (nblk > 0) k_block_count<<<nblk, kThreads, 0, s>>>(tok.mask, T, m.blk);
   if (n_seq > 0) k_seq_count<<<(unsigned)n_seq, kThreads, 0, s>>>(tok.mask, tok.seq_start, n_seq, T, m.n_i);
-  k_scan<<<1, kThreads, 0, s>>>(m.blk, nblk, m.n_i, n_seq, m.meta);
+  k_scan<<<1, kThreads, 0, s>>>(m.blk, nblk, m.n_i, n_seq, tok.is_expert, m.meta);
   if (nblk > 0 && n_seq > 0)
     k_scatter<<<nblk, kThreads, 0, s>>>(tok.mask, tok.seq_start, n_seq, T, m.blk, m.rows,
                                         m.row_seq, m.kidx);

@@ -82,6 +82,8 @@ rft_status check_params(const rft_ppo_params* p, const char* fn) {
     return fail(RFT_E_PARAM, "%s: agg=%d unknown", fn, p->agg);
   if (!(p->denom_override >= 0.0) || !std::isfinite(p->denom_override))
     return fail(RFT_E_PARAM, "%s: denom_override=%g must be finite and >= 0", fn, p->denom_override);
+  if (!(p->mix_mu >= 0.f && p->mix_mu <= 1.f))
+    return fail(RFT_E_PARAM, "%s: mix_mu=%g must be in [0, 1]", fn, (double)p->mix_mu);
   return RFT_OK;
 }
 
@@ -97,6 +99,16 @@ LossConst loss_const(const rft_ppo_params* p, int64_t V) {
                               : -std::numeric_limits<float>::infinity();
   c.thr_hi = std::isfinite(p->eps_high) ? (float)std::log1p((double)p->eps_high)
                                         : std::numeric_limits<float>::infinity();
+  c.is_expert = nullptr;
+  c.mix = 0;
+  c.mu = p->mix_mu;
+  return c;
+}
+
+LossConst loss_const(const rft_ppo_params* p, int64_t V, const rft_tokens& tok) {
+  LossConst c = loss_const(p, V);
+  c.is_expert = tok.is_expert;
+  c.mix = tok.is_expert ? 1 : 0;
   return c;
 }
 
@@ -399,7 +411,7 @@ rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* 
   w = carve_loss(ws, *tok, false);
   hipStream_t s = (hipStream_t)stream;
   RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
-  LossConst c = loss_const(params, V);
+  LossConst c = loss_const(params, V, *tok);
   RFT_HIP(launch_loss_fwd(*tok, w.m, logp, old_logp, params->kl_coef > 0.f ? ref_logp : nullptr,
                           adv, entropy, c, grad_logp, w.parts, stats, s),
           fn);
@@ -513,7 +525,7 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
   w = carve_loss(ws, *tok, true);
   hipStream_t s = (hipStream_t)stream;
   RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
-  LossConst c = loss_const(params, V);
+  LossConst c = loss_const(params, V, *tok);
   RFT_HIP(launch_logits_fused(logits, *tok, w.m, V, old_logp,
                               params->kl_coef > 0.f ? ref_logp : nullptr, adv, c, logp, entropy,
                               lse, grad_logp, d_logits, w.parts, stats, s),
@@ -557,7 +569,7 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
   StepWs w = carve_step(ws, *tok, d, V, Tc);
   hipStream_t s = (hipStream_t)stream;
   const int64_t T = tok->T;
-  const LossConst c = loss_const(params, V);
+  const LossConst c = loss_const(params, V, *tok);
   const uint16_t* H = (const uint16_t*)hidden;
   const uint16_t* W = (const uint16_t*)weight;
   const int64_t nchunks = T > 0 ? (T + Tc - 1) / Tc : 0;

@@ -110,7 +110,7 @@ struct TokMeta {
   int32_t* kidx;     // [T]  compacted index of row t, -1 if masked
   int32_t* n_i;      // [n_seq] valid tokens per rollout
   int32_t* blk;      // [nblk] per-block counts, then offsets
-  int32_t* meta;     // [4]  N, S
+  int32_t* meta;     // [4]  N, S, expert tokens, expert rollouts with tokens
 };
 
 struct Carver {
@@ -139,6 +139,9 @@ struct LossConst {
   int agg;
   double denom;           // 0 = use S or N
   int64_t V;
+  int mix;                // 1: expert flags given (MIX loss)
+  float mu;               // SFT weight of the MIX loss
+  const uint8_t* is_expert;  // [n_seq] device flags, or nullptr
 };
 
 // Per-token PPO-clip + k3 KL terms.  Returns false for an out-of-range id.
@@ -174,9 +177,40 @@ __device__ __forceinline__ TokLoss token_loss(float lp, float old, float ref, fl
 
 // Partial sums of one block of tokens, reduced in a fixed order.
 struct LossPartial {
-  double loss, pg, klw, kl, ent, ratio;
-  long long clipped, bad;
+  double loss, pg, klw, kl, ent, ratio, sft;
+  long long clipped, bad, expert;
 };
+
+// Loss terms of one valid row whose id is in range: adds its terms to p and
+// returns c_t = d loss / d logp.  meta = {N, S, expert tokens, expert rollouts
+// with tokens}; the on-policy (GRPO) part uses the counts without the expert
+// rollouts, scaled by 1 - mu under MIX; an expert row contributes mu * (-logp)
+// / (expert tokens) (the SFT term of the MIX loss).
+__device__ __forceinline__ float row_loss(float lp, float old, float ref, float A, int n_seq_i,
+                                          bool expert, const int32_t* meta, double ent,
+                                          const LossConst& c, LossPartial& p) {
+  p.ent = ent;
+  if (c.mix && expert) {
+    const int Ne = meta[2];
+    const double inv = Ne > 0 ? 1.0 / (double)Ne : 0.0;
+    p.sft = -(double)lp;
+    p.loss = (double)c.mu * p.sft * inv;
+    p.expert = 1;
+    return (float)(-(double)c.mu * inv);
+  }
+  const int Ng = meta[0] - meta[2], Sg = meta[1] - meta[3];
+  TokLoss L = token_loss(lp, old, ref, A, n_seq_i, Ng, Sg, c);
+  const double scale = c.mix ? 1.0 - (double)c.mu : 1.0;
+  p.loss = scale * (L.w * ((double)L.pg + (double)c.beta * (double)L.kl));
+  p.pg = L.w * (double)L.pg;
+  p.klw = L.w * (double)c.beta * (double)L.kl;
+  p.kl = (double)L.kl;
+  p.ratio = (double)L.rho;
+  p.clipped = L.clipped ? 1 : 0;
+  return (float)(scale * L.w * (double)L.g);
+}
+
+#define RFT_ZERO_PARTIAL LossPartial{0, 0, 0, 0, 0, 0, 0, 0, 0, 0}
 
 hipError_t launch_loss_final(const LossPartial* parts, int nparts, const int32_t* meta,
                              rft_ppo_stats* stats, hipStream_t s);

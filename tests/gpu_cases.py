@@ -35,14 +35,16 @@ def cpu(t):
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
-def tokens_of(b: synth.Batch) -> R.Tokens:
+def tokens_of(b: synth.Batch, is_expert=None) -> R.Tokens:
     dev = torch.device("cuda")
+    ex = None if is_expert is None else torch.from_numpy(np.asarray(is_expert, np.uint8)).to(dev)
     return R.Tokens(b.seq_start.to(dev).contiguous(), b.mask.to(dev).contiguous(),
-                    b.ids.to(dev).contiguous())
+                    b.ids.to(dev).contiguous(), ex)
 
 
-def params_of(cfg: synth.Config, denom=0.0, agg=None) -> R.rft_ppo_params:
-    return R.ppo_params(cfg.eps_low, cfg.eps_high, cfg.beta, cfg.agg if agg is None else agg, denom)
+def params_of(cfg: synth.Config, denom=0.0, agg=None, mix_mu=0.0) -> R.rft_ppo_params:
+    return R.ppo_params(cfg.eps_low, cfg.eps_high, cfg.beta, cfg.agg if agg is None else agg, denom,
+                        mix_mu)
 
 
 def oracle_eps(cfg):
@@ -58,18 +60,18 @@ def perturbed_logprobs(logp_fp64, batch: synth.Batch):
     return old, ref
 
 
-def gpu_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bwd_bytes=None):
+def gpu_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bwd_bytes=None, is_expert=None, mu=0.0):
     """adv -> log-probs -> loss -> backward through the binding; CPU results."""
     dev = torch.device("cuda")
     cfg = b.cfg
-    tok = tokens_of(b)
+    tok = tokens_of(b, is_expert)
     H, W = b.H.to(dev).contiguous(), b.W.to(dev).contiguous()
     adv = R.rft_group_advantages(b.rewards.to(dev), cfg.group)
     logp, ent, lse = R.rft_token_logprobs(tok, H, W)
     old = torch.from_numpy(old32).to(dev)
     ref = torch.from_numpy(ref32).to(dev)
-    grad, st = R.rft_ppo_clip_loss_fwd(tok, cfg.V, logp, old, ref, adv, params_of(cfg, denom),
-                                       entropy=ent)
+    grad, st = R.rft_ppo_clip_loss_fwd(tok, cfg.V, logp, old, ref, adv,
+                                       params_of(cfg, denom, mix_mu=mu), entropy=ent)
     ws = None
     if ws_bwd_bytes is not None:
         ws = torch.empty(ws_bwd_bytes, dtype=torch.uint8, device=dev)
@@ -79,11 +81,12 @@ def gpu_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bwd_bytes=None):
             "grad_logp": cpu(grad), "stats": R.stats_to_dict(st), "dH": cpu(dH), "dW": cpu(dW)}
 
 
-def gpu_fused_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bytes=None, dW_init=None):
+def gpu_fused_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bytes=None, dW_init=None,
+                   is_expert=None, mu=0.0):
     """adv -> rft_ppo_clip_step (the whole step in one call); CPU results."""
     dev = torch.device("cuda")
     cfg = b.cfg
-    tok = tokens_of(b)
+    tok = tokens_of(b, is_expert)
     H, W = b.H.to(dev).contiguous(), b.W.to(dev).contiguous()
     adv = R.rft_group_advantages(b.rewards.to(dev), cfg.group)
     old = torch.from_numpy(old32).to(dev)
@@ -93,19 +96,19 @@ def gpu_fused_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bytes=None, dW_in
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     dW = None if dW_init is None else torch.from_numpy(dW_init).to(dev)
     logp, ent, lse, grad, dH, dW, st = R.rft_ppo_clip_step(
-        tok, H, W, old, ref, adv, params_of(cfg, denom), d_weight=dW,
+        tok, H, W, old, ref, adv, params_of(cfg, denom, mix_mu=mu), d_weight=dW,
         accumulate_dw=dW_init is not None, ws=ws)
     torch.cuda.synchronize()
     return {"adv": cpu(adv), "logp": cpu(logp), "entropy": cpu(ent), "lse": cpu(lse),
             "grad_logp": cpu(grad), "stats": R.stats_to_dict(st), "dH": cpu(dH), "dW": cpu(dW)}
 
 
-def oracle_step(b: synth.Batch, old32, ref32, denom=0.0):
+def oracle_step(b: synth.Batch, old32, ref32, denom=0.0, is_expert=None, mu=0.0):
     cfg = b.cfg
     el, eh, be = oracle_eps(cfg)
     return O.trainer_step(b.H, b.W, b.ids, b.mask, b.seq_start, b.rewards, cfg.group,
                           old32.astype(np.float64), ref32.astype(np.float64), el, eh, be, cfg.agg,
-                          denom)
+                          denom, is_expert=is_expert, mix_mu=f32(mu))
 
 
 def compare_step(g, o, b: synth.Batch, check_bwd=True):
@@ -129,6 +132,11 @@ def compare_step(g, o, b: synth.Batch, check_bwd=True):
     bad = np.abs(gr - orr) > 1e-3 * np.abs(orr) + 1e-7 * scale
     assert not bad.any(), f"grad_logp: {bad.sum()} tokens off"
     assert abs(st["n_clipped"] - of["n_clipped"]) <= int((~keep).sum())
+    assert st["n_expert"] == of["n_expert"]
+    assert abs(st["sft_loss"] - of["sft_loss"]) <= TOL_LOSS_REL * abs(of["sft_loss"]) + TOL_LOSS_ABS
+    er = of.get("expert_rows")
+    if er is not None and er.size:
+        np.testing.assert_allclose(g["grad_logp"][er], of["grad_logp"][er], rtol=1e-6)
     if check_bwd:
         assert np.all(g["dH"][~m] == 0.0), "dH masked rows must be exactly 0"
         assert rel_fro(g["dH"], o["dH"]) <= TOL_GRAD_FRO, rel_fro(g["dH"], o["dH"])

@@ -31,7 +31,9 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     L = R.lib()
-    assert L.rft_abi_version() == 1
+    hdr = open(os.path.join(ROOT, "include", "rft.h")).read()
+    ver = int(re.search(r"#define RFT_ABI_VERSION (\d+)", hdr).group(1))
+    assert L.rft_abi_version() == ver
     for s in range(8):
         assert L.rft_status_str(s)
     assert L.rft_status_str(99) == b"unknown status"
@@ -96,7 +98,8 @@ def test_argument_validation_returns_codes():
     for p, code in [(P(eps_low=-0.1), R.RFT_E_PARAM), (P(eps_low=1.5), R.RFT_E_PARAM),
                     (P(eps_high=-1.0), R.RFT_E_PARAM), (P(eps_high=float("nan")), R.RFT_E_PARAM),
                     (P(kl_coef=-1.0), R.RFT_E_PARAM), (P(kl_coef=float("inf")), R.RFT_E_PARAM),
-                    (P(agg=5), R.RFT_E_PARAM), (P(denom_override=-2.0), R.RFT_E_PARAM)]:
+                    (P(agg=5), R.RFT_E_PARAM), (P(denom_override=-2.0), R.RFT_E_PARAM),
+                    (P(mix_mu=-0.1), R.RFT_E_PARAM), (P(mix_mu=1.5), R.RFT_E_PARAM)]:
         assert L.rft_ppo_clip_loss_fwd(*base, ctypes.byref(p), *tail) == code
     assert L.rft_ppo_clip_loss_fwd(*base, None, *tail) == R.RFT_E_NULL
     # KL requested without reference log-probs
