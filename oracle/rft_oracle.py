@@ -51,6 +51,14 @@ Readings where the paper is silent (it prints no formula):
      mu * (the SFT loss of the expert rollouts: the mean of -logp over their
      valid tokens).  The GRPO metrics come from the sub-batch; the entropy
      mean, N, S and the bad-id count cover every valid token.
+  R11 Entropy bonus (the paper logs the actor's entropy as the signal of
+     exploration that diversity shaping keeps high, Sec. 3.4.2, and prints no
+     formula for a bonus): with coefficient c_H >= 0 the loss gains
+     -c_H * sum_t w_t H_t over the tokens of the PPO term, with that term's
+     aggregation weights w_t (under MIX: the non-expert sub-batch, scaled by
+     1 - mu like the rest of the GRPO part); ``entropy_loss`` reports
+     sum_t w_t H_t.  Its gradient reaches the logits through
+     dH/dz_j = -p_j (z_j - sum_k p_k z_k).
 """
 from __future__ import annotations
 
@@ -200,16 +208,20 @@ def clip_thresholds(eps_low, eps_high):
 
 def ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids=None, V=None,
                       eps_low=0.2, eps_high=0.2, beta=0.0, agg=AGG_SEQ_MEAN_TOKEN_MEAN,
-                      denom_override=0.0, entropy=None, is_expert=None, mix_mu=0.0):
+                      denom_override=0.0, entropy=None, is_expert=None, mix_mu=0.0,
+                      entropy_coef=0.0):
+    if entropy_coef > 0 and entropy is None:
+        raise ValueError("the entropy bonus needs the entropies")
     if is_expert is not None:
         return _mix_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, eps_low,
-                             eps_high, beta, agg, denom_override, entropy, is_expert, mix_mu)
+                             eps_high, beta, agg, denom_override, entropy, is_expert, mix_mu,
+                             entropy_coef)
     return _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, eps_low,
-                          eps_high, beta, agg, denom_override, entropy)
+                          eps_high, beta, agg, denom_override, entropy, entropy_coef)
 
 
 def _mix_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, eps_low, eps_high,
-                  beta, agg, denom_override, entropy, is_expert, mu):
+                  beta, agg, denom_override, entropy, is_expert, mu, entropy_coef=0.0):
     """MIX loss (reading R10): the GRPO loss of the non-expert rollouts and the
     SFT loss of the expert rollouts, weighted 1 - mu and mu."""
     m = _int(mask) != 0
@@ -222,7 +234,7 @@ def _mix_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, ep
         row_expert[a:b] = ex[i]
     # GRPO on the sub-batch of non-expert rollouts (expert rows masked out)
     g = _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, m & ~row_expert, seq_start, ids, V,
-                       eps_low, eps_high, beta, agg, denom_override, None)
+                       eps_low, eps_high, beta, agg, denom_override, entropy, entropy_coef)
     # SFT on the expert rollouts: mean of -logp over their valid tokens
     lp = _f64(logp)
     er = np.nonzero(m & row_expert)[0]
@@ -243,6 +255,7 @@ def _mix_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, ep
         "sft_loss": sft, "n_expert": Ne, "n_valid": N, "n_seq_valid": cnt["S"],
         "n_bad_ids": g["n_bad_ids"] + int((~good_e).sum()),
         "grad_logp": grad, "expert_rows": er[good_e],
+        "grad_entropy": (1.0 - mu) * g["grad_entropy"],
     })
     if entropy is not None:
         rows = cnt["rows"]
@@ -257,14 +270,15 @@ def _mix_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, ep
 
 
 def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, eps_low,
-                   eps_high, beta, agg, denom_override, entropy):
+                   eps_high, beta, agg, denom_override, entropy, entropy_coef=0.0):
     """Clipped PPO surrogate with a k3 KL term toward the reference policy,
     aggregated over the masked tokens (Sec. 3.3.2 clip 1 +/- 0.2 and KL; Sec. 3.2
     Listing 4 loss-function call shape returning the loss and its metrics;
     readings R1, R2, R4, R5, R6).
 
-    Returns a dict with the loss, its parts, the statistics and ``grad_logp``
-    (d loss / d logp per row, 0 on masked rows).
+    Returns a dict with the loss, its parts, the statistics, ``grad_logp``
+    (d loss / d logp per row, 0 on masked rows) and ``grad_entropy`` (minus
+    d loss / d H per row: the entropy-bonus coefficient, reading R11).
     """
     cnt = token_counts(mask, seq_start)
     rows, seq, n, N, S = cnt["rows"], cnt["seq"], cnt["n"], cnt["N"], cnt["S"]
@@ -311,8 +325,15 @@ def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, e
 
     grad = np.zeros(T)
     grad[rows] = c
+    # entropy bonus (R11): -c_H sum_t w_t H_t over the rows with a valid id
+    ent_rows = np.where(good, _f64(entropy)[rows], 0.0) if entropy is not None else None
+    ent_w = float((w * ent_rows).sum()) if entropy is not None else 0.0
+    grad_ent = np.zeros(T)
+    if entropy_coef > 0:
+        grad_ent[rows] = np.where(good, entropy_coef * w, 0.0)
     out = {
-        "loss": float((w * ell).sum()),
+        "loss": float((w * ell).sum()) - entropy_coef * ent_w,
+        "entropy_loss": ent_w, "grad_entropy": grad_ent,
         "pg_loss": float((w * pg).sum()),
         "kl_loss": float((w * beta * kl).sum()),
         "kl_mean": float(kl.sum() / N) if N else 0.0,
@@ -334,19 +355,26 @@ def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, e
 
 
 # -------------------------------------------------------------- backward ----
-def logit_grad_rows(z, y, lse, c):
-    """d loss / d z for a block of rows: ``c (onehot(y) - exp(z - lse))``."""
+def logit_grad_rows(z, y, lse, c, e=None, ent=None):
+    """d loss / d z for a block of rows: ``c (onehot(y) - p)`` with
+    ``p = exp(z - lse)``, plus, with the entropy bonus (R11), ``e`` times
+    ``-dH/dz = p (z - mu)``, ``mu = lse - H`` the softmax mean of z."""
     p = np.exp(z - lse[:, None])
     dz = -p
     ok = np.nonzero((y >= 0) & (y < z.shape[1]))[0]
     dz[ok, y[ok]] += 1.0
-    return c[:, None] * dz
+    out = c[:, None] * dz
+    if e is not None:
+        mu = lse - ent
+        out += e[:, None] * p * (z - mu[:, None])
+    return out
 
 
 def ppo_clip_loss_bwd(H, W, lse, grad_logp, ids, mask, rows=None, dw_rows=None, block=256,
-                      want_dw=True):
-    """Backward through the policy head: ``dZ = c (onehot(y) - softmax(z))``,
-    ``dH = dZ W`` and ``dW = dZ^T H`` over the valid rows.
+                      want_dw=True, grad_entropy=None, entropy=None):
+    """Backward through the policy head: ``dZ = c (onehot(y) - softmax(z))``
+    (plus the entropy-bonus term when ``grad_entropy`` and ``entropy`` are
+    given), ``dH = dZ W`` and ``dW = dZ^T H`` over the valid rows.
 
     ``rows`` restricts which rows of dH are returned (others 0).  ``dw_rows``
     returns only those rows of dW, each summed over every valid token, so a
@@ -358,14 +386,20 @@ def ppo_clip_loss_bwd(H, W, lse, grad_logp, ids, mask, rows=None, dw_rows=None, 
     y = _int(ids)
     L = _f64(lse)
     C = _f64(grad_logp)
+    E = _f64(grad_entropy) if grad_entropy is not None else None
+    Hn = _f64(entropy) if grad_entropy is not None else None
     T = m.size
+
+    def eh(rr):
+        return (None, None) if E is None else (E[rr], Hn[rr])
+
     valid = np.nonzero(m)[0]
     dH = np.zeros((T, d))
     want = valid if rows is None else np.asarray([r for r in _int(rows) if m[r]], dtype=np.int64)
     for b0 in range(0, want.size, block):
         rr = want[b0:b0 + block]
         h = _take(H, rr)
-        dz = logit_grad_rows(h @ Wd.T, y[rr], L[rr], C[rr])
+        dz = logit_grad_rows(h @ Wd.T, y[rr], L[rr], C[rr], *eh(rr))
         dH[rr] = dz @ Wd
     dW = None
     if want_dw and dw_rows is None:
@@ -373,7 +407,7 @@ def ppo_clip_loss_bwd(H, W, lse, grad_logp, ids, mask, rows=None, dw_rows=None, 
         for b0 in range(0, valid.size, block):
             rr = valid[b0:b0 + block]
             h = _take(H, rr)
-            dz = logit_grad_rows(h @ Wd.T, y[rr], L[rr], C[rr])
+            dz = logit_grad_rows(h @ Wd.T, y[rr], L[rr], C[rr], *eh(rr))
             dW += dz.T @ h
     elif want_dw:
         js = _int(dw_rows)
@@ -383,19 +417,26 @@ def ppo_clip_loss_bwd(H, W, lse, grad_logp, ids, mask, rows=None, dw_rows=None, 
             rr = valid[b0:b0 + 4096]
             h = _take(H, rr)
             zj = h @ Wj.T                                  # [B, J]
-            dz = -np.exp(zj - L[rr][:, None])
-            dz += (y[rr][:, None] == js[None, :])
+            p = np.exp(zj - L[rr][:, None])
+            dz = (y[rr][:, None] == js[None, :]) - p
             dz *= C[rr][:, None]
+            if E is not None:
+                mu = L[rr] - Hn[rr]
+                dz += E[rr][:, None] * p * (zj - mu[:, None])
             dW += dz.T @ h
     return dH, dW
 
 
-def bwd_logits(logits, lse, grad_logp, ids, mask, rows=None, block=256):
-    """``dlogits = c (onehot(y) - exp(z - lse))`` on valid rows, 0 elsewhere."""
+def bwd_logits(logits, lse, grad_logp, ids, mask, rows=None, block=256, grad_entropy=None,
+               entropy=None):
+    """``dlogits = c (onehot(y) - exp(z - lse))`` (plus the entropy-bonus term
+    when ``grad_entropy`` and ``entropy`` are given) on valid rows."""
     m = _int(mask) != 0
     y = _int(ids)
     L = _f64(lse)
     C = _f64(grad_logp)
+    E = _f64(grad_entropy) if grad_entropy is not None else None
+    Hn = _f64(entropy) if grad_entropy is not None else None
     T, V = logits.shape
     want = np.nonzero(m)[0] if rows is None else np.asarray([r for r in _int(rows) if m[r]],
                                                             dtype=np.int64)
@@ -403,7 +444,8 @@ def bwd_logits(logits, lse, grad_logp, ids, mask, rows=None, block=256):
     for b0 in range(0, want.size, block):
         rr = want[b0:b0 + block]
         z = _take(logits, rr)
-        dz = logit_grad_rows(z, y[rr], L[rr], C[rr])
+        dz = logit_grad_rows(z, y[rr], L[rr], C[rr], *((None, None) if E is None
+                                                       else (E[rr], Hn[rr])))
         for k, r in enumerate(rr):
             out[int(r)] = dz[k]
     return out
@@ -412,7 +454,7 @@ def bwd_logits(logits, lse, grad_logp, ids, mask, rows=None, block=256):
 # ------------------------------------------------------------ whole step ----
 def trainer_step(H, W, ids, mask, seq_start, rewards, group_size, old_logp, ref_logp,
                  eps_low, eps_high, beta, agg, denom_override=0.0, adv_eps=1e-6, want_dw=True,
-                 is_expert=None, mix_mu=0.0):
+                 is_expert=None, mix_mu=0.0, entropy_coef=0.0):
     """One pass of the whole path: advantages, log-probs/entropy, loss and the
     gradients to H and W."""
     adv = group_advantages(rewards, group_size, adv_eps)
@@ -420,14 +462,16 @@ def trainer_step(H, W, ids, mask, seq_start, rewards, group_size, old_logp, ref_
     V = _f64(W).shape[0]
     fw = ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv, mask, seq_start, ids, V,
                            eps_low, eps_high, beta, agg, denom_override, entropy=ent,
-                           is_expert=is_expert, mix_mu=mix_mu)
-    dH, dW = ppo_clip_loss_bwd(H, W, lse, fw["grad_logp"], ids, mask, want_dw=want_dw)
+                           is_expert=is_expert, mix_mu=mix_mu, entropy_coef=entropy_coef)
+    eg = (fw["grad_entropy"], ent) if entropy_coef > 0 else (None, None)
+    dH, dW = ppo_clip_loss_bwd(H, W, lse, fw["grad_logp"], ids, mask, want_dw=want_dw,
+                               grad_entropy=eg[0], entropy=eg[1])
     return {"adv": adv, "logp": logp, "entropy": ent, "lse": lse, "fwd": fw, "dH": dH, "dW": dW}
 
 
 def loss_only_step(logits, ids, mask, seq_start, rewards, group_size, old_logp, ref_logp,
                    eps_low, eps_high, beta, agg, denom_override=0.0, adv_eps=1e-6, rows=None,
-                   is_expert=None, mix_mu=0.0):
+                   is_expert=None, mix_mu=0.0, entropy_coef=0.0):
     """The loss-only path from given logits: log-probs, entropy, loss, dlogits.
     ``rows`` samples the dlogits rows returned; the loss always uses every row."""
     adv = group_advantages(rewards, group_size, adv_eps)
@@ -435,6 +479,8 @@ def loss_only_step(logits, ids, mask, seq_start, rewards, group_size, old_logp, 
     V = logits.shape[1]
     fw = ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv, mask, seq_start, ids, V,
                            eps_low, eps_high, beta, agg, denom_override, entropy=ent,
-                           is_expert=is_expert, mix_mu=mix_mu)
-    dl = bwd_logits(logits, lse, fw["grad_logp"], ids, mask, rows=rows)
+                           is_expert=is_expert, mix_mu=mix_mu, entropy_coef=entropy_coef)
+    eg = (fw["grad_entropy"], ent) if entropy_coef > 0 else (None, None)
+    dl = bwd_logits(logits, lse, fw["grad_logp"], ids, mask, rows=rows, grad_entropy=eg[0],
+                    entropy=eg[1])
     return {"adv": adv, "logp": logp, "entropy": ent, "lse": lse, "fwd": fw, "dlogits": dl}

@@ -604,3 +604,117 @@ def test_mix_finite_difference():
         assert fd == pytest.approx(out["grad_logp"][t], rel=1e-6, abs=1e-9), t
         checked += 1
     assert checked > 10
+
+
+# ---------------------------------------------------- entropy bonus (R11) ----
+def _ent_loss_of_logits(z, ids, mask, ss, old, ref, adv, agg, coef, **kw):
+    lp, ent, _ = O.token_logprobs_from_logits(z, ids, mask)
+    return O.ppo_clip_loss_fwd(lp, old, ref, adv, mask, ss, ids, z.shape[1], 0.2, 0.2, 0.05, agg,
+                               entropy=ent, entropy_coef=coef, **kw)
+
+
+@pytest.mark.parametrize("mix", [False, True])
+def test_entropy_bonus_finite_difference_logits(mix):
+    """Central differences of the loss with the entropy bonus (entropy taken
+    from the logits by its definition) against the oracle's d loss / d z."""
+    rng = np.random.default_rng(61)
+    ss = np.array([0, 4, 8, 12], np.int32)
+    mask = np.array([1, 1, 0, 1, 1, 1, 1, 0, 1, 1, 1, 0], np.uint8)
+    T, V = 12, 7
+    z = rng.standard_normal((T, V)) * 1.5
+    ids = rng.integers(0, V, size=T)
+    lp, ent, lse = O.token_logprobs_from_logits(z, ids, mask)
+    old = lp + 0.1 * rng.standard_normal(T)
+    ref = lp + 0.2 * rng.standard_normal(T)
+    adv = np.array([0.8, -1.1, 0.4])
+    kw = dict(is_expert=np.array([0, 1, 0], np.uint8), mix_mu=0.3) if mix else {}
+    args = (ids, mask, ss, old, ref, adv, 0, 0.07)
+    base = _ent_loss_of_logits(z, *args, **kw)
+    assert base["margin"].min() > 1e-3
+    assert base["grad_entropy"].max() > 0
+    dl = O.bwd_logits(z, lse, base["grad_logp"], ids, mask, grad_entropy=base["grad_entropy"],
+                      entropy=ent)
+    h = 1e-6
+    for t in range(T):
+        for j in range(V):
+            zp = z.copy(); zp[t, j] += h
+            zm = z.copy(); zm[t, j] -= h
+            fd = (_ent_loss_of_logits(zp, *args, **kw)["loss"] -
+                  _ent_loss_of_logits(zm, *args, **kw)["loss"]) / (2 * h)
+            g = dl[t][j] if t in dl else 0.0
+            assert abs(fd - g) < 1e-8, (t, j, fd, g)
+
+
+def test_entropy_bonus_uniform_rows():
+    """Rows of equal logits: H = log V, the bonus moves the loss by exactly
+    -c_H log V (the weights of the sequence-mean token-mean sum to 1) and
+    leaves d loss / d z unchanged (dH/dz = 0 at the uniform distribution)."""
+    ss, mask = _layout([3, 5, 2], 5)
+    T, V, coef = 15, 13, 0.3
+    z = np.repeat(np.linspace(-1, 1, T)[:, None], V, axis=1)
+    rng = np.random.default_rng(62)
+    ids = rng.integers(0, V, size=T)
+    lp, ent, lse = O.token_logprobs_from_logits(z, ids, mask)
+    np.testing.assert_allclose(ent[mask != 0], math.log(V), rtol=1e-14)
+    old = lp + 0.05 * rng.standard_normal(T)
+    adv = np.array([1.0, -0.5, 0.25])
+    a0 = O.ppo_clip_loss_fwd(lp, old, lp, adv, mask, ss, ids, V, 0.2, 0.2, 0.0, 0, entropy=ent)
+    a1 = O.ppo_clip_loss_fwd(lp, old, lp, adv, mask, ss, ids, V, 0.2, 0.2, 0.0, 0, entropy=ent,
+                             entropy_coef=coef)
+    assert a1["loss"] - a0["loss"] == pytest.approx(-coef * math.log(V), rel=1e-12)
+    assert a1["entropy_loss"] == pytest.approx(math.log(V), rel=1e-13)
+    d0 = O.bwd_logits(z, lse, a0["grad_logp"], ids, mask)
+    d1 = O.bwd_logits(z, lse, a1["grad_logp"], ids, mask, grad_entropy=a1["grad_entropy"],
+                      entropy=ent)
+    for t in d0:
+        np.testing.assert_allclose(d1[t], d0[t], atol=1e-15)
+
+
+def test_entropy_loss_token_mean_equals_entropy_mean():
+    """With token-mean weights 1/N the weighted entropy sum is the entropy
+    mean, which the oracle aggregates separately."""
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=63)
+    ent = np.random.default_rng(63).random(mask.size) * 3
+    out = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.0, 1,
+                              entropy=ent, entropy_coef=0.01)
+    assert out["n_bad_ids"] == 0
+    assert out["entropy_loss"] == pytest.approx(out["entropy_mean"], rel=1e-13)
+    np.testing.assert_allclose(out["grad_entropy"][mask != 0], 0.01 / out["n_valid"], rtol=1e-15)
+    assert np.all(out["grad_entropy"][mask == 0] == 0)
+
+
+def test_entropy_bonus_torch_autograd():
+    """torch float64 autograd of the naive expression with the entropy taken
+    as -sum p log p, through H and W (a third implementation)."""
+    H, W, ids, mask, ss, old, ref, adv = _grad_case(33)
+    eps_l, eps_h, beta, coef = 0.2, 0.28, 0.05, 0.02
+    lp, ent, lse = O.token_logprobs(H, W, ids, mask)
+    base = O.ppo_clip_loss_fwd(lp, old, ref, adv, mask, ss, ids, W.shape[0], eps_l, eps_h, beta,
+                               0, entropy=ent, entropy_coef=coef)
+    dH, dW = O.ppo_clip_loss_bwd(H, W, lse, base["grad_logp"], ids, mask,
+                                 grad_entropy=base["grad_entropy"], entropy=ent)
+    _, dWs = O.ppo_clip_loss_bwd(H, W, lse, base["grad_logp"], ids, mask, dw_rows=[1, 4],
+                                 grad_entropy=base["grad_entropy"], entropy=ent)
+
+    Ht = torch.tensor(H, requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    logits = Ht @ Wt.T
+    logsm = torch.log_softmax(logits, dim=-1)
+    logprob = logsm.gather(1, torch.tensor(ids)[:, None])[:, 0]
+    entropy = -(logsm.exp() * logsm).sum(-1)
+    m = torch.tensor(mask, dtype=torch.float64)
+    T = mask.size
+    seq = torch.tensor(np.searchsorted(ss, np.arange(T), side="right") - 1)
+    A = torch.tensor(adv)[seq]
+    ratio = torch.exp(logprob - torch.tensor(old))
+    surr = torch.maximum(-A * ratio, -A * torch.clamp(ratio, 1 - eps_l, 1 + eps_h))
+    dk = torch.tensor(ref) - logprob
+    per_tok = surr + beta * (torch.exp(dk) - dk - 1) - coef * entropy
+    n_i = torch.zeros(len(ss) - 1, dtype=torch.float64).index_add_(0, seq, m)
+    S = (n_i > 0).sum()
+    loss = ((per_tok * m) / n_i[seq].clamp(min=1)).sum() / S
+    loss.backward()
+    assert loss.item() == pytest.approx(base["loss"], rel=1e-12)
+    np.testing.assert_allclose(dH, Ht.grad.numpy(), rtol=1e-10, atol=1e-14)
+    np.testing.assert_allclose(dW, Wt.grad.numpy(), rtol=1e-10, atol=1e-14)
+    np.testing.assert_allclose(dWs, dW[[1, 4]], rtol=1e-12, atol=1e-15)
