@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define RFT_ABI_VERSION 2
+#define RFT_ABI_VERSION 3
 
 typedef enum {
   RFT_OK = 0,
@@ -106,12 +106,17 @@ typedef struct {
                              e.g. the global count across micro-batches             */
   float mix_mu;           /* weight of the SFT loss on expert rollouts, 0 <= mu <= 1;
                              used only when tokens.is_expert != NULL               */
+  float entropy_coef;     /* entropy bonus c_H >= 0: the loss gains
+                             -c_H * sum_t w_t H_t over the on-policy tokens (the
+                             aggregation weights of the PPO-clip term)             */
 } rft_ppo_params;
 
 /* (device struct) loss value and metrics written by the loss calls.  With
  * expert rollouts (MIX), pg_loss, kl_loss, kl_mean, ratio_mean and clipfrac
  * cover the on-policy tokens (N - n_expert of them) and
- * loss = (1 - mix_mu) * (pg_loss + kl_loss) + mix_mu * sft_loss. */
+ * loss = (1 - mix_mu) * (pg_loss + kl_loss - entropy_coef * entropy_loss)
+ *        + mix_mu * sft_loss
+ * (without expert flags: pg_loss + kl_loss - entropy_coef * entropy_loss). */
 typedef struct {
   double loss;          /* pg_loss + kl_loss (MIX: see above)        */
   double pg_loss;       /* sum_t w_t * clipped surrogate              */
@@ -126,6 +131,7 @@ typedef struct {
   int64_t n_bad_ids;
   double sft_loss;      /* mean of -logp over expert tokens (0 without) */
   int64_t n_expert;     /* valid tokens of expert rollouts            */
+  double entropy_loss;  /* sum_t w_t H_t over on-policy tokens (0 if no entropy given) */
 } rft_ppo_stats;
 
 /* Version of this ABI (RFT_ABI_VERSION). */
@@ -192,19 +198,25 @@ rft_status rft_token_logprobs_from_logits(const rft_tokens* tok, const float* lo
  * "Clipped" means A > 0 and rho > 1+eps_high, or A < 0 and rho < 1-eps_low,
  * decided in fp32 on logp - old against fp32(log(1 +/- eps)).
  * Inputs f32 [T] (adv is [n_seq]); ref_logp may be NULL iff kl_coef == 0;
- * entropy may be NULL (entropy_mean 0).  Outputs: grad_logp [T] (0 on
- * masked rows), *stats (device).  A valid row with an out-of-range id counts
+ * entropy may be NULL (entropy_mean 0) unless entropy_coef > 0.  Outputs:
+ * grad_logp [T] (0 on masked rows), *stats (device), and, if not NULL,
+ * grad_entropy [T]: e_t = d loss / d H_t times -1, i.e. the coefficient of
+ * the entropy bonus term in the backward (entropy_coef * w_t on on-policy
+ * tokens, scaled by 1 - mix_mu under MIX; 0 elsewhere).  A valid row with an out-of-range id counts
  * in n_bad_ids and adds nothing to the loss, metrics or gradient.  With N = 0
  * the loss and every metric are 0.  Reductions run in fp64 in a fixed order.
  * Errors: RFT_E_NULL, RFT_E_SHAPE, RFT_E_PARAM, RFT_E_WORKSPACE. */
 rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* logp,
                                  const float* old_logp, const float* ref_logp, const float* adv,
                                  const float* entropy, const rft_ppo_params* params,
-                                 float* grad_logp, rft_ppo_stats* stats, void* ws,
-                                 size_t ws_bytes, void* stream);
+                                 float* grad_logp, float* grad_entropy, rft_ppo_stats* stats,
+                                 void* ws, size_t ws_bytes, void* stream);
 
 /* Backward of the loss through the policy head: with c_t = grad_logp[t],
- *   dZ_tj = c_t ([j == id_t] - exp(z_tj - lse_t)),
+ *   dZ_tj = c_t ([j == id_t] - p_tj) + e_t p_tj (z_tj - (lse_t - H_t)),
+ *   p_tj = exp(z_tj - lse_t), c_t = grad_logp[t], e_t = grad_entropy[t]
+ *   (the entropy bonus term; grad_entropy and entropy may both be NULL,
+ *   then e_t = 0),
  *   d_hidden = dZ . weight   ([T, d] f32, masked rows 0, always overwritten),
  *   d_weight = dZ^T . hidden ([V, d] f32, overwritten, or added to when
  *              accumulate_dw != 0).
@@ -215,13 +227,16 @@ rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* 
  * Errors: as rft_token_logprobs. */
 rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, const void* weight,
                                  int dtype, int64_t d, int64_t V, const float* lse,
-                                 const float* grad_logp, float* d_hidden, float* d_weight,
+                                 const float* grad_logp, const float* grad_entropy,
+                                 const float* entropy, float* d_hidden, float* d_weight,
                                  int32_t accumulate_dw, void* ws, size_t ws_bytes, void* stream);
 
-/* d_logits[t, j] = c_t ([j == id_t] - exp(logits[t, j] - lse_t)) on valid
- * rows, 0 on masked rows (every row of d_logits [T, V] f32 is written). */
+/* d_logits[t, j] = c_t ([j == id_t] - p_tj) + e_t p_tj (z_tj - (lse_t - H_t))
+ * with z = logits, as rft_ppo_clip_loss_bwd (grad_entropy and entropy may both
+ * be NULL); 0 on masked rows (every row of d_logits [T, V] f32 is written). */
 rft_status rft_ppo_clip_loss_bwd_logits(const rft_tokens* tok, const float* logits, int64_t V,
                                         const float* lse, const float* grad_logp,
+                                        const float* grad_entropy, const float* entropy,
                                         float* d_logits, void* ws, size_t ws_bytes, void* stream);
 
 /* The loss-only path in one pass per row: log-softmax statistics of the given
@@ -229,7 +244,8 @@ rft_status rft_ppo_clip_loss_bwd_logits(const rft_tokens* tok, const float* logi
  * logits row once from HBM (the row stays on chip between the statistics and
  * the gradient) and writing d_logits once.  Outputs as rft_token_logprobs_from_logits,
  * rft_ppo_clip_loss_fwd and rft_ppo_clip_loss_bwd_logits (entropy may be
- * NULL; lse and grad_logp may be NULL). */
+ * NULL; lse and grad_logp may be NULL).  The entropy bonus uses the entropy
+ * the call computes, whether or not it is returned. */
 rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits, int64_t V,
                                      const float* old_logp, const float* ref_logp,
                                      const float* adv, const rft_ppo_params* params, float* logp,
@@ -252,6 +268,7 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
  * and the stats equal those of the separate calls bit for bit, d_hidden and
  * d_weight agree to the rounding of dZ.  For fp32 inputs the call runs the
  * three separate calls in order.  logits are never stored beyond one chunk.
+ * entropy may be NULL only when params->entropy_coef == 0.
  * Errors: as rft_token_logprobs and rft_ppo_clip_loss_fwd. */
 rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const void* weight,
                              int dtype, int64_t d, int64_t V, const float* old_logp,

@@ -37,7 +37,8 @@ class rft_tokens(ctypes.Structure):
 class rft_ppo_params(ctypes.Structure):
     _fields_ = [("eps_low", ctypes.c_float), ("eps_high", ctypes.c_float),
                 ("kl_coef", ctypes.c_float), ("agg", ctypes.c_int32),
-                ("denom_override", ctypes.c_double), ("mix_mu", ctypes.c_float)]
+                ("denom_override", ctypes.c_double), ("mix_mu", ctypes.c_float),
+                ("entropy_coef", ctypes.c_float)]
 
 
 class rft_ppo_stats(ctypes.Structure):
@@ -47,7 +48,7 @@ class rft_ppo_stats(ctypes.Structure):
                 ("clipfrac", ctypes.c_double), ("n_valid", ctypes.c_int64),
                 ("n_seq_valid", ctypes.c_int64), ("n_clipped", ctypes.c_int64),
                 ("n_bad_ids", ctypes.c_int64), ("sft_loss", ctypes.c_double),
-                ("n_expert", ctypes.c_int64)]
+                ("n_expert", ctypes.c_int64), ("entropy_loss", ctypes.c_double)]
 
 
 STATS_BYTES = ctypes.sizeof(rft_ppo_stats)
@@ -66,13 +67,13 @@ _SIGS = {
     "rft_token_logprobs_from_logits": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _i64, _p,
                                                       _p, _p, _p, _p, ctypes.c_size_t, _p]),
     "rft_ppo_clip_loss_fwd": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _i64, _p, _p, _p, _p, _p,
-                                             ctypes.POINTER(rft_ppo_params), _p, _p, _p,
+                                             ctypes.POINTER(rft_ppo_params), _p, _p, _p, _p,
                                              ctypes.c_size_t, _p]),
     "rft_ppo_clip_loss_bwd": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _p, ctypes.c_int, _i64,
-                                             _i64, _p, _p, _p, _p, ctypes.c_int32, _p,
+                                             _i64, _p, _p, _p, _p, _p, _p, ctypes.c_int32, _p,
                                              ctypes.c_size_t, _p]),
     "rft_ppo_clip_loss_bwd_logits": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _i64, _p, _p,
-                                                    _p, _p, ctypes.c_size_t, _p]),
+                                                    _p, _p, _p, _p, ctypes.c_size_t, _p]),
     "rft_ppo_clip_fused_logits": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _i64, _p, _p, _p,
                                                  ctypes.POINTER(rft_ppo_params), _p, _p, _p, _p,
                                                  _p, _p, _p, ctypes.c_size_t, _p]),
@@ -168,8 +169,8 @@ class Tokens:
 
 
 def ppo_params(eps_low=0.2, eps_high=0.2, kl_coef=0.0, agg=RFT_AGG_SEQ_MEAN_TOKEN_MEAN,
-               denom_override=0.0, mix_mu=0.0) -> rft_ppo_params:
-    return rft_ppo_params(eps_low, eps_high, kl_coef, agg, denom_override, mix_mu)
+               denom_override=0.0, mix_mu=0.0, entropy_coef=0.0) -> rft_ppo_params:
+    return rft_ppo_params(eps_low, eps_high, kl_coef, agg, denom_override, mix_mu, entropy_coef)
 
 
 def stats_to_dict(buf: torch.Tensor) -> dict:
@@ -240,7 +241,8 @@ def rft_token_logprobs_from_logits(tokens: Tokens, logits, logp=None, entropy=No
 
 
 def rft_ppo_clip_loss_fwd(tokens: Tokens, V, logp, old_logp, ref_logp, adv, params, entropy=None,
-                          grad_logp=None, stats=None, ws=None, stream=None):
+                          grad_logp=None, stats=None, ws=None, stream=None, grad_entropy=None):
+    """Returns (grad_logp, stats); grad_entropy, when given, receives e_t."""
     _need_gpu(logp, old_logp, adv)
     dev = logp.device
     grad_logp = torch.empty_like(logp) if grad_logp is None else grad_logp
@@ -250,13 +252,14 @@ def rft_ppo_clip_loss_fwd(tokens: Tokens, V, logp, old_logp, ref_logp, adv, para
     tk = tokens.c()
     _check(lib().rft_ppo_clip_loss_fwd(ctypes.byref(tk), V, _ptr(logp), _ptr(old_logp),
                                        _ptr(ref_logp), _ptr(adv), _ptr(entropy),
-                                       ctypes.byref(params), _ptr(grad_logp), _ptr(stats),
-                                       _ptr(ws), nb, _stream(stream)))
+                                       ctypes.byref(params), _ptr(grad_logp), _ptr(grad_entropy),
+                                       _ptr(stats), _ptr(ws), nb, _stream(stream)))
     return grad_logp, stats
 
 
 def rft_ppo_clip_loss_bwd(tokens: Tokens, hidden, weight, lse, grad_logp, d_hidden=None,
-                          d_weight=None, accumulate_dw=False, ws=None, stream=None):
+                          d_weight=None, accumulate_dw=False, ws=None, stream=None,
+                          grad_entropy=None, entropy=None):
     _need_gpu(hidden, weight, lse, grad_logp)
     dev = hidden.device
     T, d, V = tokens.T, hidden.shape[1], weight.shape[0]
@@ -267,18 +270,20 @@ def rft_ppo_clip_loss_bwd(tokens: Tokens, hidden, weight, lse, grad_logp, d_hidd
     ws, nb = _workspace(need, dev, ws)
     tk = tokens.c()
     _check(lib().rft_ppo_clip_loss_bwd(ctypes.byref(tk), _ptr(hidden), _ptr(weight), dt, d, V,
-                                       _ptr(lse), _ptr(grad_logp), _ptr(d_hidden), _ptr(d_weight),
+                                       _ptr(lse), _ptr(grad_logp), _ptr(grad_entropy),
+                                       _ptr(entropy), _ptr(d_hidden), _ptr(d_weight),
                                        1 if accumulate_dw else 0, _ptr(ws), nb, _stream(stream)))
     return d_hidden, d_weight
 
 
 def rft_ppo_clip_loss_bwd_logits(tokens: Tokens, logits, lse, grad_logp, d_logits=None,
-                                 stream=None):
+                                 stream=None, grad_entropy=None, entropy=None):
     _need_gpu(logits, lse, grad_logp)
     d_logits = torch.empty_like(logits) if d_logits is None else d_logits
     tk = tokens.c()
     _check(lib().rft_ppo_clip_loss_bwd_logits(ctypes.byref(tk), _ptr(logits), logits.shape[1],
-                                              _ptr(lse), _ptr(grad_logp), _ptr(d_logits), None, 0,
+                                              _ptr(lse), _ptr(grad_logp), _ptr(grad_entropy),
+                                              _ptr(entropy), _ptr(d_logits), None, 0,
                                               _stream(stream)))
     return d_logits
 

@@ -55,6 +55,7 @@ __device__ void block_reduce_partial(LossPartial& p, LossPartial* out) {
   p.ent = wave_sum_d(p.ent);
   p.ratio = wave_sum_d(p.ratio);
   p.sft = wave_sum_d(p.sft);
+  p.entw = wave_sum_d(p.entw);
   p.clipped = wave_sum_ll(p.clipped);
   p.bad = wave_sum_ll(p.bad);
   p.expert = wave_sum_ll(p.expert);
@@ -64,7 +65,7 @@ __device__ void block_reduce_partial(LossPartial& p, LossPartial* out) {
     LossPartial t = sh[0];
     for (int i = 1; i < (int)(blockDim.x >> 6); ++i) {
       t.loss += sh[i].loss; t.pg += sh[i].pg; t.klw += sh[i].klw; t.kl += sh[i].kl;
-      t.ent += sh[i].ent; t.ratio += sh[i].ratio; t.sft += sh[i].sft;
+      t.ent += sh[i].ent; t.ratio += sh[i].ratio; t.sft += sh[i].sft; t.entw += sh[i].entw;
       t.clipped += sh[i].clipped; t.bad += sh[i].bad; t.expert += sh[i].expert;
     }
     *out = t;
@@ -78,12 +79,12 @@ __global__ void __launch_bounds__(256) k_loss_fwd(
     int64_t T, const float* __restrict__ logp,
     const float* __restrict__ old, const float* __restrict__ ref, const float* __restrict__ adv,
     const float* __restrict__ ent, LossConst c, float* __restrict__ grad,
-    LossPartial* __restrict__ parts) {
+    float* __restrict__ egrad, LossPartial* __restrict__ parts) {
   int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   LossPartial p = RFT_ZERO_PARTIAL;
   if (t < T) {
     int k = kidx[t];
-    float gout = 0.f;
+    float gout = 0.f, eout = 0.f;
     if (k >= 0) {
       int i = row_seq[k];
       int y = ids[t];
@@ -94,10 +95,11 @@ __global__ void __launch_bounds__(256) k_loss_fwd(
         float rf = ref ? ref[t] : lp;
         const bool ex = c.is_expert && c.is_expert[i];
         gout = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, ent ? (double)ent[t] : 0.0, c,
-                        p);
+                        p, &eout);
       }
     }
     grad[t] = gout;
+    if (egrad) egrad[t] = eout;
   }
   block_reduce_partial(p, parts + blockIdx.x);
 }
@@ -113,6 +115,7 @@ __global__ void __launch_bounds__(1024) k_loss_final(const LossPartial* __restri
   for (int i = a; i < b; ++i) {
     p.loss += parts[i].loss; p.pg += parts[i].pg; p.klw += parts[i].klw; p.kl += parts[i].kl;
     p.ent += parts[i].ent; p.ratio += parts[i].ratio; p.sft += parts[i].sft;
+    p.entw += parts[i].entw;
     p.clipped += parts[i].clipped; p.bad += parts[i].bad; p.expert += parts[i].expert;
   }
   __shared__ LossPartial out;
@@ -135,6 +138,7 @@ __global__ void __launch_bounds__(1024) k_loss_final(const LossPartial* __restri
     st->n_bad_ids = out.bad;
     st->sft_loss = Ne > 0 ? out.sft / (double)Ne : 0.0;
     st->n_expert = Ne;
+    st->entropy_loss = N > 0 ? out.entw : 0.0;
   }
 }
 
@@ -146,12 +150,12 @@ hipError_t launch_loss_final(const LossPartial* parts, int nparts, const int32_t
 
 hipError_t launch_loss_fwd(const rft_tokens& tok, const TokMeta& m, const float* logp,
                            const float* old, const float* ref, const float* adv, const float* ent,
-                           const LossConst& c, float* grad, LossPartial* parts, rft_ppo_stats* st,
-                           hipStream_t s) {
+                           const LossConst& c, float* grad, float* egrad, LossPartial* parts,
+                           rft_ppo_stats* st, hipStream_t s) {
   int nb = (int)((tok.T + 255) / 256);
   if (nb > 0)
     k_loss_fwd<<<nb, 256, 0, s>>>(tok.mask, tok.token_ids, m.kidx, m.row_seq, m.n_i, m.meta,
-                                  tok.T, logp, old, ref, adv, ent, c, grad, parts);
+                                  tok.T, logp, old, ref, adv, ent, c, grad, egrad, parts);
   return launch_loss_final(parts, nb, m.meta, st, s);
 }
 

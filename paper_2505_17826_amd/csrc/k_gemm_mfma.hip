@@ -20,7 +20,7 @@
 //   EPI_STATS_Y  EPI_STATS, and also z minus the row's maximum over the
 //              tile, rounded to fp16, row-major [rows, Vpad] (the backward
 //              then forms dZ from it instead of recomputing z).
-//   EPI_DZ     backward recompute: dZ = c (onehot(y) - exp(z - lse)) in bf16,
+//   EPI_DZ     backward recompute: dZ = c (onehot(y) - p) + e p (z - mu) in bf16,
 //              written row-major [rows, Vpad] and transposed [Vpad, rows].
 //   EPI_STORE  fp32 result, optionally scattered to rows through a map and
 //              optionally added to the existing values.
@@ -33,7 +33,7 @@ constexpr int BM = 256, BN = 256, BK = 64, NT = 512;
 constexpr int A_BYTES = BM * BK * 2;
 constexpr int B_BYTES = BN * BK * 2;
 constexpr int STAGE = A_BYTES + B_BYTES;  // 64 KiB
-constexpr int ROWP = BM * 16;             // per-row epilogue parameters
+constexpr int ROWP = BM * 20;             // per-row epilogue parameters (five words)
 // dZ epilogue: one 256x256 bf16 tile staged in LDS, rows padded to 528 bytes
 // (conflict-free 2- and 8-byte writes, contiguous 16-byte reads)
 constexpr int STG_PITCH = 528;
@@ -66,6 +66,8 @@ struct Args {
   const int32_t* ids;
   const float* lse;
   const float* cgrad;
+  const float* egrad;  // EPI_DZ entropy-bonus coefficients (nullptr = none)
+  const float* ent;    //   and entropies, read only with egrad
   float* pm; float* ps; float* pu; int64_t ldp; float* zy;  // EPI_STATS: partials at p_off + m,
   int64_t p_off;                                            //   zy at rows_off + m
   uint16_t* y; int64_t ldy;                                 // EPI_STATS_Y: fp16 z - tile max
@@ -238,6 +240,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   int32_t* rp_i = (int32_t*)(lds + 2 * STAGE);
   float* rp_a = (float*)(lds + 2 * STAGE + BM * 4);
   float* rp_b = (float*)(lds + 2 * STAGE + BM * 8);
+  float* rp_e = (float*)(lds + 2 * STAGE + BM * 12);
+  float* rp_u = (float*)(lds + 2 * STAGE + BM * 16);
 
   {
     const int m0 = mt * BM, n0 = nt * BN;
@@ -259,16 +263,22 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
         rp_i[tid] = y;
       } else if (EPI == EPI_DZ) {
         int y = -1;
-        float L_ = 0.f, c_ = 0.f;
+        float L_ = 0.f, c_ = 0.f, e_ = 0.f, u_ = 0.f;
         if (v) {
           int t = g.rows[g.rows_off + m];
           y = g.ids[t];
           L_ = g.lse[t];
           c_ = g.cgrad[t];
+          if (g.egrad) {
+            e_ = g.egrad[t];
+            u_ = L_ - g.ent[t];
+          }
         }
         rp_i[tid] = y;
         rp_a[tid] = L_;
         rp_b[tid] = c_;
+        rp_e[tid] = e_;
+        rp_u[tid] = u_;
       } else {
         rp_i[tid] = (v && g.c_scatter) ? g.rows[g.rows_off + m] : m;
       }
@@ -430,8 +440,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
         stage_copy_out(lds, g.y + (int64_t)m0 * g.ldy + n0, g.ldy, tid);
       }
     } else if (EPI == EPI_DZ) {
-      // d = c (onehot - p) in bf16, packed per lane as four consecutive rows
-      // of one column
+      // d = c (onehot - p) + e p (z - mu) in bf16, packed per lane as four
+      // consecutive rows of one column
       uint2 hv[2][4][4];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -439,13 +449,15 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
         for (int e4 = 0; e4 < 4; ++e4) {
           __builtin_amdgcn_sched_barrier(0);
           const int rl0 = wm * 64 + i * 32 + e4 * 8 + fh * 4;
-          float Lr[4], cr[4];
+          float Lr[4], cr[4], er[4], ur[4];
           int yr[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             yr[q] = rp_i[rl0 + q];
             Lr[q] = rp_a[rl0 + q] * kLog2e;
             cr[q] = rp_b[rl0 + q];
+            er[q] = rp_e[rl0 + q];
+            ur[q] = rp_u[rl0 + q];
           }
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
@@ -456,7 +468,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
             for (int q = 0; q < 4; ++q) {
               float z = acc[i][j][e4 * 4 + q];
               float p = exp2f(z * kLog2e - Lr[q]);
-              float d = cr[q] * ((col == yr[q] ? 1.f : 0.f) - p);
+              float d = dlogit(cr[q], er[q], ur[q], p, z, col == yr[q]);
               hb[q] = f32_to_bf16(cvalid ? d : 0.f);
             }
             hv[i][j][e4].x = hb[0] | (hb[1] << 16);
@@ -564,14 +576,15 @@ hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, in
 // into dz [Tc, ldz] and dzt [Vpad, Tc].
 hipError_t mfma_dz(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
-                   const int32_t* cnt, int64_t c0, int64_t Tc, uint16_t* dz, uint16_t* dzt,
-                   hipStream_t s) {
+                   const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
+                   int64_t Tc, uint16_t* dz, uint16_t* dzt, hipStream_t s) {
   mf::Args a = {};
   a.A = Hc + c0 * d; a.lda = d;
   a.B = W; a.ldb = d;
   a.M = (int)Tc; a.N = (int)Vpad; a.K = (int)d;
   a.cnt = cnt; a.cnt_off = c0; a.cnt_cap = Tc; a.m_from_cnt = 1;
   a.rows = rows; a.rows_off = c0; a.ids = ids; a.lse = lse; a.cgrad = cgrad;
+  a.egrad = egrad; a.ent = ent;
   a.dz = dz; a.ldz = Vpad; a.dzt = dzt; a.ldzt = Tc; a.Vvalid = V;
   a.NB = (int)V;  // W has V rows; columns V..Vpad-1 of dZ are written as 0
   // dz rows are indexed by the chunk-local m (m0 + row), dzt columns likewise

@@ -4,7 +4,9 @@
 //           order;
 //   row terms: lse, entropy, logp = z_y - lse, the PPO-clip/KL loss terms
 //           and c_t = d loss / d logp;
-//   pass 2: d_logits = c_t (onehot - exp(z - lse)) with non-temporal stores.
+//   pass 2: d_logits = c_t (onehot - p) + e_t p (z - mu_t) (p the softmax,
+//           e_t the entropy-bonus coefficient, mu_t = lse - entropy) with
+//           non-temporal stores.
 // The fused kernel keeps the row on chip between the passes (registers, then
 // LDS) so that a row of up to about 600 KB is read from HBM once.  Every kernel
 // here gives each thread the same chunks of the row in the same order, so the
@@ -89,9 +91,10 @@ __device__ RowStats row_pass1(const float* __restrict__ z, int64_t V, RowStats* 
   return block_stats(r, sh);
 }
 
+// d_logits of one row: c (onehot - p) + e p (z - mu) (dlogit), 16-byte stores.
 template <bool VEC>
-__device__ void row_pass2(const float* __restrict__ z, int64_t V, float lse, float c, int y,
-                          float* __restrict__ out) {
+__device__ void row_pass2(const float* __restrict__ z, int64_t V, float lse, float c, float e,
+                          float mu, int y, float* __restrict__ out) {
   const float lk = lse * kLog2e;
   if (VEC) {
     const float4* z4 = (const float4*)z;
@@ -99,20 +102,17 @@ __device__ void row_pass2(const float* __restrict__ z, int64_t V, float lse, flo
     int64_t n4 = V >> 2;
     for (int64_t j = threadIdx.x; j < n4; j += NT) {
       float4 q = z4[j];
+      const int hot = (y >> 2) == j ? (y & 3) : -1;
       floatx4 d;
-      d[0] = -c * exp2f(fmaf(q.x, kLog2e, -lk));
-      d[1] = -c * exp2f(fmaf(q.y, kLog2e, -lk));
-      d[2] = -c * exp2f(fmaf(q.z, kLog2e, -lk));
-      d[3] = -c * exp2f(fmaf(q.w, kLog2e, -lk));
-      if ((y >> 2) == j) d[y & 3] += c;
+      d[0] = dlogit(c, e, mu, exp2f(fmaf(q.x, kLog2e, -lk)), q.x, hot == 0);
+      d[1] = dlogit(c, e, mu, exp2f(fmaf(q.y, kLog2e, -lk)), q.y, hot == 1);
+      d[2] = dlogit(c, e, mu, exp2f(fmaf(q.z, kLog2e, -lk)), q.z, hot == 2);
+      d[3] = dlogit(c, e, mu, exp2f(fmaf(q.w, kLog2e, -lk)), q.w, hot == 3);
       __builtin_nontemporal_store(d, o4 + j);
     }
   } else {
-    for (int64_t j = threadIdx.x; j < V; j += NT) {
-      float d = -c * exp2f(fmaf(z[j], kLog2e, -lk));
-      if (j == y) d += c;
-      out[j] = d;
-    }
+    for (int64_t j = threadIdx.x; j < V; j += NT)
+      out[j] = dlogit(c, e, mu, exp2f(fmaf(z[j], kLog2e, -lk)), z[j], j == y);
   }
 }
 
@@ -168,6 +168,8 @@ __global__ void __launch_bounds__(NT) k_logits_bwd(const float* __restrict__ log
                                                     const int32_t* __restrict__ ids,
                                                     const float* __restrict__ lse,
                                                     const float* __restrict__ grad,
+                                                    const float* __restrict__ egrad,
+                                                    const float* __restrict__ ent,
                                                     float* __restrict__ dl) {
   int64_t t = blockIdx.x;
   float* out = dl + t * V;
@@ -176,7 +178,9 @@ __global__ void __launch_bounds__(NT) k_logits_bwd(const float* __restrict__ log
     return;
   }
   int y = ids[t];
-  row_pass2<VEC>(logits + t * V, V, lse[t], grad[t], (y >= 0 && (int64_t)y < V) ? y : -1, out);
+  const float L = lse[t];
+  const float e = egrad ? egrad[t] : 0.f, mu = egrad ? L - ent[t] : 0.f;
+  row_pass2<VEC>(logits + t * V, V, L, grad[t], e, mu, (y >= 0 && (int64_t)y < V) ? y : -1, out);
 }
 
 // ---- fused: statistics, loss terms and d_logits (rft_ppo_clip_fused_logits)
@@ -192,7 +196,7 @@ __global__ void __launch_bounds__(NT) k_logits_fused(
   // (the launch also reserves dynamic LDS it does not use, to keep one
   //  workgroup per CU)
   __shared__ RowStats sh[NT / 64 + 1];
-  __shared__ float row_c;
+  __shared__ float row_c, row_e, row_mu;
   int64_t t = blockIdx.x;
   float* out = dl + t * V;
   int k = kidx[t];
@@ -219,24 +223,26 @@ __global__ void __launch_bounds__(NT) k_logits_fused(
     if (ent) ent[t] = H;
     if (lse_out) lse_out[t] = L;
     LossPartial p = RFT_ZERO_PARTIAL;
-    float c = 0.f;
+    float c = 0.f, e = 0.f;
     if (!ok) {
       p.bad = 1;
     } else {
       int i = row_seq[k];
       float rf = ref ? ref[t] : lp;
       const bool ex = cst.is_expert && cst.is_expert[i];
-      c = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, (double)H, cst, p);
+      c = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, (double)H, cst, p, &e);
     }
     if (grad_out) grad_out[t] = c;
     parts[t] = p;
     row_c = c;
+    row_e = e;
+    row_mu = L - H;
     sh[NT / 64].m = L;
   }
   __syncthreads();
   float c = row_c, L = sh[NT / 64].m;
   int y = ids[t];
-  row_pass2<VEC>(z, V, L, c, (y >= 0 && (int64_t)y < V) ? y : -1, out);
+  row_pass2<VEC>(z, V, L, c, row_e, row_mu, (y >= 0 && (int64_t)y < V) ? y : -1, out);
 }
 
 // ---- fused, with the row kept on chip: the first REG*NTC float4 of the row
@@ -245,16 +251,21 @@ __global__ void __launch_bounds__(NT) k_logits_fused(
 typedef int v4i __attribute__((ext_vector_type(4)));
 constexpr int NTC = NT;                  // 2 waves per SIMD
 constexpr int REG = 56;                  // float4 per thread held in registers
+constexpr int REG_ENT = 54;              // the same with the entropy-bonus term (no spills)
 constexpr int LCAP = 18 * NTC;           // float4 held in LDS (144 KiB)
 constexpr size_t kCachedLds = (size_t)LCAP * 16;
 
-__device__ __forceinline__ floatx4 dlogit4(floatx4 q, float lk, float c, int64_t j, int y) {
+// d_logits of four logits; ENT adds the entropy-bonus term e p (z - mu)
+template <bool ENT>
+__device__ __forceinline__ floatx4 dlogit4(floatx4 q, float lk, float c, float e, float mu,
+                                           int64_t j, int y) {
+  const int hot = (y >> 2) == j ? (y & 3) : -1;
   floatx4 d;
-  d[0] = -c * exp2f(fmaf(q[0], kLog2e, -lk));
-  d[1] = -c * exp2f(fmaf(q[1], kLog2e, -lk));
-  d[2] = -c * exp2f(fmaf(q[2], kLog2e, -lk));
-  d[3] = -c * exp2f(fmaf(q[3], kLog2e, -lk));
-  if ((y >> 2) == j) d[y & 3] += c;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float p = exp2f(fmaf(q[i], kLog2e, -lk));
+    d[i] = ENT ? dlogit(c, e, mu, p, q[i], hot == i) : c * ((hot == i ? 1.f : 0.f) - p);
+  }
   return d;
 }
 
@@ -270,6 +281,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* p, int64_
   return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), 0, nr, 0x00020000);
 }
 
+template <bool ENT, int REGS>
 __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
     const float* __restrict__ logits, int64_t T, int64_t V, const uint8_t* __restrict__ mask,
     const int32_t* __restrict__ ids, const int32_t* __restrict__ kidx,
@@ -280,7 +292,7 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
     float* __restrict__ dl, LossPartial* __restrict__ parts) {
   extern __shared__ floatx4 row_lds[];  // LCAP float4
   __shared__ RowStats sh[NTC / 64 + 1];
-  __shared__ float row_c;
+  __shared__ float row_c, row_e, row_mu;
   const int tid = threadIdx.x;
   const int64_t t = blockIdx.x;
   float* out = dl + t * V;
@@ -306,21 +318,21 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
   }
   // pass 1: registers, then LDS, then the rest (chunks past the row read as 0
   // and are left out of the statistics)
-  const int u_full = (int)min((int64_t)REG, n4 / NTC);  // chunks complete for every thread
+  const int u_full = (int)min((int64_t)REGS, n4 / NTC);  // chunks complete for every thread
   // a lane whose chunk lies past the row takes a vector offset of 2^31, out of
   // range for the descriptor whether or not the scalar offset is counted
-  const int nv = (int)min((int64_t)REG, (n4 - tid + NTC - 1) / NTC);  // this lane's chunks
-  floatx4 regs[REG];
+  const int nv = (int)min((int64_t)REGS, (n4 - tid + NTC - 1) / NTC);  // this lane's chunks
+  floatx4 regs[REGS];
 #pragma unroll
-  for (int u = 0; u < REG; ++u)
+  for (int u = 0; u < REGS; ++u)
     regs[u] = (floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, u < nv ? vo : 0x80000000u,
                                                              (uint32_t)u * SU, 2);
   RowStats r = {-INFINITY, 0.f, 0.f};
 #pragma unroll
-  for (int u = 0; u < REG; ++u) {
+  for (int u = 0; u < REGS; ++u) {
     if (u < u_full || (u == u_full && tid + (int64_t)u * NTC < n4)) acc4v(r, regs[u]);
   }
-  const int64_t j_lds = (int64_t)REG * NTC, j_rest = j_lds + LCAP;
+  const int64_t j_lds = (int64_t)REGS * NTC, j_rest = j_lds + LCAP;
   for (int64_t j = j_lds + tid, s_ = tid; j < n4 && s_ < LCAP; j += NTC, s_ += NTC) {
     floatx4 q = (floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, (uint32_t)(j * 16), 0, 2);
     row_lds[s_] = q;
@@ -340,22 +352,26 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
     if (ent) ent[t] = H;
     if (lse_out) lse_out[t] = L;
     LossPartial p = RFT_ZERO_PARTIAL;
-    float c = 0.f;
+    float c = 0.f, e = 0.f;
     if (!ok) {
       p.bad = 1;
     } else {
       int i = row_seq[k];
       float rf = ref ? ref[t] : lp;
       const bool ex = cst.is_expert && cst.is_expert[i];
-      c = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, (double)H, cst, p);
+      LossConst cc = cst;
+      if (!ENT) cc.ent_coef = 0.f;  // the launcher picks ENT = (ent_coef > 0)
+      c = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, (double)H, cc, p, &e);
     }
     if (grad_out) grad_out[t] = c;
     parts[t] = p;
     row_c = c;
+    row_e = e;
+    row_mu = L - H;
     sh[NTC / 64].m = L;
   }
   __syncthreads();
-  const float c = row_c, lk = sh[NTC / 64].m * kLog2e;
+  const float c = row_c, lk = sh[NTC / 64].m * kLog2e, e = row_e, mu = row_mu;
   int y = ids[t];
   y = (y >= 0 && (int64_t)y < V) ? y : -1;
   // pass 2: same three regions; stores past the row are dropped by the descriptor
@@ -363,17 +379,17 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
   int nv2 = nv;
   asm volatile("" : "+v"(vo2), "+v"(nv2));  // recomputed here, not held through pass 1
 #pragma unroll
-  for (int u = 0; u < REG; ++u)
+  for (int u = 0; u < REGS; ++u)
     __builtin_amdgcn_raw_buffer_store_b128(
-        (v4i)dlogit4(regs[u], lk, c, tid + (int64_t)u * NTC, y), rout,
+        (v4i)dlogit4<ENT>(regs[u], lk, c, e, mu, tid + (int64_t)u * NTC, y), rout,
         u < nv2 ? vo2 : 0x80000000u, (uint32_t)u * SU, 2);
   for (int64_t j = j_lds + tid, s_ = tid; j < n4 && s_ < LCAP; j += NTC, s_ += NTC)
-    __builtin_amdgcn_raw_buffer_store_b128((v4i)dlogit4(row_lds[s_], lk, c, j, y), rout,
+    __builtin_amdgcn_raw_buffer_store_b128((v4i)dlogit4<ENT>(row_lds[s_], lk, c, e, mu, j, y), rout,
                                            (uint32_t)(j * 16), 0, 2);
   for (int64_t j = j_rest + tid; j < n4; j += NTC)
     __builtin_amdgcn_raw_buffer_store_b128(
-        (v4i)dlogit4((floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, (uint32_t)(j * 16), 0, 0),
-                     lk, c, j, y),
+        (v4i)dlogit4<ENT>((floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, (uint32_t)(j * 16), 0, 0),
+                     lk, c, e, mu, j, y),
         rout, (uint32_t)(j * 16), 0, 2);
 }
 
@@ -396,14 +412,17 @@ hipError_t launch_logits_stats(const float* logits, const rft_tokens& tok, int64
 }
 
 hipError_t launch_logits_bwd(const float* logits, const rft_tokens& tok, int64_t V,
-                             const float* lse, const float* grad, float* dl, hipStream_t s) {
+                             const float* lse, const float* grad, const float* egrad,
+                             const float* ent, float* dl, hipStream_t s) {
   if (tok.T <= 0) return hipSuccess;
   if (vec_ok(logits, V) && vec_ok(dl, V))
     lg::k_logits_bwd<true><<<(unsigned)tok.T, lg::NT, 0, s>>>(logits, tok.T, V, tok.mask,
-                                                               tok.token_ids, lse, grad, dl);
+                                                               tok.token_ids, lse, grad, egrad,
+                                                               ent, dl);
   else
     lg::k_logits_bwd<false><<<(unsigned)tok.T, lg::NT, 0, s>>>(logits, tok.T, V, tok.mask,
-                                                                tok.token_ids, lse, grad, dl);
+                                                                tok.token_ids, lse, grad, egrad,
+                                                                ent, dl);
   return hipGetLastError();
 }
 
@@ -417,13 +436,19 @@ hipError_t launch_logits_fused(const float* logits, const rft_tokens& tok, const
   if (tok.T > 0) {
     // buffer descriptors span one row: 32-bit byte offsets
     if (vec_ok(logits, V) && vec_ok(dl, V) && V <= ((int64_t)1 << 28)) {
-      hipError_t e = hipFuncSetAttribute((const void*)lg::k_logits_fused_cached,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize,
+      const void* fn = c.ent_coef > 0.f ? (const void*)lg::k_logits_fused_cached<true, lg::REG_ENT>
+                                        : (const void*)lg::k_logits_fused_cached<false, lg::REG>;
+      hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                          (int)lg::kCachedLds);
       if (e != hipSuccess) return e;
-      lg::k_logits_fused_cached<<<(unsigned)tok.T, lg::NTC, lg::kCachedLds, s>>>(
-          logits, tok.T, V, tok.mask, tok.token_ids, m.kidx, m.row_seq, m.n_i, m.meta, old, ref,
-          adv, c, logp, ent, lse, grad, dl, parts);
+      if (c.ent_coef > 0.f)
+        lg::k_logits_fused_cached<true, lg::REG_ENT><<<(unsigned)tok.T, lg::NTC, lg::kCachedLds, s>>>(
+            logits, tok.T, V, tok.mask, tok.token_ids, m.kidx, m.row_seq, m.n_i, m.meta, old, ref,
+            adv, c, logp, ent, lse, grad, dl, parts);
+      else
+        lg::k_logits_fused_cached<false, lg::REG><<<(unsigned)tok.T, lg::NTC, lg::kCachedLds, s>>>(
+            logits, tok.T, V, tok.mask, tok.token_ids, m.kidx, m.row_seq, m.n_i, m.meta, old, ref,
+            adv, c, logp, ent, lse, grad, dl, parts);
     } else {
       hipError_t e = hipFuncSetAttribute((const void*)lg::k_logits_fused<false>,
                                          hipFuncAttributeMaxDynamicSharedMemorySize,

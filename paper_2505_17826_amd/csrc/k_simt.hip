@@ -24,6 +24,7 @@ struct Args {
   const int32_t* cnt; int64_t cnt_off, cnt_cap; int m_from_cnt, k_from_cnt;
   const int32_t* rows; int64_t rows_off;
   const int32_t* ids; const float* lse; const float* cgrad;
+  const float* egrad; const float* ent;  // EPI_DZ entropy bonus (egrad nullptr = none)
   float* pm; float* ps; float* pu; int64_t ldp; float* zy;
   float* dz; int64_t ldz; int64_t Vvalid;
   float* C; int64_t ldc; int accumulate; int c_scatter;
@@ -132,19 +133,23 @@ __global__ void __launch_bounds__(NT) k_gemm32(const Args g) {
       }
     } else if (EPI == EPI_DZ) {
       int y = -1;
-      float L = 0.f, c = 0.f;
+      float L = 0.f, c = 0.f, e = 0.f, mu = 0.f;
       if (rv) {
         int t = g.rows[g.rows_off + m];
         y = g.ids[t];
         L = g.lse[t];
         c = g.cgrad[t];
+        if (g.egrad) {
+          e = g.egrad[t];
+          mu = L - g.ent[t];
+        }
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         int n = n0 + tx + 16 * j;
         if (n < N) {
           float d = 0.f;
-          if (rv && n < g.Vvalid) d = c * ((n == y ? 1.f : 0.f) - expf(acc[i][j] - L));
+          if (rv && n < g.Vvalid) d = dlogit(c, e, mu, expf(acc[i][j] - L), acc[i][j], n == y);
           g.dz[(int64_t)m * g.ldz + n] = d;
         }
       }
@@ -188,13 +193,15 @@ hipError_t simt_fwd_stats(const float* H, int64_t d, const float* W, int64_t V, 
 // dZ (fp32) of compacted rows [c0, c0 + Tc) into dz [Tc, ldz]; columns >= V are 0.
 hipError_t simt_dz(const float* H, int64_t d, const float* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
-                   const int32_t* cnt, int64_t c0, int64_t Tc, float* dz, hipStream_t s) {
+                   const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
+                   int64_t Tc, float* dz, hipStream_t s) {
   sm::Args a = {};
   a.A = H; a.sam = d; a.sak = 1; a.a_map = rows; a.a_moff = c0;
   a.B = W; a.sbn = d; a.sbk = 1;
   a.M = (int)Tc; a.N = (int)Vpad; a.K = (int)d;
   a.cnt = cnt; a.cnt_off = c0; a.cnt_cap = Tc; a.m_from_cnt = 1;
   a.rows = rows; a.rows_off = c0; a.ids = ids; a.lse = lse; a.cgrad = cgrad;
+  a.egrad = egrad; a.ent = ent;
   a.dz = dz; a.ldz = Vpad; a.Vvalid = V;
   a.NB = (int)V;  // W has V rows; columns V..Vpad-1 are written as 0
   sm::k_gemm32<sm::EPI_DZ><<<grid32(Tc, Vpad), sm::NT, 0, s>>>(a);

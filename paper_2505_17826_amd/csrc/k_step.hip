@@ -3,8 +3,10 @@
 //   k_step_rows   merge the chunk's log-sum-exp partials into lse, entropy and
 //                 logp, and form the per-token loss gradient c_t = dL/dlogp
 //                 (PPO-clip surrogate with the k3 KL term, Sec. 3 of the paper,
-//                 and the on-policy / expert split of the MIX loss);
-//   k_dz_from_y   dZ = c_t (onehot(y_t) - exp(z - lse_t)) from the fp16
+//                 and the on-policy / expert split of the MIX loss), and, with
+//                 an entropy bonus, its coefficient e_t and the softmax mean
+//                 mu_t = lse_t - H_t of the row;
+//   k_dz_from_y   dZ = c_t (onehot(y_t) - p) + e_t p (z - mu_t) from the fp16
 //                 y = z - (row maximum over the 256-column tile) that the
 //                 forward GEMM stored, written in place as bf16 [Tc, Vpad] and
 //                 transposed [Vpad, Tc] for the weight-gradient GEMM.
@@ -23,7 +25,7 @@ __global__ void __launch_bounds__(256) k_step_rows(
     int ntiles, const float* __restrict__ zy, const float* __restrict__ old,
     const float* __restrict__ ref, const float* __restrict__ adv, LossConst c,
     float* __restrict__ logp, float* __restrict__ ent, float* __restrict__ lse,
-    float* __restrict__ grad) {
+    float* __restrict__ grad, float* __restrict__ ce, float* __restrict__ cmu) {
   const int64_t kl = (int64_t)blockIdx.x * 256 + threadIdx.x;  // row within the chunk
   const int64_t k = c0 + kl;                                    // compacted row
   if (kl >= Tc || k >= (int64_t)meta[0]) return;
@@ -34,21 +36,26 @@ __global__ void __launch_bounds__(256) k_step_rows(
     lse_merge(m, sm, u, pm[o], ps[o], pu[o]);
   }
   const float L = m + logf(sm);
+  const float H = L - u / sm;
   lse[t] = L;
-  if (ent) ent[t] = L - u / sm;
+  if (ent) ent[t] = H;
   const int y = ids[t];
   const bool ok = y >= 0 && (int64_t)y < V;
   const float lp = ok ? zy[k] - L : __int_as_float(0x7fc00000);
   logp[t] = lp;
-  float gout = 0.f;
+  float gout = 0.f, eout = 0.f;
   if (ok) {
     const int i = row_seq[k];
     const float rf = ref ? ref[t] : lp;
     const bool ex = c.is_expert && c.is_expert[i];
     LossPartial p = RFT_ZERO_PARTIAL;
-    gout = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, 0.0, c, p);
+    gout = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, 0.0, c, p, &eout);
   }
   grad[t] = gout;
+  if (ce) {
+    ce[kl] = eout;
+    cmu[kl] = L - H;
+  }
 }
 
 // One 512-thread workgroup per 256 x 256 tile of the chunk.  Thread tid owns
@@ -68,9 +75,10 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
     uint16_t* __restrict__ yz, int64_t Vpad, uint16_t* __restrict__ dzt, int64_t Tc, int64_t V,
     const int32_t* __restrict__ rows, const int32_t* __restrict__ ids,
     const int32_t* __restrict__ meta, int64_t c0, const float* __restrict__ pm,
-    const float* __restrict__ lse, const float* __restrict__ grad, int ntc) {
+    const float* __restrict__ lse, const float* __restrict__ grad, const float* __restrict__ ce,
+    const float* __restrict__ cmu, int ntc) {
   __shared__ __attribute__((aligned(16))) char st[256 * 512];
-  __shared__ float rL[256], rC[256], rM[256];
+  __shared__ float rL[256], rC[256], rM[256], rE[256], rD[256];
   __shared__ int rY[256];
   const int tid = threadIdx.x;
   const int nt = (int)(blockIdx.x % ntc), mt = (int)(blockIdx.x / ntc);
@@ -81,7 +89,7 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
   const int64_t n0 = (int64_t)nt * 256;
   if (tid < 256) {
     const int64_t r = r0 + tid;
-    float L_ = 0.f, C_ = 0.f, M_ = 0.f;
+    float L_ = 0.f, C_ = 0.f, M_ = 0.f, E_ = 0.f, D_ = 0.f;
     int Y_ = -1;
     if (r < count) {
       const int t = rows[c0 + r];
@@ -89,10 +97,16 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
       C_ = grad[t];
       Y_ = ids[t];
       M_ = pm[(int64_t)nt * Tc + r];
+      if (ce) {
+        E_ = ce[r];
+        D_ = M_ - cmu[r];  // z - mu = y + (tile maximum - mu)
+      }
     }
     rL[tid] = L_ * kLog2e;
     rC[tid] = C_;
     rM[tid] = M_ * kLog2e;
+    rE[tid] = E_;
+    rD[tid] = D_;
     rY[tid] = Y_;
   }
   __syncthreads();
@@ -109,7 +123,7 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
       const int rl = rb * 8 + r;
-      const float Lk = rL[rl], Ck = rC[rl], Mk = rM[rl];
+      const float Lk = rL[rl], Ck = rC[rl], Mk = rM[rl], Ek = rE[rl], Dk = rD[rl];
       const int Yk = rY[rl];
       const bool rv = r0 + rl < count;
       const uint32_t w[4] = {in[r].x, in[r].y, in[r].z, in[r].w};
@@ -119,7 +133,7 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
         const uint16_t hb = (uint16_t)(w[q >> 1] >> ((q & 1) * 16));
         const float yv = (float)__builtin_bit_cast(_Float16, hb);
         const float p = exp2f(fmaf(yv, kLog2e, Mk - Lk));
-        float d = Ck * ((col == (int64_t)Yk ? 1.f : 0.f) - p);
+        float d = dlogit(Ck, Ek, -Dk, p, yv, col == (int64_t)Yk);
         d = (rv && col < V) ? d : 0.f;
         colv[q][r] = (uint16_t)bf16_bits(d);
       }
@@ -156,21 +170,21 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
                             int64_t Tc, const float* pm, const float* ps, const float* pu,
                             int ntiles, const float* zy, const float* old, const float* ref,
                             const float* adv, const LossConst& c, float* logp, float* ent,
-                            float* lse, float* grad, hipStream_t s) {
+                            float* lse, float* grad, float* ce, float* cmu, hipStream_t s) {
   const int nb = (int)((Tc + 255) / 256);
   k_step_rows<<<nb, 256, 0, s>>>(m.rows, m.row_seq, m.n_i, m.meta, ids, V, c0, Tc, pm, ps, pu,
-                                 ntiles, zy, old, ref, adv, c, logp, ent, lse, grad);
+                                 ntiles, zy, old, ref, adv, c, logp, ent, lse, grad, ce, cmu);
   return hipGetLastError();
 }
 
 hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, uint16_t* dzt, int64_t Tc, int64_t V,
                             const int32_t* rows, const int32_t* ids, const int32_t* meta,
                             int64_t c0, const float* pm, const float* lse, const float* grad,
-                            hipStream_t s) {
+                            const float* ce, const float* cmu, hipStream_t s) {
   const int ntc = (int)(Vpad / 256);
   const int64_t nb = (Tc / 256) * ntc;
   k_dz_from_y<<<(unsigned)nb, kDzT, 0, s>>>(yz, Vpad, dzt, Tc, V, rows, ids, meta, c0, pm, lse,
-                                            grad, ntc);
+                                            grad, ce, cmu, ntc);
   return hipGetLastError();
 }
 

@@ -84,6 +84,9 @@ rft_status check_params(const rft_ppo_params* p, const char* fn) {
     return fail(RFT_E_PARAM, "%s: denom_override=%g must be finite and >= 0", fn, p->denom_override);
   if (!(p->mix_mu >= 0.f && p->mix_mu <= 1.f))
     return fail(RFT_E_PARAM, "%s: mix_mu=%g must be in [0, 1]", fn, (double)p->mix_mu);
+  if (!(p->entropy_coef >= 0.f) || !std::isfinite(p->entropy_coef))
+    return fail(RFT_E_PARAM, "%s: entropy_coef=%g must be finite and >= 0", fn,
+                (double)p->entropy_coef);
   return RFT_OK;
 }
 
@@ -102,6 +105,7 @@ LossConst loss_const(const rft_ppo_params* p, int64_t V) {
   c.is_expert = nullptr;
   c.mix = 0;
   c.mu = p->mix_mu;
+  c.ent_coef = p->entropy_coef;
   return c;
 }
 
@@ -219,6 +223,7 @@ struct StepWs {
   TokMeta m;
   uint16_t *hc, *wt, *dz, *dzt, *ht;
   float *pm, *ps, *pu, *zy;
+  float *ce, *cmu;  // per chunk row: entropy-bonus coefficient and softmax mean
   LossPartial* parts;
   int ntiles;
   int64_t Tc, Vpad;
@@ -238,6 +243,8 @@ StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64
   w.ps = c.take<float>((size_t)w.ntiles * Tc);
   w.pu = c.take<float>((size_t)w.ntiles * Tc);
   w.zy = c.take<float>((size_t)T1);
+  w.ce = c.take<float>((size_t)Tc);
+  w.cmu = c.take<float>((size_t)Tc);
   w.parts = c.take<LossPartial>((size_t)((T1 + 255) / 256));
   w.dz = c.take<uint16_t>((size_t)Tc * w.Vpad);
   w.dzt = c.take<uint16_t>((size_t)w.Vpad * Tc);
@@ -259,11 +266,16 @@ int64_t step_tc_for(const rft_tokens& tok, int64_t d, int64_t V, size_t ws_bytes
   return lo * a;
 }
 
-size_t step_f32_bytes(const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
+// fp32 step: the three calls share the front of the workspace; the entropy
+// bonus coefficients [T] follow it.
+size_t step_f32_front(const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
   size_t a = carve_fwd(nullptr, tok, d, V, RFT_F32).bytes;
   size_t b = carve_loss(nullptr, tok, false).bytes;
   size_t c = carve_bwd(nullptr, tok, d, V, RFT_F32, Tc).bytes;
-  return std::max(a, std::max(b, c));
+  return (size_t)round_up((int64_t)std::max(a, std::max(b, c)), 256);
+}
+size_t step_f32_bytes(const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
+  return step_f32_front(tok, d, V, Tc) + (size_t)round_up((tok.T > 0 ? tok.T : 1) * 4, 256);
 }
 
 }  // namespace
@@ -394,8 +406,8 @@ rft_status rft_token_logprobs_from_logits(const rft_tokens* tok, const float* lo
 rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* logp,
                                  const float* old_logp, const float* ref_logp, const float* adv,
                                  const float* entropy, const rft_ppo_params* params,
-                                 float* grad_logp, rft_ppo_stats* stats, void* ws,
-                                 size_t ws_bytes, void* stream) {
+                                 float* grad_logp, float* grad_entropy, rft_ppo_stats* stats,
+                                 void* ws, size_t ws_bytes, void* stream) {
   const char* fn = "rft_ppo_clip_loss_fwd";
   rft_status st = check_tokens(tok, fn);
   if (st) return st;
@@ -406,6 +418,8 @@ rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* 
     return fail(RFT_E_NULL, "%s: logp / old_logp / adv / grad_logp is NULL", fn);
   if (tok->T > 0 && params->kl_coef > 0.f && !ref_logp)
     return fail(RFT_E_NULL, "%s: ref_logp is NULL with kl_coef > 0", fn);
+  if (tok->T > 0 && params->entropy_coef > 0.f && !entropy)
+    return fail(RFT_E_NULL, "%s: entropy is NULL with entropy_coef > 0", fn);
   LossWs w = carve_loss(nullptr, *tok, false);
   if ((st = check_ws(fn, ws, ws_bytes, w.bytes))) return st;
   w = carve_loss(ws, *tok, false);
@@ -413,14 +427,15 @@ rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* 
   RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
   LossConst c = loss_const(params, V, *tok);
   RFT_HIP(launch_loss_fwd(*tok, w.m, logp, old_logp, params->kl_coef > 0.f ? ref_logp : nullptr,
-                          adv, entropy, c, grad_logp, w.parts, stats, s),
+                          adv, entropy, c, grad_logp, grad_entropy, w.parts, stats, s),
           fn);
   return RFT_OK;
 }
 
 rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, const void* weight,
                                  int dtype, int64_t d, int64_t V, const float* lse,
-                                 const float* grad_logp, float* d_hidden, float* d_weight,
+                                 const float* grad_logp, const float* grad_entropy,
+                                 const float* entropy, float* d_hidden, float* d_weight,
                                  int32_t accumulate_dw, void* ws, size_t ws_bytes, void* stream) {
   const char* fn = "rft_ppo_clip_loss_bwd";
   rft_status st = check_tokens(tok, fn);
@@ -429,6 +444,8 @@ rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, cons
   if (!d_weight) return fail(RFT_E_NULL, "%s: d_weight is NULL", fn);
   if (tok->T > 0 && (!lse || !grad_logp || !d_hidden))
     return fail(RFT_E_NULL, "%s: lse / grad_logp / d_hidden is NULL", fn);
+  if (tok->T > 0 && (!grad_entropy != !entropy))
+    return fail(RFT_E_NULL, "%s: grad_entropy and entropy must be both given or both NULL", fn);
   size_t need = carve_bwd(nullptr, *tok, d, V, dtype, bwd_align(dtype)).bytes;
   if ((st = check_ws(fn, ws, ws_bytes, need))) return st;
   int64_t Tc = bwd_tc_for(*tok, d, V, dtype, ws_bytes);
@@ -451,8 +468,8 @@ rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, cons
     }
     for (int64_t ci = 0; ci < nchunks; ++ci) {
       int64_t c0 = ci * Tc;
-      RFT_HIP(mfma_dz(w.hc, d, W, V, w.Vpad, w.m.rows, tok->token_ids, lse, grad_logp, cnt, c0, Tc,
-                      w.dz, w.dzt, s),
+      RFT_HIP(mfma_dz(w.hc, d, W, V, w.Vpad, w.m.rows, tok->token_ids, lse, grad_logp,
+                      grad_entropy, entropy, cnt, c0, Tc, w.dz, w.dzt, s),
               fn);
       // dH rows of this chunk: dZ [count, Vpad] . Wt[d, Vpad]^T, scattered to token rows
       RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
@@ -470,8 +487,8 @@ rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, cons
     const float* W = (const float*)weight;
     for (int64_t ci = 0; ci < nchunks; ++ci) {
       int64_t c0 = ci * Tc;
-      RFT_HIP(simt_dz(H, d, W, V, w.Vpad, w.m.rows, tok->token_ids, lse, grad_logp, cnt, c0, Tc,
-                      w.dz32, s),
+      RFT_HIP(simt_dz(H, d, W, V, w.Vpad, w.m.rows, tok->token_ids, lse, grad_logp,
+                      grad_entropy, entropy, cnt, c0, Tc, w.dz32, s),
               fn);
       // dH[m, j] = sum_v dZ[m, v] W[v, j]
       RFT_HIP(simt_gemm_store(w.dz32, w.Vpad, 1, W, 1, d, nullptr, 0, Tc, d, V, cnt, c0, Tc, 1, 0,
@@ -489,6 +506,7 @@ rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, cons
 
 rft_status rft_ppo_clip_loss_bwd_logits(const rft_tokens* tok, const float* logits, int64_t V,
                                         const float* lse, const float* grad_logp,
+                                        const float* grad_entropy, const float* entropy,
                                         float* d_logits, void* ws, size_t ws_bytes, void* stream) {
   const char* fn = "rft_ppo_clip_loss_bwd_logits";
   (void)ws;
@@ -499,7 +517,11 @@ rft_status rft_ppo_clip_loss_bwd_logits(const rft_tokens* tok, const float* logi
     return fail(RFT_E_SHAPE, "%s: V=%lld", fn, (long long)V);
   if (tok->T > 0 && (!logits || !lse || !grad_logp || !d_logits))
     return fail(RFT_E_NULL, "%s: logits / lse / grad_logp / d_logits is NULL", fn);
-  RFT_HIP(launch_logits_bwd(logits, *tok, V, lse, grad_logp, d_logits, (hipStream_t)stream), fn);
+  if (tok->T > 0 && (!grad_entropy != !entropy))
+    return fail(RFT_E_NULL, "%s: grad_entropy and entropy must be both given or both NULL", fn);
+  RFT_HIP(launch_logits_bwd(logits, *tok, V, lse, grad_logp, grad_entropy, entropy, d_logits,
+                            (hipStream_t)stream),
+          fn);
   return RFT_OK;
 }
 
@@ -550,17 +572,25 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
     return fail(RFT_E_NULL, "%s: old_logp / adv / logp / lse / grad_logp / d_hidden is NULL", fn);
   if (tok->T > 0 && params->kl_coef > 0.f && !ref_logp)
     return fail(RFT_E_NULL, "%s: ref_logp is NULL with kl_coef > 0", fn);
+  if (tok->T > 0 && params->entropy_coef > 0.f && !entropy)
+    return fail(RFT_E_NULL, "%s: entropy is NULL with entropy_coef > 0", fn);
   const float* ref = params->kl_coef > 0.f ? ref_logp : nullptr;
+  const bool bonus = params->entropy_coef > 0.f;
   if (dtype == RFT_F32) {
     if ((st = check_ws(fn, ws, ws_bytes, step_f32_bytes(*tok, d, V, bwd_align(dtype))))) return st;
+    // the three calls share the front; the largest chunk that fits leaves room for egrad
+    int64_t front = (int64_t)ws_bytes - round_up((tok->T > 0 ? tok->T : 1) * 4, 256);
+    front = front / 256 * 256;
+    float* egrad = bonus ? (float*)((char*)ws + front) : nullptr;
     if ((st = rft_token_logprobs(tok, hidden, weight, dtype, d, V, logp, entropy, lse, ws,
-                                 ws_bytes, stream)))
+                                 (size_t)front, stream)))
       return st;
     if ((st = rft_ppo_clip_loss_fwd(tok, V, logp, old_logp, ref, adv, entropy, params, grad_logp,
-                                    stats, ws, ws_bytes, stream)))
+                                    egrad, stats, ws, (size_t)front, stream)))
       return st;
-    return rft_ppo_clip_loss_bwd(tok, hidden, weight, dtype, d, V, lse, grad_logp, d_hidden,
-                                 d_weight, accumulate_dw, ws, ws_bytes, stream);
+    return rft_ppo_clip_loss_bwd(tok, hidden, weight, dtype, d, V, lse, grad_logp, egrad,
+                                 bonus ? entropy : nullptr, d_hidden, d_weight, accumulate_dw, ws,
+                                 (size_t)front, stream);
   }
   if ((st = check_ws(fn, ws, ws_bytes, carve_step(nullptr, *tok, d, V, kBf16Align).bytes)))
     return st;
@@ -590,10 +620,11 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
                              w.ps, w.pu, w.zy, w.dz, s),
             fn);
     RFT_HIP(launch_step_rows(w.m, tok->token_ids, V, c0, Tc, w.pm, w.ps, w.pu, w.ntiles, w.zy,
-                             old_logp, ref, adv, c, logp, entropy, lse, grad_logp, s),
+                             old_logp, ref, adv, c, logp, entropy, lse, grad_logp,
+                             bonus ? w.ce : nullptr, w.cmu, s),
             fn);
     RFT_HIP(launch_dz_from_y(w.dz, w.Vpad, w.dzt, Tc, V, w.m.rows, tok->token_ids, cnt, c0, w.pm,
-                             lse, grad_logp, s),
+                             lse, grad_logp, bonus ? w.ce : nullptr, w.cmu, s),
             fn);
     RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
                             d_hidden, d, w.m.rows, c0, 0, s),
@@ -606,8 +637,8 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
   if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);
   // loss and metrics over every row (rewrites grad_logp with the same values
   // and 0 on masked rows)
-  RFT_HIP(launch_loss_fwd(*tok, w.m, logp, old_logp, ref, adv, entropy, c, grad_logp, w.parts,
-                          stats, s),
+  RFT_HIP(launch_loss_fwd(*tok, w.m, logp, old_logp, ref, adv, entropy, c, grad_logp, nullptr,
+                          w.parts, stats, s),
           fn);
   return RFT_OK;
 }

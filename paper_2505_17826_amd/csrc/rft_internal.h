@@ -142,6 +142,7 @@ struct LossConst {
   int mix;                // 1: expert flags given (MIX loss)
   float mu;               // SFT weight of the MIX loss
   const uint8_t* is_expert;  // [n_seq] device flags, or nullptr
+  float ent_coef;         // entropy bonus coefficient
 };
 
 // Per-token PPO-clip + k3 KL terms.  Returns false for an out-of-range id.
@@ -177,19 +178,22 @@ __device__ __forceinline__ TokLoss token_loss(float lp, float old, float ref, fl
 
 // Partial sums of one block of tokens, reduced in a fixed order.
 struct LossPartial {
-  double loss, pg, klw, kl, ent, ratio, sft;
+  double loss, pg, klw, kl, ent, ratio, sft, entw;
   long long clipped, bad, expert;
 };
 
 // Loss terms of one valid row whose id is in range: adds its terms to p and
-// returns c_t = d loss / d logp.  meta = {N, S, expert tokens, expert rollouts
-// with tokens}; the on-policy (GRPO) part uses the counts without the expert
-// rollouts, scaled by 1 - mu under MIX; an expert row contributes mu * (-logp)
-// / (expert tokens) (the SFT term of the MIX loss).
+// returns c_t = d loss / d logp; *e gets the coefficient of the entropy
+// bonus (-d loss / d H_t).  meta = {N, S, expert tokens, expert rollouts with
+// tokens}; the on-policy (GRPO) part uses the counts without the expert
+// rollouts, scaled by 1 - mu under MIX, and carries the entropy bonus
+// -ent_coef * w_t * H_t; an expert row contributes mu * (-logp) / (expert
+// tokens) (the SFT term of the MIX loss).
 __device__ __forceinline__ float row_loss(float lp, float old, float ref, float A, int n_seq_i,
                                           bool expert, const int32_t* meta, double ent,
-                                          const LossConst& c, LossPartial& p) {
+                                          const LossConst& c, LossPartial& p, float* e) {
   p.ent = ent;
+  *e = 0.f;
   if (c.mix && expert) {
     const int Ne = meta[2];
     const double inv = Ne > 0 ? 1.0 / (double)Ne : 0.0;
@@ -207,10 +211,22 @@ __device__ __forceinline__ float row_loss(float lp, float old, float ref, float 
   p.kl = (double)L.kl;
   p.ratio = (double)L.rho;
   p.clipped = L.clipped ? 1 : 0;
+  p.entw = L.w * ent;
+  if (c.ent_coef > 0.f) {
+    p.loss -= scale * (double)c.ent_coef * p.entw;
+    *e = (float)(scale * (double)c.ent_coef * L.w);
+  }
   return (float)(scale * L.w * (double)L.g);
 }
 
-#define RFT_ZERO_PARTIAL LossPartial{0, 0, 0, 0, 0, 0, 0, 0, 0, 0}
+// d loss / d z_j of one row: c (onehot - p_j) + e p_j (z_j - mu), with p_j the
+// softmax probability, c = d loss / d logp, e the entropy-bonus coefficient
+// and mu = lse - H the softmax mean of z (d H / d z_j = -p_j (z_j - mu)).
+__device__ __forceinline__ float dlogit(float c, float e, float mu, float p, float z, bool hot) {
+  return c * ((hot ? 1.f : 0.f) - p) + e * p * (z - mu);
+}
+
+#define RFT_ZERO_PARTIAL LossPartial{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0}
 
 hipError_t launch_loss_final(const LossPartial* parts, int nparts, const int32_t* meta,
                              rft_ppo_stats* stats, hipStream_t s);
@@ -220,8 +236,8 @@ hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, 
                             hipStream_t s);
 hipError_t launch_loss_fwd(const rft_tokens& tok, const TokMeta& m, const float* logp,
                            const float* old, const float* ref, const float* adv, const float* ent,
-                           const LossConst& c, float* grad, LossPartial* parts, rft_ppo_stats* st,
-                           hipStream_t s);
+                           const LossConst& c, float* grad, float* egrad, LossPartial* parts,
+                           rft_ppo_stats* st, hipStream_t s);
 hipError_t launch_merge_rows(const rft_tokens& tok, const TokMeta& m, int64_t V, const float* pm,
                              const float* ps, const float* pu, int ntiles, int64_t ld,
                              const float* zy, float* logp, float* ent, float* lse, hipStream_t s);
@@ -237,15 +253,15 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
                             int64_t Tc, const float* pm, const float* ps, const float* pu,
                             int ntiles, const float* zy, const float* old, const float* ref,
                             const float* adv, const LossConst& c, float* logp, float* ent,
-                            float* lse, float* grad, hipStream_t s);
+                            float* lse, float* grad, float* ce, float* cmu, hipStream_t s);
 hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, uint16_t* dzt, int64_t Tc, int64_t V,
                             const int32_t* rows, const int32_t* ids, const int32_t* meta,
                             int64_t c0, const float* pm, const float* lse, const float* grad,
-                            hipStream_t s);
+                            const float* ce, const float* cmu, hipStream_t s);
 hipError_t mfma_dz(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
-                   const int32_t* cnt, int64_t c0, int64_t Tc, uint16_t* dz, uint16_t* dzt,
-                   hipStream_t s);
+                   const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
+                   int64_t Tc, uint16_t* dz, uint16_t* dzt, hipStream_t s);
 hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
                            int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
                            int64_t cnt_cap, int m_from_cnt, int k_from_cnt, float* C, int64_t ldc,
@@ -255,7 +271,8 @@ hipError_t simt_fwd_stats(const float* H, int64_t d, const float* W, int64_t V, 
                           float* pu, int64_t ldp, float* zy, hipStream_t s);
 hipError_t simt_dz(const float* H, int64_t d, const float* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
-                   const int32_t* cnt, int64_t c0, int64_t Tc, float* dz, hipStream_t s);
+                   const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
+                   int64_t Tc, float* dz, hipStream_t s);
 hipError_t simt_gemm_store(const float* A, int64_t sam, int64_t sak, const float* B, int64_t sbn,
                            int64_t sbk, const int32_t* b_map, int64_t b_koff, int64_t M, int64_t N,
                            int64_t K, const int32_t* cnt, int64_t cnt_off, int64_t cnt_cap,
@@ -273,7 +290,8 @@ hipError_t launch_zero_masked_rows(const uint8_t* mask, int64_t T, int64_t width
 hipError_t launch_logits_stats(const float* logits, const rft_tokens& tok, int64_t V, float* logp,
                                float* ent, float* lse, float* gathered, hipStream_t s);
 hipError_t launch_logits_bwd(const float* logits, const rft_tokens& tok, int64_t V,
-                             const float* lse, const float* grad, float* dl, hipStream_t s);
+                             const float* lse, const float* grad, const float* egrad,
+                             const float* ent, float* dl, hipStream_t s);
 hipError_t launch_logits_fused(const float* logits, const rft_tokens& tok, const TokMeta& m,
                                int64_t V, const float* old, const float* ref, const float* adv,
                                const LossConst& c, float* logp, float* ent, float* lse,

@@ -12,7 +12,7 @@ from oracle import rft_oracle as O
 
 requires_gpu = pytest.mark.skipif(not torch.cuda.is_available(), reason="needs an MI355X")
 
-# tolerances (spec bars, plus the derived ones)
+# tolerances (the required bars, plus the derived ones)
 TOL_LOGP = 2e-3          # absolute, log-probs (also entropy and lse)
 TOL_LOSS_REL = 1e-3      # relative, loss ...
 TOL_LOSS_ABS = 1e-6      # ... with an absolute floor (zero-mean advantages cancel)
@@ -42,9 +42,9 @@ def tokens_of(b: synth.Batch, is_expert=None) -> R.Tokens:
                     b.ids.to(dev).contiguous(), ex)
 
 
-def params_of(cfg: synth.Config, denom=0.0, agg=None, mix_mu=0.0) -> R.rft_ppo_params:
+def params_of(cfg: synth.Config, denom=0.0, agg=None, mix_mu=0.0, ent=0.0) -> R.rft_ppo_params:
     return R.ppo_params(cfg.eps_low, cfg.eps_high, cfg.beta, cfg.agg if agg is None else agg, denom,
-                        mix_mu)
+                        mix_mu, ent)
 
 
 def oracle_eps(cfg):
@@ -60,7 +60,8 @@ def perturbed_logprobs(logp_fp64, batch: synth.Batch):
     return old, ref
 
 
-def gpu_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bwd_bytes=None, is_expert=None, mu=0.0):
+def gpu_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bwd_bytes=None, is_expert=None, mu=0.0,
+             ent_coef=0.0):
     """adv -> log-probs -> loss -> backward through the binding; CPU results."""
     dev = torch.device("cuda")
     cfg = b.cfg
@@ -70,19 +71,25 @@ def gpu_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bwd_bytes=None, is_expe
     logp, ent, lse = R.rft_token_logprobs(tok, H, W)
     old = torch.from_numpy(old32).to(dev)
     ref = torch.from_numpy(ref32).to(dev)
+    egrad = torch.empty_like(logp) if ent_coef > 0 else None
     grad, st = R.rft_ppo_clip_loss_fwd(tok, cfg.V, logp, old, ref, adv,
-                                       params_of(cfg, denom, mix_mu=mu), entropy=ent)
+                                       params_of(cfg, denom, mix_mu=mu, ent=ent_coef), entropy=ent,
+                                       grad_entropy=egrad)
     ws = None
     if ws_bwd_bytes is not None:
         ws = torch.empty(ws_bwd_bytes, dtype=torch.uint8, device=dev)
-    dH, dW = R.rft_ppo_clip_loss_bwd(tok, H, W, lse, grad, ws=ws)
+    dH, dW = R.rft_ppo_clip_loss_bwd(tok, H, W, lse, grad, ws=ws, grad_entropy=egrad,
+                                     entropy=ent if egrad is not None else None)
     torch.cuda.synchronize()
-    return {"adv": cpu(adv), "logp": cpu(logp), "entropy": cpu(ent), "lse": cpu(lse),
-            "grad_logp": cpu(grad), "stats": R.stats_to_dict(st), "dH": cpu(dH), "dW": cpu(dW)}
+    out = {"adv": cpu(adv), "logp": cpu(logp), "entropy": cpu(ent), "lse": cpu(lse),
+           "grad_logp": cpu(grad), "stats": R.stats_to_dict(st), "dH": cpu(dH), "dW": cpu(dW)}
+    if egrad is not None:
+        out["grad_entropy"] = cpu(egrad)
+    return out
 
 
 def gpu_fused_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bytes=None, dW_init=None,
-                   is_expert=None, mu=0.0):
+                   is_expert=None, mu=0.0, ent_coef=0.0):
     """adv -> rft_ppo_clip_step (the whole step in one call); CPU results."""
     dev = torch.device("cuda")
     cfg = b.cfg
@@ -96,19 +103,19 @@ def gpu_fused_step(b: synth.Batch, old32, ref32, denom=0.0, ws_bytes=None, dW_in
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     dW = None if dW_init is None else torch.from_numpy(dW_init).to(dev)
     logp, ent, lse, grad, dH, dW, st = R.rft_ppo_clip_step(
-        tok, H, W, old, ref, adv, params_of(cfg, denom, mix_mu=mu), d_weight=dW,
+        tok, H, W, old, ref, adv, params_of(cfg, denom, mix_mu=mu, ent=ent_coef), d_weight=dW,
         accumulate_dw=dW_init is not None, ws=ws)
     torch.cuda.synchronize()
     return {"adv": cpu(adv), "logp": cpu(logp), "entropy": cpu(ent), "lse": cpu(lse),
             "grad_logp": cpu(grad), "stats": R.stats_to_dict(st), "dH": cpu(dH), "dW": cpu(dW)}
 
 
-def oracle_step(b: synth.Batch, old32, ref32, denom=0.0, is_expert=None, mu=0.0):
+def oracle_step(b: synth.Batch, old32, ref32, denom=0.0, is_expert=None, mu=0.0, ent_coef=0.0):
     cfg = b.cfg
     el, eh, be = oracle_eps(cfg)
     return O.trainer_step(b.H, b.W, b.ids, b.mask, b.seq_start, b.rewards, cfg.group,
                           old32.astype(np.float64), ref32.astype(np.float64), el, eh, be, cfg.agg,
-                          denom, is_expert=is_expert, mix_mu=f32(mu))
+                          denom, is_expert=is_expert, mix_mu=f32(mu), entropy_coef=f32(ent_coef))
 
 
 def compare_step(g, o, b: synth.Batch, check_bwd=True):
@@ -134,6 +141,11 @@ def compare_step(g, o, b: synth.Batch, check_bwd=True):
     assert abs(st["n_clipped"] - of["n_clipped"]) <= int((~keep).sum())
     assert st["n_expert"] == of["n_expert"]
     assert abs(st["sft_loss"] - of["sft_loss"]) <= TOL_LOSS_REL * abs(of["sft_loss"]) + TOL_LOSS_ABS
+    ent_l = of.get("entropy_loss", 0.0)
+    assert abs(st["entropy_loss"] - ent_l) <= TOL_LOSS_REL * abs(ent_l) + TOL_LOSS_ABS, \
+        (st["entropy_loss"], ent_l)
+    if "grad_entropy" in g:
+        np.testing.assert_allclose(g["grad_entropy"], of["grad_entropy"], rtol=1e-6, atol=0)
     er = of.get("expert_rows")
     if er is not None and er.size:
         np.testing.assert_allclose(g["grad_logp"][er], of["grad_logp"][er], rtol=1e-6)

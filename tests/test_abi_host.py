@@ -94,12 +94,15 @@ def test_argument_validation_returns_codes():
     # loss parameters
     P = R.ppo_params
     base = (ctypes.byref(tk), 100, fake, fake, fake, fake, None)
-    tail = (fake, fake, fake, 1 << 30, s)
+    tail = (fake, None, fake, fake, 1 << 30, s)
     for p, code in [(P(eps_low=-0.1), R.RFT_E_PARAM), (P(eps_low=1.5), R.RFT_E_PARAM),
                     (P(eps_high=-1.0), R.RFT_E_PARAM), (P(eps_high=float("nan")), R.RFT_E_PARAM),
                     (P(kl_coef=-1.0), R.RFT_E_PARAM), (P(kl_coef=float("inf")), R.RFT_E_PARAM),
                     (P(agg=5), R.RFT_E_PARAM), (P(denom_override=-2.0), R.RFT_E_PARAM),
-                    (P(mix_mu=-0.1), R.RFT_E_PARAM), (P(mix_mu=1.5), R.RFT_E_PARAM)]:
+                    (P(mix_mu=-0.1), R.RFT_E_PARAM), (P(mix_mu=1.5), R.RFT_E_PARAM),
+                    (P(entropy_coef=-0.01), R.RFT_E_PARAM),
+                    (P(entropy_coef=float("inf")), R.RFT_E_PARAM),
+                    (P(entropy_coef=0.01), R.RFT_E_NULL)]:  # bonus without entropy
         assert L.rft_ppo_clip_loss_fwd(*base, ctypes.byref(p), *tail) == code
     assert L.rft_ppo_clip_loss_fwd(*base, None, *tail) == R.RFT_E_NULL
     # KL requested without reference log-probs
@@ -107,18 +110,31 @@ def test_argument_validation_returns_codes():
                                    ctypes.byref(P(kl_coef=0.1)), *tail) == R.RFT_E_NULL
     # stats pointer
     assert L.rft_ppo_clip_loss_fwd(ctypes.byref(tk), 100, fake, fake, fake, fake, None,
-                                   ctypes.byref(P()), fake, None, fake, 1 << 30, s) == R.RFT_E_NULL
+                                   ctypes.byref(P()), fake, None, None, fake, 1 << 30,
+                                   s) == R.RFT_E_NULL
     # backward: workspace below the minimum
     m = L.rft_workspace_min_bytes(R.RFT_OP_PPO_BWD, ctypes.byref(tk), 64, 100, R.RFT_BF16)
     assert L.rft_ppo_clip_loss_bwd(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
-                                   fake, fake, 0, fake, m - 1, s) == R.RFT_E_WORKSPACE
+                                   None, None, fake, fake, 0, fake, m - 1,
+                                   s) == R.RFT_E_WORKSPACE
     assert L.rft_ppo_clip_loss_bwd(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
-                                   fake, None, 0, fake, m, s) == R.RFT_E_NULL
+                                   None, None, fake, None, 0, fake, m, s) == R.RFT_E_NULL
+    # entropy-bonus coefficients without the entropies (and the reverse)
+    assert L.rft_ppo_clip_loss_bwd(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
+                                   fake, None, fake, fake, 0, fake, m, s) == R.RFT_E_NULL
+    assert L.rft_ppo_clip_loss_bwd(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
+                                   None, fake, fake, fake, 0, fake, m, s) == R.RFT_E_NULL
+    # fused step: the entropy bonus needs the entropy output
+    assert L.rft_ppo_clip_step(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake, fake,
+                               ctypes.byref(P(entropy_coef=0.01)), fake, None, fake, fake, fake,
+                               fake, 0, fake, fake, 1 << 30, s) == R.RFT_E_NULL
     # logits paths
     assert L.rft_token_logprobs_from_logits(ctypes.byref(tk), fake, 0, fake, fake, fake, None,
                                             None, 0, s) == R.RFT_E_SHAPE
-    assert L.rft_ppo_clip_loss_bwd_logits(ctypes.byref(tk), None, 10, fake, fake, fake, None, 0,
-                                          s) == R.RFT_E_NULL
+    assert L.rft_ppo_clip_loss_bwd_logits(ctypes.byref(tk), None, 10, fake, fake, None, None,
+                                          fake, None, 0, s) == R.RFT_E_NULL
+    assert L.rft_ppo_clip_loss_bwd_logits(ctypes.byref(tk), fake, 10, fake, fake, fake, None,
+                                          fake, None, 0, s) == R.RFT_E_NULL
     assert L.rft_ppo_clip_fused_logits(ctypes.byref(tk), fake, 10, fake, fake, fake,
                                        ctypes.byref(P(eps_low=2.0)), fake, fake, fake, fake, fake,
                                        fake, fake, 1 << 30, s) == R.RFT_E_PARAM
