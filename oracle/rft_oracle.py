@@ -59,6 +59,18 @@ Readings where the paper is silent (it prints no formula):
      1 - mu like the rest of the GRPO part); ``entropy_loss`` reports
      sum_t w_t H_t.  Its gradient reaches the logits through
      dH/dz_j = -p_j (z_j - sum_k p_k z_k).
+  R12 SFT loss (the train-only mode treats SFT as a special case, Sec. 2.1.1):
+     sum_t w_t (-logp_t) over the valid tokens with the weights of R2 (token
+     mean by default, which is the SFT term of R10); d loss / d logp_t = -w_t.
+  R13 DPO loss (the same mode names DPO on preference pairs, Sec. 2.1.1 and
+     Sec. 2.3.1's preference-pair data model; the paper cites DPO and prints no
+     formula, so the published sigmoid form is used): rollouts 2k and 2k+1 are
+     the chosen and the rejected response of pair k; pi_s and rho_s are the sums
+     of the policy and reference log-probs over rollout s's valid tokens (bad
+     ids left out); u_k = beta ((pi_c - rho_c) - (pi_r - rho_r)); a pair counts
+     when both rollouts have a valid token; the loss is the mean over the P
+     counted pairs of -(1 - ls) log sigmoid(u_k) - ls log sigmoid(-u_k) (ls the
+     label smoothing of conservative DPO, 0 by default).
 """
 from __future__ import annotations
 
@@ -352,6 +364,99 @@ def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, e
     else:
         out["entropy_mean"] = 0.0
     return out
+
+
+# ---------------------------------------------------- train-only losses ----
+def _weights(cnt, agg, denom_override):
+    """Aggregation weights w_t of the valid rows (reading R2)."""
+    rows, seq, n, N, S = cnt["rows"], cnt["seq"], cnt["n"], cnt["N"], cnt["S"]
+    if agg == AGG_SEQ_MEAN_TOKEN_MEAN:
+        Sd = denom_override if denom_override > 0 else S
+        return np.zeros(rows.size) if Sd == 0 else 1.0 / (Sd * n[seq].astype(np.float64))
+    if agg == AGG_TOKEN_MEAN:
+        Nd = denom_override if denom_override > 0 else N
+        return np.zeros(rows.size) if Nd == 0 else np.full(rows.size, 1.0 / Nd)
+    raise ValueError(agg)
+
+
+def _good_rows(rows, ids, V):
+    if ids is None or V is None:
+        return np.ones(rows.size, dtype=bool)
+    yy = _int(ids)[rows]
+    return (yy >= 0) & (yy < V)
+
+
+def sft_loss_fwd(logp, mask, seq_start, ids=None, V=None, agg=AGG_TOKEN_MEAN,
+                 denom_override=0.0):
+    """SFT loss of the train-only mode (Sec. 2.1.1; reading R12): the
+    aggregated negative log-likelihood of the valid tokens."""
+    cnt = token_counts(mask, seq_start)
+    rows = cnt["rows"]
+    w = _weights(cnt, agg, denom_override)
+    good = _good_rows(rows, ids, V)
+    lp = _f64(logp)
+    nll = np.where(good, -lp[rows], 0.0)
+    grad = np.zeros(lp.size)
+    grad[rows] = np.where(good, -w, 0.0)
+    return {"loss": float((w * nll).sum()), "grad_logp": grad, "n_valid": cnt["N"],
+            "n_seq_valid": cnt["S"], "n_bad_ids": int((~good).sum())}
+
+
+def _log_sigmoid(x):
+    """log(1 / (1 + exp(-x))) without overflow."""
+    return -(np.maximum(-x, 0.0) + np.log1p(np.exp(-np.abs(x))))
+
+
+def _sigmoid(x):
+    return np.exp(_log_sigmoid(x))
+
+
+def dpo_loss_fwd(logp, ref_logp, mask, seq_start, ids=None, V=None, beta=0.1,
+                 label_smoothing=0.0):
+    """DPO loss over preference pairs (Sec. 2.1.1 train-only mode, Sec. 2.3.1
+    preference pairs; reading R13).  Returns the loss, the per-token gradient,
+    the per-rollout policy sums and the pair statistics."""
+    m = _int(mask) != 0
+    ss = _int(seq_start)
+    n_seq = len(ss) - 1
+    if n_seq % 2:
+        raise ValueError("DPO needs an even number of rollouts")
+    T = m.size
+    lp, rf = _f64(logp), _f64(ref_logp)
+    cnt = token_counts(mask, seq_start)
+    rows = cnt["rows"]
+    good = _good_rows(rows, ids, V)
+    good_row = np.zeros(T, dtype=bool)
+    good_row[rows[good]] = True
+    pi = np.zeros(n_seq)
+    rho = np.zeros(n_seq)
+    for s_ in range(n_seq):
+        rr = [t for t in range(ss[s_], ss[s_ + 1]) if good_row[t]]
+        pi[s_] = float(sum(lp[t] for t in rr))
+        rho[s_] = float(sum(rf[t] for t in rr))
+    n = cnt["n"]
+    c_, r_ = np.arange(0, n_seq, 2), np.arange(1, n_seq, 2)
+    counted = (n[c_] > 0) & (n[r_] > 0)
+    P = int(counted.sum())
+    rc = beta * (pi[c_] - rho[c_])
+    rj = beta * (pi[r_] - rho[r_])
+    u = rc - rj
+    ls = label_smoothing
+    loss_k = -(1.0 - ls) * _log_sigmoid(u) - ls * _log_sigmoid(-u)
+    dldu = -(1.0 - ls) * _sigmoid(-u) + ls * _sigmoid(u)     # d loss_k / d u
+    coef = np.zeros(n_seq)                                   # d loss / d pi_s
+    if P:
+        coef[c_] = np.where(counted, beta * dldu / P, 0.0)
+        coef[r_] = np.where(counted, -beta * dldu / P, 0.0)
+    grad = np.zeros(T)
+    seq_of = np.searchsorted(ss, np.arange(T), side="right") - 1
+    grad[good_row] = coef[seq_of[good_row]]
+    mean = (lambda x: float(x[counted].sum() / P)) if P else (lambda x: 0.0)
+    return {"loss": mean(loss_k), "chosen_reward": mean(rc), "rejected_reward": mean(rj),
+            "reward_acc": float((u[counted] > 0).sum() / P) if P else 0.0,
+            "margin_mean": mean(u), "n_pairs": P, "n_valid": cnt["N"],
+            "n_bad_ids": int((~good).sum()), "grad_logp": grad, "seq_logp": pi,
+            "pair_counted": counted, "margins": u}
 
 
 # -------------------------------------------------------------- backward ----

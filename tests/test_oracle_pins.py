@@ -718,3 +718,157 @@ def test_entropy_bonus_torch_autograd():
     np.testing.assert_allclose(dH, Ht.grad.numpy(), rtol=1e-10, atol=1e-14)
     np.testing.assert_allclose(dW, Wt.grad.numpy(), rtol=1e-10, atol=1e-14)
     np.testing.assert_allclose(dWs, dW[[1, 4]], rtol=1e-12, atol=1e-15)
+
+
+# ------------------------------------------------------ SFT (R12) -----------
+def test_golden_sft_two_rollouts():
+    g = GOLD["sft_two_rollouts"]
+    lens = [len(x) for x in g["logp"]]
+    ss, mask = _layout(lens, 3)
+    logp = np.zeros(6)
+    for i, x in enumerate(g["logp"]):
+        logp[i * 3:i * 3 + len(x)] = x
+    tm = O.sft_loss_fwd(logp, mask, ss, agg=O.AGG_TOKEN_MEAN)
+    assert tm["loss"] == pytest.approx(g["loss_token_mean"], rel=1e-15)
+    np.testing.assert_allclose(tm["grad_logp"][mask != 0], g["grad_token_mean"], rtol=1e-15)
+    sm = O.sft_loss_fwd(logp, mask, ss, agg=O.AGG_SEQ_MEAN_TOKEN_MEAN)
+    assert sm["loss"] == pytest.approx(g["loss_seq_mean"], rel=1e-15)
+    assert sm["grad_logp"][0] == pytest.approx(g["grad_seq_mean"][0], rel=1e-15)
+    np.testing.assert_allclose(sm["grad_logp"][3:6], g["grad_seq_mean"][1], rtol=1e-15)
+    assert np.all(sm["grad_logp"][mask == 0] == 0)
+
+
+def test_sft_matches_mix_all_expert_and_finite_differences():
+    """Token-mean SFT is the MIX loss with every rollout an expert one and
+    mu = 1 (a separate code path); bad ids are left out of both; central
+    differences of the loss in each logp give the gradient."""
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=71)
+    ids = ids.copy()
+    ids[np.nonzero(mask)[0][3]] = V + 2           # one bad id
+    sft = O.sft_loss_fwd(logp, mask, ss, ids, V, agg=O.AGG_TOKEN_MEAN)
+    mix = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.0, 0,
+                              is_expert=np.ones(adv.size, np.uint8), mix_mu=1.0)
+    assert sft["n_bad_ids"] == 1 == mix["n_bad_ids"]
+    assert sft["loss"] == pytest.approx(mix["loss"], rel=1e-13)
+    np.testing.assert_allclose(sft["grad_logp"], mix["grad_logp"], rtol=1e-13, atol=0)
+    for agg in (0, 1):
+        base = O.sft_loss_fwd(logp, mask, ss, ids, V, agg=agg, denom_override=3.5 * agg)
+        for t in np.nonzero(mask)[0][:12]:
+            lp1, lp2 = logp.copy(), logp.copy()
+            lp1[t] += 1e-6
+            lp2[t] -= 1e-6
+            fd = (O.sft_loss_fwd(lp1, mask, ss, ids, V, agg=agg, denom_override=3.5 * agg)["loss"]
+                  - O.sft_loss_fwd(lp2, mask, ss, ids, V, agg=agg,
+                                   denom_override=3.5 * agg)["loss"]) / 2e-6
+            assert fd == pytest.approx(base["grad_logp"][t], rel=1e-7, abs=1e-10)
+
+
+# ------------------------------------------------------ DPO (R13) -----------
+def _dpo_golden_layout():
+    g = GOLD["dpo_single_pair"]
+    ss = np.array([0, 2, 3], np.int32)
+    mask = np.ones(3, np.uint8)
+    logp = np.array(g["logp_chosen"] + g["logp_rejected"])
+    ref = np.array(g["ref_chosen"] + g["ref_rejected"])
+    return g, ss, mask, logp, ref
+
+
+def test_golden_dpo_single_pair():
+    g, ss, mask, logp, ref = _dpo_golden_layout()
+    out = O.dpo_loss_fwd(logp, ref, mask, ss, beta=g["beta"])
+    assert out["loss"] == pytest.approx(g["loss"], rel=1e-15)
+    np.testing.assert_allclose(out["grad_logp"], [g["grad_chosen"]] * 2 + [g["grad_rejected"]],
+                               rtol=1e-15)
+    assert out["chosen_reward"] == pytest.approx(g["chosen_reward"], rel=1e-15)
+    assert out["rejected_reward"] == pytest.approx(g["rejected_reward"], rel=1e-15)
+    assert out["margin_mean"] == pytest.approx(g["margin"], rel=1e-15)
+    assert out["reward_acc"] == 1.0 and out["n_pairs"] == 1
+    ls = O.dpo_loss_fwd(logp, ref, mask, ss, beta=g["beta"], label_smoothing=0.1)
+    assert ls["loss"] == pytest.approx(g["loss_label_smoothing_0.1"], rel=1e-15)
+
+
+def _dpo_case(seed, n_pairs=5, pad=6, V=30):
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(1, pad + 1, size=2 * n_pairs)
+    lens[3] = 0                                    # pair 1 has an empty rejected rollout
+    ss, mask = _layout(lens, pad)
+    T = mask.size
+    logp = -rng.random(T) * 3
+    ref = logp + rng.standard_normal(T) * 0.5
+    ids = rng.integers(0, V, size=T)
+    return ss, mask, logp, ref, ids, V
+
+
+def test_dpo_policy_equals_reference():
+    """pi = rho: every margin is 0, the loss is ln 2 whatever the smoothing,
+    and each token's gradient is +-beta (2 ls - 1) / (2 P)."""
+    ss, mask, logp, _, ids, V = _dpo_case(72)
+    for ls in (0.0, 0.2):
+        out = O.dpo_loss_fwd(logp, logp, mask, ss, ids, V, beta=0.3, label_smoothing=ls)
+        P = out["n_pairs"]
+        assert P == 4
+        assert out["loss"] == pytest.approx(math.log(2.0), rel=1e-15)
+        g = 0.3 * (2 * ls - 1) / (2 * P)
+        for s_ in range(len(ss) - 1):
+            k, role = divmod(s_, 2)
+            want = 0.0 if k == 1 else (g if role == 0 else -g)
+            rr = [t for t in range(ss[s_], ss[s_ + 1]) if mask[t]]
+            np.testing.assert_allclose(out["grad_logp"][rr], want, rtol=1e-14, atol=0)
+
+
+def test_dpo_swap_identity():
+    """Swapping chosen and rejected turns each -log sigmoid(u) into
+    -log sigmoid(-u) = -log sigmoid(u) + u: the mean loss grows by the mean
+    margin, and the tokens of the new chosen rollout get -beta sigmoid(u) / P,
+    those of the new rejected one +beta sigmoid(u) / P."""
+    ss, mask, logp, ref, ids, V = _dpo_case(73)
+    beta = 0.2
+    out = O.dpo_loss_fwd(logp, ref, mask, ss, ids, V, beta=beta)
+    n_seq = len(ss) - 1
+    lens = np.diff(ss)
+    perm = np.arange(n_seq).reshape(-1, 2)[:, ::-1].ravel()
+    rows = np.concatenate([np.arange(ss[i], ss[i + 1]) for i in perm])
+    ss2 = np.concatenate([[0], np.cumsum(lens[perm])]).astype(np.int32)
+    sw = O.dpo_loss_fwd(logp[rows], ref[rows], mask[rows], ss2, ids[rows], V, beta=beta)
+    assert sw["loss"] == pytest.approx(out["loss"] + out["margin_mean"], rel=1e-13)
+    assert sw["margin_mean"] == pytest.approx(-out["margin_mean"], rel=1e-13)
+    P = out["n_pairs"]
+    seq2 = np.searchsorted(ss2, np.arange(rows.size), side="right") - 1
+    for t in np.nonzero(mask[rows])[0]:
+        pair, role = divmod(int(seq2[t]), 2)
+        if not out["pair_counted"][pair]:
+            assert sw["grad_logp"][t] == 0.0
+            continue
+        sg = 1.0 / (1.0 + math.exp(-out["margins"][pair]))
+        want = -beta * sg / P if role == 0 else beta * sg / P
+        assert sw["grad_logp"][t] == pytest.approx(want, rel=1e-12)
+
+
+def test_dpo_torch_autograd_and_bad_ids():
+    """torch float64 autograd of the naive pairwise expression (segment sums
+    by index_add, F.logsigmoid) as a third implementation; a bad id is left out
+    of the sums and gets no gradient."""
+    ss, mask, logp, ref, ids, V = _dpo_case(74)
+    ids = ids.copy()
+    bad_t = int(np.nonzero(mask)[0][5])
+    ids[bad_t] = -1
+    beta, ls = 0.15, 0.05
+    out = O.dpo_loss_fwd(logp, ref, mask, ss, ids, V, beta=beta, label_smoothing=ls)
+    assert out["n_bad_ids"] == 1 and out["grad_logp"][bad_t] == 0.0
+    T = mask.size
+    keep = torch.tensor((mask != 0) & (ids >= 0) & (ids < V), dtype=torch.float64)
+    seq = torch.tensor(np.searchsorted(ss, np.arange(T), side="right") - 1)
+    lp = torch.tensor(logp, requires_grad=True)
+    n_seq = len(ss) - 1
+    pi = torch.zeros(n_seq, dtype=torch.float64).index_add(0, seq, lp * keep)
+    rho = torch.zeros(n_seq, dtype=torch.float64).index_add(0, seq, torch.tensor(ref) * keep)
+    n_i = torch.zeros(n_seq, dtype=torch.float64).index_add(0, seq,
+                                                              torch.tensor(mask, dtype=torch.float64))
+    u = beta * ((pi[0::2] - rho[0::2]) - (pi[1::2] - rho[1::2]))
+    ok = (n_i[0::2] > 0) & (n_i[1::2] > 0)
+    lk = -(1 - ls) * torch.nn.functional.logsigmoid(u) - ls * torch.nn.functional.logsigmoid(-u)
+    loss = lk[ok].sum() / ok.sum()
+    loss.backward()
+    assert loss.item() == pytest.approx(out["loss"], rel=1e-13)
+    np.testing.assert_allclose(out["grad_logp"], lp.grad.numpy(), rtol=1e-12, atol=1e-16)
+    assert out["reward_acc"] == pytest.approx(float((u[ok] > 0).double().mean()), rel=1e-15)
