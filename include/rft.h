@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define RFT_ABI_VERSION 3
+#define RFT_ABI_VERSION 4
 
 typedef enum {
   RFT_OK = 0,
@@ -83,7 +83,9 @@ typedef enum {
   RFT_OP_PPO_BWD = 3,
   RFT_OP_PPO_BWD_LOGITS = 4,
   RFT_OP_PPO_FUSED_LOGITS = 5,
-  RFT_OP_PPO_STEP = 6
+  RFT_OP_PPO_STEP = 6,
+  RFT_OP_SFT_FWD = 7,
+  RFT_OP_DPO_FWD = 8
 } rft_op;
 
 /* (host struct holding device pointers) */
@@ -133,6 +135,19 @@ typedef struct {
   int64_t n_expert;     /* valid tokens of expert rollouts            */
   double entropy_loss;  /* sum_t w_t H_t over on-policy tokens (0 if no entropy given) */
 } rft_ppo_stats;
+
+/* (device struct) DPO loss value and metrics written by rft_dpo_loss_fwd.
+ * Means are over the counted pairs (both rollouts have a valid token). */
+typedef struct {
+  double loss;             /* mean of -(1-ls) log sigmoid(u) - ls log sigmoid(-u) */
+  double chosen_reward;    /* mean beta (pi_c - rho_c)                           */
+  double rejected_reward;  /* mean beta (pi_r - rho_r)                           */
+  double reward_acc;       /* fraction of pairs with u > 0                       */
+  double margin_mean;      /* mean u                                             */
+  int64_t n_pairs;         /* counted pairs P                                    */
+  int64_t n_valid;         /* valid tokens N                                     */
+  int64_t n_bad_ids;
+} rft_dpo_stats;
 
 /* Version of this ABI (RFT_ABI_VERSION). */
 int rft_abi_version(void);
@@ -277,6 +292,40 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
                              float* lse, float* grad_logp, float* d_hidden, float* d_weight,
                              int32_t accumulate_dw, rft_ppo_stats* stats, void* ws,
                              size_t ws_bytes, void* stream);
+
+/* SFT loss of the train-only mode (Sec. 2.1.1: SFT as a special case of
+ * training from stored experiences): loss = sum_t w_t (-logp_t) over the
+ * valid tokens, w_t from `agg` and `denom_override` as in rft_ppo_params
+ * (RFT_AGG_TOKEN_MEAN gives the mean negative log-likelihood, the SFT term of
+ * the MIX loss); grad_logp[t] = -w_t (0 on masked rows and for out-of-range
+ * ids, which count in n_bad_ids).  tokens.is_expert is ignored.  Writes
+ * loss = sft_loss, n_valid, n_seq_valid and n_bad_ids of *stats (the PPO
+ * fields are 0).  The gradient feeds rft_ppo_clip_loss_bwd or
+ * rft_ppo_clip_loss_bwd_logits.
+ * Errors: RFT_E_NULL, RFT_E_SHAPE, RFT_E_PARAM (agg unknown, denom_override
+ * negative or not finite), RFT_E_WORKSPACE. */
+rft_status rft_sft_loss_fwd(const rft_tokens* tok, int64_t V, const float* logp, int32_t agg,
+                            double denom_override, float* grad_logp, rft_ppo_stats* stats,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/* DPO loss of the train-only mode (Sec. 2.1.1, DPO on preference pairs;
+ * Sec. 2.3.1, the preference-pair data model).  Rollouts 2k and 2k+1 are the
+ * chosen and the rejected response of pair k (n_seq must be even).  With
+ * pi_s, rho_s the sums of logp and ref_logp over rollout s's valid tokens
+ * whose id is in range (fp64, fixed order):
+ *   u_k = beta ((pi_2k - rho_2k) - (pi_2k+1 - rho_2k+1)),
+ *   loss = (1/P) sum_k [-(1 - ls) log sigmoid(u_k) - ls log sigmoid(-u_k)]
+ * over the P pairs whose two rollouts both have a valid token (ls = label
+ * smoothing, 0 for plain DPO).  grad_logp[t] = d loss / d pi_s of the row's
+ * rollout (0 on masked rows, rows with an out-of-range id and rows of pairs
+ * that do not count); it feeds the backward calls as for the other losses.
+ * seq_logp [n_seq] (may be NULL) receives pi_s.  Inputs f32 [T].
+ * Errors: RFT_E_NULL, RFT_E_SHAPE (odd n_seq), RFT_E_PARAM (beta <= 0 or not
+ * finite, ls outside [0, 0.5]), RFT_E_WORKSPACE. */
+rft_status rft_dpo_loss_fwd(const rft_tokens* tok, int64_t V, const float* logp,
+                            const float* ref_logp, float beta, float label_smoothing,
+                            float* grad_logp, float* seq_logp, rft_dpo_stats* stats, void* ws,
+                            size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -23,7 +23,8 @@ RFT_OK, RFT_E_NULL, RFT_E_SHAPE, RFT_E_DTYPE, RFT_E_PARAM, RFT_E_WORKSPACE, \
 RFT_F32, RFT_BF16 = 0, 1
 RFT_AGG_SEQ_MEAN_TOKEN_MEAN, RFT_AGG_TOKEN_MEAN = 0, 1
 (RFT_OP_TOKEN_LOGPROBS, RFT_OP_TOKEN_LOGPROBS_FROM_LOGITS, RFT_OP_PPO_FWD, RFT_OP_PPO_BWD,
- RFT_OP_PPO_BWD_LOGITS, RFT_OP_PPO_FUSED_LOGITS, RFT_OP_PPO_STEP) = range(7)
+ RFT_OP_PPO_BWD_LOGITS, RFT_OP_PPO_FUSED_LOGITS, RFT_OP_PPO_STEP, RFT_OP_SFT_FWD,
+ RFT_OP_DPO_FWD) = range(9)
 
 _p = ctypes.c_void_p
 _i64 = ctypes.c_int64
@@ -51,7 +52,15 @@ class rft_ppo_stats(ctypes.Structure):
                 ("n_expert", ctypes.c_int64), ("entropy_loss", ctypes.c_double)]
 
 
+class rft_dpo_stats(ctypes.Structure):
+    _fields_ = [("loss", ctypes.c_double), ("chosen_reward", ctypes.c_double),
+                ("rejected_reward", ctypes.c_double), ("reward_acc", ctypes.c_double),
+                ("margin_mean", ctypes.c_double), ("n_pairs", ctypes.c_int64),
+                ("n_valid", ctypes.c_int64), ("n_bad_ids", ctypes.c_int64)]
+
+
 STATS_BYTES = ctypes.sizeof(rft_ppo_stats)
+DPO_STATS_BYTES = ctypes.sizeof(rft_dpo_stats)
 
 _SIGS = {
     "rft_abi_version": (ctypes.c_int, []),
@@ -81,6 +90,10 @@ _SIGS = {
                                          _i64, _p, _p, _p, ctypes.POINTER(rft_ppo_params), _p, _p,
                                          _p, _p, _p, _p, ctypes.c_int32, _p, _p, ctypes.c_size_t,
                                          _p]),
+    "rft_sft_loss_fwd": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _i64, _p, ctypes.c_int32,
+                                        ctypes.c_double, _p, _p, _p, ctypes.c_size_t, _p]),
+    "rft_dpo_loss_fwd": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _i64, _p, _p, ctypes.c_float,
+                                        ctypes.c_float, _p, _p, _p, _p, ctypes.c_size_t, _p]),
 }
 
 _LIB = None
@@ -173,11 +186,13 @@ def ppo_params(eps_low=0.2, eps_high=0.2, kl_coef=0.0, agg=RFT_AGG_SEQ_MEAN_TOKE
     return rft_ppo_params(eps_low, eps_high, kl_coef, agg, denom_override, mix_mu, entropy_coef)
 
 
-def stats_to_dict(buf: torch.Tensor) -> dict:
-    """Decode an rft_ppo_stats device buffer (synchronises on the copy)."""
+def stats_to_dict(buf: torch.Tensor, kind=None) -> dict:
+    """Decode an rft_ppo_stats (or, with kind=rft_dpo_stats, an rft_dpo_stats)
+    device buffer (synchronises on the copy)."""
+    kind = rft_ppo_stats if kind is None else kind
     raw = bytes(buf.detach().cpu().numpy().tobytes())
-    s = rft_ppo_stats.from_buffer_copy(raw[:STATS_BYTES])
-    return {k: getattr(s, k) for k, _ in rft_ppo_stats._fields_}
+    s = kind.from_buffer_copy(raw[:ctypes.sizeof(kind)])
+    return {k: getattr(s, k) for k, _ in kind._fields_}
 
 
 def workspace_bytes(op, tokens: Tokens, d=0, V=1, dtype=RFT_F32, minimum=False) -> int:
@@ -332,6 +347,39 @@ def rft_ppo_clip_step(tokens: Tokens, hidden, weight, old_logp, ref_logp, adv, p
                                    _ptr(d_hidden), _ptr(d_weight), 1 if accumulate_dw else 0,
                                    _ptr(stats), _ptr(ws), nb, _stream(stream)))
     return logp, entropy, lse, grad_logp, d_hidden, d_weight, stats
+
+
+def rft_sft_loss_fwd(tokens: Tokens, V, logp, agg=RFT_AGG_TOKEN_MEAN, denom_override=0.0,
+                     grad_logp=None, stats=None, ws=None, stream=None):
+    """Returns (grad_logp, stats)."""
+    _need_gpu(logp)
+    dev = logp.device
+    grad_logp = torch.empty_like(logp) if grad_logp is None else grad_logp
+    stats = torch.zeros(STATS_BYTES, dtype=torch.uint8, device=dev) if stats is None else stats
+    ws, nb = _workspace(workspace_bytes(RFT_OP_SFT_FWD, tokens, 0, V), dev, ws)
+    tk = tokens.c()
+    _check(lib().rft_sft_loss_fwd(ctypes.byref(tk), V, _ptr(logp), agg, denom_override,
+                                  _ptr(grad_logp), _ptr(stats), _ptr(ws), nb, _stream(stream)))
+    return grad_logp, stats
+
+
+def rft_dpo_loss_fwd(tokens: Tokens, V, logp, ref_logp, beta=0.1, label_smoothing=0.0,
+                     grad_logp=None, seq_logp=None, want_seq_logp=True, stats=None, ws=None,
+                     stream=None):
+    """Returns (grad_logp, seq_logp, stats); decode stats with
+    stats_to_dict(stats, rft_dpo_stats)."""
+    _need_gpu(logp, ref_logp)
+    dev = logp.device
+    grad_logp = torch.empty_like(logp) if grad_logp is None else grad_logp
+    if seq_logp is None and want_seq_logp:
+        seq_logp = torch.empty(tokens.n_seq, dtype=torch.float32, device=dev)
+    stats = torch.zeros(DPO_STATS_BYTES, dtype=torch.uint8, device=dev) if stats is None else stats
+    ws, nb = _workspace(workspace_bytes(RFT_OP_DPO_FWD, tokens, 0, V), dev, ws)
+    tk = tokens.c()
+    _check(lib().rft_dpo_loss_fwd(ctypes.byref(tk), V, _ptr(logp), _ptr(ref_logp), beta,
+                                  label_smoothing, _ptr(grad_logp), _ptr(seq_logp), _ptr(stats),
+                                  _ptr(ws), nb, _stream(stream)))
+    return grad_logp, seq_logp, stats
 
 
 def loaded_library_path() -> str:

@@ -21,7 +21,7 @@ LIB = os.path.join(HERE, "librft.so")
 ARCH = os.environ.get("RFT_OFFLOAD_ARCH", "gfx950")
 
 SOURCES = ["rft_abi.hip", "k_tokens.hip", "k_adv_loss.hip", "k_gemm_mfma.hip", "k_simt.hip",
-           "k_logits.hip", "k_step.hip"]
+           "k_logits.hip", "k_step.hip", "k_pref.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,

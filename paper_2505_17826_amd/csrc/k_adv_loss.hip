@@ -1,6 +1,6 @@
-// GRPO group advantages, the per-token PPO-clip/KL loss with its fixed-order
-// fp64 reduction, and the merge of the per-tile log-sum-exp partials into
-// per-token log-prob / entropy / lse.
+// GRPO group advantages, the per-token PPO-clip/KL loss and the SFT loss with
+// their fixed-order fp64 reduction, and the merge of the per-tile
+// log-sum-exp partials into per-token log-prob / entropy / lse.
 #include "rft_internal.h"
 
 namespace rft {
@@ -107,7 +107,7 @@ __global__ void __launch_bounds__(256) k_loss_fwd(
 // One block: fixed-order sum of the block partials into the stats struct.
 __global__ void __launch_bounds__(1024) k_loss_final(const LossPartial* __restrict__ parts, int n,
                                                      const int32_t* __restrict__ meta,
-                                                     rft_ppo_stats* __restrict__ st) {
+                                                     rft_ppo_stats* __restrict__ st, int sft_only) {
   LossPartial p = RFT_ZERO_PARTIAL;
   // each thread sums a contiguous run, in order
   int per = (n + 1023) / 1024;
@@ -136,16 +136,56 @@ __global__ void __launch_bounds__(1024) k_loss_final(const LossPartial* __restri
     st->n_seq_valid = S;
     st->n_clipped = out.clipped;
     st->n_bad_ids = out.bad;
-    st->sft_loss = Ne > 0 ? out.sft / (double)Ne : 0.0;
+    st->sft_loss = sft_only ? st->loss : (Ne > 0 ? out.sft / (double)Ne : 0.0);
     st->n_expert = Ne;
     st->entropy_loss = N > 0 ? out.entw : 0.0;
   }
 }
 
 hipError_t launch_loss_final(const LossPartial* parts, int nparts, const int32_t* meta,
-                             rft_ppo_stats* stats, hipStream_t s) {
-  k_loss_final<<<1, 1024, 0, s>>>(parts, nparts, meta, stats);
+                             rft_ppo_stats* stats, hipStream_t s, int sft_only) {
+  k_loss_final<<<1, 1024, 0, s>>>(parts, nparts, meta, stats, sft_only);
   return hipGetLastError();
+}
+
+// SFT loss of the train-only mode: sum_t w_t (-logp_t) over the valid rows
+// whose id is in range, w_t the aggregation weight; grad = -w_t.
+__global__ void __launch_bounds__(256) k_sft_fwd(
+    const uint8_t* __restrict__ mask, const int32_t* __restrict__ ids,
+    const int32_t* __restrict__ kidx, const int32_t* __restrict__ row_seq,
+    const int32_t* __restrict__ n_i, const int32_t* __restrict__ meta, int64_t T, int64_t V,
+    const float* __restrict__ logp, int agg, double denom, float* __restrict__ grad,
+    LossPartial* __restrict__ parts) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  LossPartial p = RFT_ZERO_PARTIAL;
+  if (t < T) {
+    const int k = kidx[t];
+    float g = 0.f;
+    if (k >= 0) {
+      const int y = ids[t];
+      if (y < 0 || (int64_t)y >= V) {
+        p.bad = 1;
+      } else {
+        const double w = agg_weight(agg, denom, n_i[row_seq[k]], meta[0], meta[1]);
+        p.loss = w * -(double)logp[t];
+        g = (float)-w;
+      }
+    }
+    grad[t] = g;
+  }
+  block_reduce_partial(p, parts + blockIdx.x);
+}
+
+hipError_t launch_sft_fwd(const rft_tokens& tok, const TokMeta& m, int64_t V, const float* logp,
+                          int agg, double denom, float* grad, LossPartial* parts,
+                          rft_ppo_stats* st, hipStream_t s) {
+  const int nb = (int)((tok.T + 255) / 256);
+  if (nb > 0)
+    k_sft_fwd<<<nb, 256, 0, s>>>(tok.mask, tok.token_ids, m.kidx, m.row_seq, m.n_i, m.meta, tok.T,
+                                 V, logp, agg, denom, grad, parts);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_loss_final(parts, nb, m.meta, st, s, 1);
 }
 
 hipError_t launch_loss_fwd(const rft_tokens& tok, const TokMeta& m, const float* logp,

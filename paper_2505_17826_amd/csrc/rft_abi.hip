@@ -164,6 +164,24 @@ LossWs carve_loss(void* base, const rft_tokens& tok, bool per_row) {
   return w;
 }
 
+struct DpoCarve {
+  TokMeta m;
+  DpoWs d;
+  size_t bytes;
+};
+DpoCarve carve_dpo(void* base, const rft_tokens& tok) {
+  Carver c(base);
+  DpoCarve w;
+  w.m = carve_tokmeta(c, tok.T, tok.n_seq);
+  const size_t n = (size_t)(tok.n_seq > 0 ? tok.n_seq : 1);
+  w.d.pi = c.take<double>(n);
+  w.d.rho = c.take<double>(n);
+  w.d.bad = c.take<int32_t>(n);
+  w.d.coef = c.take<float>(n);
+  w.bytes = c.bytes();
+  return w;
+}
+
 struct BwdWs {
   TokMeta m;
   uint16_t *hc, *wt, *dz, *dzt, *ht;  // bf16 path
@@ -311,7 +329,10 @@ size_t rft_workspace_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, 
     case RFT_OP_PPO_BWD_LOGITS:
       return 0;
     case RFT_OP_PPO_FWD:
+    case RFT_OP_SFT_FWD:
       return carve_loss(nullptr, *tok, false).bytes;
+    case RFT_OP_DPO_FWD:
+      return carve_dpo(nullptr, *tok).bytes;
     case RFT_OP_PPO_FUSED_LOGITS:
       return carve_loss(nullptr, *tok, true).bytes;
     case RFT_OP_PPO_BWD: {
@@ -639,6 +660,63 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
   // and 0 on masked rows)
   RFT_HIP(launch_loss_fwd(*tok, w.m, logp, old_logp, ref, adv, entropy, c, grad_logp, nullptr,
                           w.parts, stats, s),
+          fn);
+  return RFT_OK;
+}
+
+rft_status rft_sft_loss_fwd(const rft_tokens* tok, int64_t V, const float* logp, int32_t agg,
+                            double denom_override, float* grad_logp, rft_ppo_stats* stats,
+                            void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "rft_sft_loss_fwd";
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if (V < 1) return fail(RFT_E_SHAPE, "%s: V=%lld", fn, (long long)V);
+  if (agg != RFT_AGG_SEQ_MEAN_TOKEN_MEAN && agg != RFT_AGG_TOKEN_MEAN)
+    return fail(RFT_E_PARAM, "%s: agg=%d unknown", fn, agg);
+  if (!(denom_override >= 0.0) || !std::isfinite(denom_override))
+    return fail(RFT_E_PARAM, "%s: denom_override=%g must be finite and >= 0", fn, denom_override);
+  if (!stats) return fail(RFT_E_NULL, "%s: stats is NULL", fn);
+  if (tok->T > 0 && (!logp || !grad_logp))
+    return fail(RFT_E_NULL, "%s: logp / grad_logp is NULL", fn);
+  LossWs w = carve_loss(nullptr, *tok, false);
+  if ((st = check_ws(fn, ws, ws_bytes, w.bytes))) return st;
+  w = carve_loss(ws, *tok, false);
+  hipStream_t s = (hipStream_t)stream;
+  rft_tokens t2 = *tok;
+  t2.is_expert = nullptr;
+  RFT_HIP(launch_tokmeta(t2, w.m, s), fn);
+  RFT_HIP(launch_sft_fwd(t2, w.m, V, logp, agg, denom_override, grad_logp, w.parts, stats, s), fn);
+  return RFT_OK;
+}
+
+rft_status rft_dpo_loss_fwd(const rft_tokens* tok, int64_t V, const float* logp,
+                            const float* ref_logp, float beta, float label_smoothing,
+                            float* grad_logp, float* seq_logp, rft_dpo_stats* stats, void* ws,
+                            size_t ws_bytes, void* stream) {
+  const char* fn = "rft_dpo_loss_fwd";
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if (V < 1) return fail(RFT_E_SHAPE, "%s: V=%lld", fn, (long long)V);
+  if (tok->n_seq % 2)
+    return fail(RFT_E_SHAPE, "%s: n_seq=%lld must be even (chosen, rejected pairs)", fn,
+                (long long)tok->n_seq);
+  if (!(beta > 0.f) || !std::isfinite(beta))
+    return fail(RFT_E_PARAM, "%s: beta=%g must be finite and > 0", fn, (double)beta);
+  if (!(label_smoothing >= 0.f && label_smoothing <= 0.5f))
+    return fail(RFT_E_PARAM, "%s: label_smoothing=%g must be in [0, 0.5]", fn,
+                (double)label_smoothing);
+  if (!stats) return fail(RFT_E_NULL, "%s: stats is NULL", fn);
+  if (tok->T > 0 && (!logp || !ref_logp || !grad_logp))
+    return fail(RFT_E_NULL, "%s: logp / ref_logp / grad_logp is NULL", fn);
+  DpoCarve w = carve_dpo(nullptr, *tok);
+  if ((st = check_ws(fn, ws, ws_bytes, w.bytes))) return st;
+  w = carve_dpo(ws, *tok);
+  hipStream_t s = (hipStream_t)stream;
+  rft_tokens t2 = *tok;
+  t2.is_expert = nullptr;
+  RFT_HIP(launch_tokmeta(t2, w.m, s), fn);
+  RFT_HIP(launch_dpo(t2, w.m, V, logp, ref_logp, beta, label_smoothing, w.d, grad_logp, seq_logp,
+                     stats, s),
           fn);
   return RFT_OK;
 }

@@ -152,17 +152,23 @@ struct TokLoss {
   bool clipped;
 };
 
+// Aggregation weight w_t of a valid token of a rollout with n_seq_i valid
+// tokens, among N valid tokens in S rollouts (or the override denominator).
+__device__ __forceinline__ double agg_weight(int agg, double denom, int n_seq_i, int N, int S) {
+  double den;
+  if (agg == RFT_AGG_SEQ_MEAN_TOKEN_MEAN) {
+    double Sd = denom > 0 ? denom : (double)S;
+    den = Sd * (double)n_seq_i;
+  } else {
+    den = denom > 0 ? denom : (double)N;
+  }
+  return den > 0 ? 1.0 / den : 0.0;
+}
+
 __device__ __forceinline__ TokLoss token_loss(float lp, float old, float ref, float A, int n_seq_i,
                                               int N, int S, const LossConst& c) {
   TokLoss r;
-  double den;
-  if (c.agg == RFT_AGG_SEQ_MEAN_TOKEN_MEAN) {
-    double Sd = c.denom > 0 ? c.denom : (double)S;
-    den = Sd * (double)n_seq_i;
-  } else {
-    den = c.denom > 0 ? c.denom : (double)N;
-  }
-  r.w = den > 0 ? 1.0 / den : 0.0;
+  r.w = agg_weight(c.agg, c.denom, n_seq_i, N, S);
   float delta = lp - old;
   r.rho = expf(delta);
   float lo = 1.f - c.eps_low, hi = 1.f + c.eps_high;
@@ -229,7 +235,18 @@ __device__ __forceinline__ float dlogit(float c, float e, float mu, float p, flo
 #define RFT_ZERO_PARTIAL LossPartial{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0}
 
 hipError_t launch_loss_final(const LossPartial* parts, int nparts, const int32_t* meta,
-                             rft_ppo_stats* stats, hipStream_t s);
+                             rft_ppo_stats* stats, hipStream_t s, int sft_only = 0);
+hipError_t launch_sft_fwd(const rft_tokens& tok, const TokMeta& m, int64_t V, const float* logp,
+                          int agg, double denom, float* grad, LossPartial* parts,
+                          rft_ppo_stats* st, hipStream_t s);
+struct DpoWs {
+  double *pi, *rho;  // [n_seq] sums of policy / reference log-probs
+  int32_t* bad;      // [n_seq] bad ids
+  float* coef;       // [n_seq] d loss / d pi_s
+};
+hipError_t launch_dpo(const rft_tokens& tok, const TokMeta& m, int64_t V, const float* logp,
+                      const float* ref, float beta, float ls, const DpoWs& w, float* grad,
+                      float* seq_logp, rft_dpo_stats* st, hipStream_t s);
 
 // ------------------------------------------------------------ launchers --
 hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, float* adv,

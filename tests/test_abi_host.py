@@ -128,6 +128,22 @@ def test_argument_validation_returns_codes():
     assert L.rft_ppo_clip_step(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake, fake,
                                ctypes.byref(P(entropy_coef=0.01)), fake, None, fake, fake, fake,
                                fake, 0, fake, fake, 1 << 30, s) == R.RFT_E_NULL
+    # SFT / DPO parameters and layout
+    assert L.rft_sft_loss_fwd(ctypes.byref(tk), 100, fake, 7, 0.0, fake, fake, fake, 1 << 30,
+                              s) == R.RFT_E_PARAM
+    assert L.rft_sft_loss_fwd(ctypes.byref(tk), 100, fake, 0, -1.0, fake, fake, fake, 1 << 30,
+                              s) == R.RFT_E_PARAM
+    assert L.rft_sft_loss_fwd(ctypes.byref(tk), 100, fake, 0, 0.0, None, fake, fake, 1 << 30,
+                              s) == R.RFT_E_NULL
+    for beta, ls, code in [(0.0, 0.0, R.RFT_E_PARAM), (float("nan"), 0.0, R.RFT_E_PARAM),
+                           (0.1, -0.1, R.RFT_E_PARAM), (0.1, 0.6, R.RFT_E_PARAM)]:
+        assert L.rft_dpo_loss_fwd(ctypes.byref(tk), 100, fake, fake, beta, ls, fake, None, fake,
+                                  fake, 1 << 30, s) == code
+    assert L.rft_dpo_loss_fwd(ctypes.byref(tk), 100, fake, None, 0.1, 0.0, fake, None, fake,
+                              fake, 1 << 30, s) == R.RFT_E_NULL
+    odd = R.rft_tokens(8, 3, 0x1000, 0x1000, 0x1000)
+    assert L.rft_dpo_loss_fwd(ctypes.byref(odd), 100, fake, fake, 0.1, 0.0, fake, None, fake,
+                              fake, 1 << 30, s) == R.RFT_E_SHAPE
     # logits paths
     assert L.rft_token_logprobs_from_logits(ctypes.byref(tk), fake, 0, fake, fake, fake, None,
                                             None, 0, s) == R.RFT_E_SHAPE
