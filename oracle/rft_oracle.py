@@ -71,6 +71,12 @@ Readings where the paper is silent (it prints no formula):
      when both rollouts have a valid token; the loss is the mean over the P
      counted pairs of -(1 - ls) log sigmoid(u_k) - ls log sigmoid(-u_k) (ls the
      label smoothing of conservative DPO, 0 by default).
+  R14 Advantage variants over explicit groups (rollouts that failed, were
+     skipped or whose reward has not arrived leave their group smaller,
+     Sec. 2.2): rollout i belongs to group id_i (id < 0: left out, advantage
+     0); a group's size G is the number of its rollouts.  Modes: GRPO (R3 on
+     the group); mean-centred r_i - mean; leave-one-out r_i - (mean of the
+     other G - 1 rewards).  Groups of one rollout give 0 in every mode.
 """
 from __future__ import annotations
 
@@ -144,6 +150,37 @@ def group_advantages(rewards, group_size, eps=1e-6):
         mu = grp.sum() / G
         sd = math.sqrt(((grp - mu) ** 2).sum() / (G - 1))
         out[g0:g0 + G] = (grp - mu) / (sd + eps)
+    return out
+
+
+ADV_GRPO, ADV_MEAN_CENTER, ADV_LEAVE_ONE_OUT = 0, 1, 2
+
+
+def group_advantages_ids(rewards, group_id, mode=ADV_GRPO, eps=1e-6):
+    """Advantages over explicit, variable-size groups (reading R14)."""
+    r = _f64(rewards)
+    gid = _int(group_id)
+    out = np.zeros_like(r)
+    for g in sorted(set(int(x) for x in gid if x >= 0)):
+        members = [i for i in range(r.size) if gid[i] == g]
+        G = len(members)
+        if G < 2:
+            continue
+        vals = [r[i] for i in members]
+        mu = sum(vals) / G
+        for i in members:
+            if mode == ADV_GRPO:
+                if all(v == vals[0] for v in vals):
+                    out[i] = 0.0
+                else:
+                    sd = math.sqrt(sum((v - mu) ** 2 for v in vals) / (G - 1))
+                    out[i] = (r[i] - mu) / (sd + eps)
+            elif mode == ADV_MEAN_CENTER:
+                out[i] = r[i] - mu
+            elif mode == ADV_LEAVE_ONE_OUT:
+                out[i] = r[i] - (sum(vals) - r[i]) / (G - 1)
+            else:
+                raise ValueError(mode)
     return out
 
 

@@ -872,3 +872,49 @@ def test_dpo_torch_autograd_and_bad_ids():
     assert loss.item() == pytest.approx(out["loss"], rel=1e-13)
     np.testing.assert_allclose(out["grad_logp"], lp.grad.numpy(), rtol=1e-12, atol=1e-16)
     assert out["reward_acc"] == pytest.approx(float((u[ok] > 0).double().mean()), rel=1e-15)
+
+
+# ------------------------------------------------- advantage variants (R14) --
+def test_golden_advantages_variable_groups():
+    g = GOLD["advantages_variable_groups"]
+    r, gid = np.array(g["rewards"]), np.array(g["group_id"])
+    np.testing.assert_allclose(O.group_advantages_ids(r, gid, O.ADV_MEAN_CENTER),
+                               g["mean_center"], rtol=1e-15, atol=1e-15)
+    np.testing.assert_allclose(O.group_advantages_ids(r, gid, O.ADV_LEAVE_ONE_OUT),
+                               g["leave_one_out"], rtol=1e-15, atol=1e-15)
+    np.testing.assert_allclose(O.group_advantages_ids(r, gid, O.ADV_GRPO, eps=0.0),
+                               g["grpo_eps0"], rtol=1e-14, atol=1e-15)
+
+
+def test_advantages_ids_contiguous_equals_grpo_and_identities():
+    """Contiguous ids reproduce the fixed-size GRPO advantages (a separate
+    implementation); mean-centred values sum to 0 per group; leave-one-out is
+    G / (G - 1) times mean-centred; a permutation of the rollouts permutes the
+    advantages; leaving rollouts out equals computing on the rest alone."""
+    rng = np.random.default_rng(81)
+    G, ng = 8, 12
+    r = rng.random(G * ng)
+    r[16:24] = 0.5                                  # a degenerate group
+    gid = np.repeat(np.arange(ng), G)
+    np.testing.assert_allclose(O.group_advantages_ids(r, gid, O.ADV_GRPO, 1e-6),
+                               O.group_advantages(r, G, 1e-6), rtol=1e-13, atol=1e-15)
+    gid2 = rng.integers(-1, 9, size=r.size)
+    mc = O.group_advantages_ids(r, gid2, O.ADV_MEAN_CENTER)
+    lo = O.group_advantages_ids(r, gid2, O.ADV_LEAVE_ONE_OUT)
+    for g in range(9):
+        idx = np.nonzero(gid2 == g)[0]
+        if idx.size >= 2:
+            assert abs(mc[idx].sum()) < 1e-12
+            np.testing.assert_allclose(lo[idx], idx.size / (idx.size - 1) * mc[idx], rtol=1e-12,
+                                       atol=1e-15)
+        else:
+            assert np.all(mc[idx] == 0) and np.all(lo[idx] == 0)
+    assert np.all(mc[gid2 < 0] == 0)
+    perm = rng.permutation(r.size)
+    for mode in (O.ADV_GRPO, O.ADV_MEAN_CENTER, O.ADV_LEAVE_ONE_OUT):
+        a = O.group_advantages_ids(r, gid2, mode)
+        np.testing.assert_allclose(O.group_advantages_ids(r[perm], gid2[perm], mode), a[perm],
+                                   rtol=1e-13, atol=1e-15)
+        keep = gid2 >= 0
+        np.testing.assert_allclose(O.group_advantages_ids(r[keep], gid2[keep], mode), a[keep],
+                                   rtol=1e-13, atol=1e-15)
