@@ -73,8 +73,9 @@ Readings where the paper is silent (it prints no formula):
      label smoothing of conservative DPO, 0 by default).
   R14 Advantage variants over explicit groups (rollouts that failed, were
      skipped or whose reward has not arrived leave their group smaller,
-     Sec. 2.2): rollout i belongs to group id_i (id < 0: left out, advantage
-     0); a group's size G is the number of its rollouts.  Modes: GRPO (R3 on
+     Sec. 2.2): rollout i belongs to group id_i (an id outside [0, number of
+     groups) leaves it out: advantage 0); a group's size G is the number of
+     its rollouts.  Modes: GRPO (R3 on
      the group); mean-centred r_i - mean; leave-one-out r_i - (mean of the
      other G - 1 rewards).  Groups of one rollout give 0 in every mode.
 """
@@ -156,12 +157,13 @@ def group_advantages(rewards, group_size, eps=1e-6):
 ADV_GRPO, ADV_MEAN_CENTER, ADV_LEAVE_ONE_OUT = 0, 1, 2
 
 
-def group_advantages_ids(rewards, group_id, mode=ADV_GRPO, eps=1e-6):
-    """Advantages over explicit, variable-size groups (reading R14)."""
+def group_advantages_ids(rewards, group_id, mode=ADV_GRPO, eps=1e-6, n_groups=None):
+    """Advantages over explicit, variable-size groups (reading R14); with
+    ``n_groups`` given, ids at or above it also leave their rollout out."""
     r = _f64(rewards)
     gid = _int(group_id)
     out = np.zeros_like(r)
-    for g in sorted(set(int(x) for x in gid if x >= 0)):
+    for g in sorted(set(int(x) for x in gid if x >= 0 and (n_groups is None or x < n_groups))):
         members = [i for i in range(r.size) if gid[i] == g]
         G = len(members)
         if G < 2:

@@ -918,3 +918,9 @@ def test_advantages_ids_contiguous_equals_grpo_and_identities():
         keep = gid2 >= 0
         np.testing.assert_allclose(O.group_advantages_ids(r[keep], gid2[keep], mode), a[keep],
                                    rtol=1e-13, atol=1e-15)
+        # ids at or above the group count leave their rollouts out as well
+        a7 = O.group_advantages_ids(r, gid2, mode, n_groups=7)
+        k7 = gid2 < 7
+        np.testing.assert_allclose(a7[k7], O.group_advantages_ids(r[k7], gid2[k7], mode),
+                                   rtol=1e-13, atol=1e-15)
+        assert np.all(a7[~k7] == 0)
