@@ -163,24 +163,27 @@ def group_advantages_ids(rewards, group_id, mode=ADV_GRPO, eps=1e-6, n_groups=No
     r = _f64(rewards)
     gid = _int(group_id)
     out = np.zeros_like(r)
-    for g in sorted(set(int(x) for x in gid if x >= 0 and (n_groups is None or x < n_groups))):
-        members = [i for i in range(r.size) if gid[i] == g]
+    groups = {}
+    for i in range(r.size):
+        g = int(gid[i])
+        if g >= 0 and (n_groups is None or g < n_groups):
+            groups.setdefault(g, []).append(i)
+    for g, members in groups.items():
         G = len(members)
         if G < 2:
             continue
         vals = [r[i] for i in members]
-        mu = sum(vals) / G
+        total = sum(vals)
+        mu = total / G
+        sd = math.sqrt(sum((v - mu) ** 2 for v in vals) / (G - 1))
+        tied = all(v == vals[0] for v in vals)
         for i in members:
             if mode == ADV_GRPO:
-                if all(v == vals[0] for v in vals):
-                    out[i] = 0.0
-                else:
-                    sd = math.sqrt(sum((v - mu) ** 2 for v in vals) / (G - 1))
-                    out[i] = (r[i] - mu) / (sd + eps)
+                out[i] = 0.0 if tied else (r[i] - mu) / (sd + eps)
             elif mode == ADV_MEAN_CENTER:
                 out[i] = r[i] - mu
             elif mode == ADV_LEAVE_ONE_OUT:
-                out[i] = r[i] - (sum(vals) - r[i]) / (G - 1)
+                out[i] = r[i] - (total - r[i]) / (G - 1)
             else:
                 raise ValueError(mode)
     return out
