@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define RFT_ABI_VERSION 4
+#define RFT_ABI_VERSION 5
 
 typedef enum {
   RFT_OK = 0,
@@ -74,6 +74,13 @@ typedef enum {
                                       weight 1/(S * n_i), S = rollouts with n_i > 0 */
   RFT_AGG_TOKEN_MEAN = 1           /* mean over all valid tokens: weight 1/N          */
 } rft_agg;
+
+/* Advantage estimators over explicit groups (rft_group_advantages_ids). */
+typedef enum {
+  RFT_ADV_GRPO = 0,          /* (r - mean) / (sample std + eps); equal rewards give 0 */
+  RFT_ADV_MEAN_CENTER = 1,   /* r - mean                                              */
+  RFT_ADV_LEAVE_ONE_OUT = 2  /* r - mean of the other rollouts of the group           */
+} rft_adv_mode;
 
 /* Operations, for rft_workspace_bytes(). */
 typedef enum {
@@ -177,6 +184,22 @@ size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t
  * RFT_E_PARAM (eps < 0 or not finite). */
 rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t group_size,
                                 float eps, float* adv, void* stream);
+
+/* Advantages over explicit, variable-size groups (Sec. 2.2: rollouts that
+ * failed, were skipped or wait for a lagged reward leave their group smaller;
+ * Sec. 3.2, Listing 4: advantage_fn grpo).  group_id[i] in [0, n_groups) puts
+ * rollout i in that group; an id outside that range leaves the rollout out
+ * (advantage 0).  G = the number of rollouts of the group; groups with G < 2
+ * give 0.  mode: RFT_ADV_GRPO (as rft_group_advantages, sample std + eps),
+ * RFT_ADV_MEAN_CENTER, RFT_ADV_LEAVE_ONE_OUT (r_i - (sum_g - r_i) / (G - 1)).
+ * Sums in fp64 in index order.  The work grows as n * n_groups (each group
+ * scans the ids), meant for batches of up to about 1e5 rollouts.
+ * rewards, adv [n] f32, group_id [n] int32; adv may not alias rewards.
+ * Errors: RFT_E_NULL, RFT_E_SHAPE (n < 0, n_groups < 0 or > 2^31 - 1),
+ * RFT_E_PARAM (mode unknown, eps < 0 or not finite). */
+rft_status rft_group_advantages_ids(const float* rewards, const int32_t* group_id, int64_t n,
+                                    int64_t n_groups, int32_t mode, float eps, float* adv,
+                                    void* stream);
 
 /* Per-token log-probability of the sampled id, entropy and log-sum-exp of the
  * policy head z_t = weight . hidden_t over the whole vocabulary (Sec. 3.1.1:

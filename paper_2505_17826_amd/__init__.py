@@ -22,6 +22,7 @@ RFT_OK, RFT_E_NULL, RFT_E_SHAPE, RFT_E_DTYPE, RFT_E_PARAM, RFT_E_WORKSPACE, \
     RFT_E_UNSUPPORTED, RFT_E_HIP = range(8)
 RFT_F32, RFT_BF16 = 0, 1
 RFT_AGG_SEQ_MEAN_TOKEN_MEAN, RFT_AGG_TOKEN_MEAN = 0, 1
+RFT_ADV_GRPO, RFT_ADV_MEAN_CENTER, RFT_ADV_LEAVE_ONE_OUT = 0, 1, 2
 (RFT_OP_TOKEN_LOGPROBS, RFT_OP_TOKEN_LOGPROBS_FROM_LOGITS, RFT_OP_PPO_FWD, RFT_OP_PPO_BWD,
  RFT_OP_PPO_BWD_LOGITS, RFT_OP_PPO_FUSED_LOGITS, RFT_OP_PPO_STEP, RFT_OP_SFT_FWD,
  RFT_OP_DPO_FWD) = range(9)
@@ -71,6 +72,8 @@ _SIGS = {
     "rft_workspace_min_bytes": (ctypes.c_size_t, [ctypes.c_int, ctypes.POINTER(rft_tokens), _i64,
                                                   _i64, ctypes.c_int]),
     "rft_group_advantages": (ctypes.c_int, [_p, _i64, ctypes.c_int32, ctypes.c_float, _p, _p]),
+    "rft_group_advantages_ids": (ctypes.c_int, [_p, _p, _i64, _i64, ctypes.c_int32, ctypes.c_float,
+                                                _p, _p]),
     "rft_token_logprobs": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _p, ctypes.c_int, _i64,
                                           _i64, _p, _p, _p, _p, ctypes.c_size_t, _p]),
     "rft_token_logprobs_from_logits": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _i64, _p,
@@ -217,6 +220,15 @@ def rft_group_advantages(rewards, group_size, eps=1e-6, out=None, stream=None):
     n_groups = rewards.numel() // group_size if group_size > 0 else 0
     _check(lib().rft_group_advantages(_ptr(rewards), n_groups, group_size, eps, _ptr(out),
                                       _stream(stream)))
+    return out
+
+
+def rft_group_advantages_ids(rewards, group_id, n_groups, mode=RFT_ADV_GRPO, eps=1e-6, out=None,
+                             stream=None):
+    _need_gpu(rewards, group_id)
+    out = torch.empty_like(rewards) if out is None else out
+    _check(lib().rft_group_advantages_ids(_ptr(rewards), _ptr(group_id), rewards.numel(), n_groups,
+                                          mode, eps, _ptr(out), _stream(stream)))
     return out
 
 

@@ -44,6 +44,92 @@ hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, 
   return hipGetLastError();
 }
 
+// ------------------------------------------- advantages over group ids ----
+// Explicit, variable-size groups: one workgroup per group id scans the ids
+// (members in index order, fp64 sums reduced in a fixed order) and writes the
+// advantages of its members; rollouts whose id is outside [0, n_groups) get 0
+// from k_adv_left_out.  Modes as rft_adv_mode.
+template <typename Tv>
+__device__ Tv block_sum256(Tv v, Tv* sh) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  return sh[0] + sh[1] + sh[2] + sh[3];
+}
+
+__global__ void __launch_bounds__(256) k_adv_left_out(const int32_t* __restrict__ gid, int64_t n,
+                                                      int64_t n_groups, float* __restrict__ adv) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n && (gid[i] < 0 || (int64_t)gid[i] >= n_groups)) adv[i] = 0.f;
+}
+
+__global__ void __launch_bounds__(256) k_adv_groups(const float* __restrict__ r,
+                                                    const int32_t* __restrict__ gid, int64_t n,
+                                                    int mode, float eps, float* __restrict__ adv) {
+  __shared__ double shd[4];
+  __shared__ int shi[4];
+  __shared__ float shf[4];
+  const int g = (int)blockIdx.x;
+  double s = 0.0;
+  int cnt = 0;
+  float mn = INFINITY, mx = -INFINITY;
+  for (int64_t i = threadIdx.x; i < n; i += 256) {
+    if (gid[i] != g) continue;
+    const float v = r[i];
+    s += (double)v;
+    ++cnt;
+    mn = fminf(mn, v);
+    mx = fmaxf(mx, v);
+  }
+  s = block_sum256(s, shd);
+  cnt = block_sum256(cnt, shi);
+  mn = wave_min_f(mn);
+  mx = wave_max_f(mx);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) shf[threadIdx.x >> 6] = mn;
+  __syncthreads();
+  mn = fminf(fminf(shf[0], shf[1]), fminf(shf[2], shf[3]));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) shf[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(shf[0], shf[1]), fmaxf(shf[2], shf[3]));
+  const double G = (double)cnt, mu = cnt > 0 ? s / G : 0.0;
+  double sd = 0.0;
+  if (mode == RFT_ADV_GRPO) {
+    double q = 0.0;
+    for (int64_t i = threadIdx.x; i < n; i += 256) {
+      if (gid[i] != g) continue;
+      const double dv = (double)r[i] - mu;
+      q += dv * dv;
+    }
+    q = block_sum256(q, shd);
+    sd = cnt > 1 ? sqrt(q / (G - 1.0)) : 0.0;
+  }
+  const bool degenerate = cnt < 2 || (mode == RFT_ADV_GRPO && mn == mx);
+  for (int64_t i = threadIdx.x; i < n; i += 256) {
+    if (gid[i] != g) continue;
+    const double v = (double)r[i];
+    double a = 0.0;
+    if (!degenerate) {
+      if (mode == RFT_ADV_GRPO) a = (v - mu) / (sd + (double)eps);
+      else if (mode == RFT_ADV_MEAN_CENTER) a = v - mu;
+      else a = v - (s - v) / (G - 1.0);
+    }
+    adv[i] = (float)a;
+  }
+}
+
+hipError_t launch_group_adv_ids(const float* r, const int32_t* gid, int64_t n, int64_t n_groups,
+                                int mode, float eps, float* adv, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  k_adv_left_out<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(gid, n, n_groups, adv);
+  if (n_groups > 0) k_adv_groups<<<(unsigned)n_groups, 256, 0, s>>>(r, gid, n, mode, eps, adv);
+  return hipGetLastError();
+}
+
 // -------------------------------------------------------- loss reduction ----
 __device__ void block_reduce_partial(LossPartial& p, LossPartial* out) {
   __shared__ LossPartial sh[16];

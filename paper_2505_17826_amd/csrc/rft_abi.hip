@@ -377,6 +377,24 @@ rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t 
   return RFT_OK;
 }
 
+rft_status rft_group_advantages_ids(const float* rewards, const int32_t* group_id, int64_t n,
+                                    int64_t n_groups, int32_t mode, float eps, float* adv,
+                                    void* stream) {
+  const char* fn = "rft_group_advantages_ids";
+  if (n < 0 || n_groups < 0 || n_groups > (int64_t)std::numeric_limits<int32_t>::max())
+    return fail(RFT_E_SHAPE, "%s: n=%lld n_groups=%lld", fn, (long long)n, (long long)n_groups);
+  if (n > 0 && (!rewards || !group_id || !adv))
+    return fail(RFT_E_NULL, "%s: rewards / group_id / adv is NULL", fn);
+  if (mode != RFT_ADV_GRPO && mode != RFT_ADV_MEAN_CENTER && mode != RFT_ADV_LEAVE_ONE_OUT)
+    return fail(RFT_E_PARAM, "%s: mode=%d unknown", fn, mode);
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(RFT_E_PARAM, "%s: eps=%g", fn, (double)eps);
+  if (n > 0 && rewards == adv) return fail(RFT_E_PARAM, "%s: adv may not alias rewards", fn);
+  RFT_HIP(launch_group_adv_ids(rewards, group_id, n, n_groups, mode, eps, adv,
+                               (hipStream_t)stream),
+          fn);
+  return RFT_OK;
+}
+
 rft_status rft_token_logprobs(const rft_tokens* tok, const void* hidden, const void* weight,
                               int dtype, int64_t d, int64_t V, float* logp, float* entropy,
                               float* lse, void* ws, size_t ws_bytes, void* stream) {

@@ -128,6 +128,15 @@ def test_argument_validation_returns_codes():
     assert L.rft_ppo_clip_step(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake, fake,
                                ctypes.byref(P(entropy_coef=0.01)), fake, None, fake, fake, fake,
                                fake, 0, fake, fake, 1 << 30, s) == R.RFT_E_NULL
+    # advantages over group ids
+    for args, code in [((fake, fake, -1, 4, 0, 1e-6, fake), R.RFT_E_SHAPE),
+                       ((fake, fake, 8, -1, 0, 1e-6, fake), R.RFT_E_SHAPE),
+                       ((fake, fake, 8, 1 << 31, 0, 1e-6, fake), R.RFT_E_SHAPE),
+                       ((fake, None, 8, 4, 0, 1e-6, fake), R.RFT_E_NULL),
+                       ((fake, fake, 8, 4, 3, 1e-6, fake), R.RFT_E_PARAM),
+                       ((fake, fake, 8, 4, 0, -1.0, fake), R.RFT_E_PARAM),
+                       ((fake, fake, 8, 4, 0, 1e-6, fake), R.RFT_E_PARAM)]:   # adv aliases rewards
+        assert L.rft_group_advantages_ids(*args, s) == code, args
     # SFT / DPO parameters and layout
     assert L.rft_sft_loss_fwd(ctypes.byref(tk), 100, fake, 7, 0.0, fake, fake, fake, 1 << 30,
                               s) == R.RFT_E_PARAM
