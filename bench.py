@@ -67,9 +67,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
-    ap.add_argument("--ws-gb", type=float, default=0.0,
-                    help="workspace of the fused step in GB (default: the library's "
-                         "recommended size); a larger workspace means fewer row chunks")
+    ap.add_argument("--ws-gb", type=float, default=96.0,
+                    help="workspace of the fused step in GB (default 96, a third of the "
+                         "MI355X's 288 GB of HBM; 0 = the library's recommended size); a "
+                         "larger workspace means fewer, larger row chunks")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GB",
                     help="only run a plain device copy of GB gigabytes (the known-size kernel "
                          "that scales the HBM byte counters) and exit")
@@ -147,8 +148,9 @@ def main():
         copy_probe(args.copy_probe)
         return
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the path would shard by whole GRPO groups (see the design notes)", file=sys.stderr)
+        print(f"bench.py: the library runs on one GPU only (asked for --gpus {args.gpus}); "
+              "multi-GPU runs (sharding by whole GRPO groups) are not implemented",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -213,8 +215,11 @@ def main():
         dW = torch.empty((V, d), **f32)
         ws_fwd = torch.empty(R.workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, tok, d, V, dt),
                              dtype=torch.uint8, device=dev)
-        ws_step_bytes = (int(args.ws_gb * 1e9) if args.ws_gb > 0
-                         else R.workspace_bytes(R.RFT_OP_PPO_STEP, tok, d, V, dt))
+        # the recommended size holds chunks of up to 65536 rows; a bigger batch
+        # gets the --ws-gb workspace (fewer chunks)
+        ws_step_bytes = R.workspace_bytes(R.RFT_OP_PPO_STEP, tok, d, V, dt)
+        if args.ws_gb > 0 and T > 65536:
+            ws_step_bytes = max(ws_step_bytes, int(args.ws_gb * 1e9))
         ws_step = torch.empty(ws_step_bytes, dtype=torch.uint8, device=dev)
         # rollout-side log-probs for the old / reference policies (setup, untimed)
         R.rft_token_logprobs(tok, b.H, b.W, logp=logp, entropy=ent, lse=lse, ws=ws_fwd)
