@@ -67,10 +67,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
-    ap.add_argument("--ws-gb", type=float, default=96.0,
-                    help="workspace of the fused step in GB (default 96, a third of the "
-                         "MI355X's 288 GB of HBM; 0 = the library's recommended size); a "
-                         "larger workspace means fewer, larger row chunks")
+    ap.add_argument("--ws-gb", type=float, default=0.0,
+                    help="workspace of the fused step in GB (default 0: the library's "
+                         "recommended size, chunks of up to 131072 rows); a larger workspace "
+                         "means fewer, larger row chunks")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GB",
                     help="only run a plain device copy of GB gigabytes (the known-size kernel "
                          "that scales the HBM byte counters) and exit")
@@ -215,10 +215,8 @@ def main():
         dW = torch.empty((V, d), **f32)
         ws_fwd = torch.empty(R.workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, tok, d, V, dt),
                              dtype=torch.uint8, device=dev)
-        # the recommended size holds chunks of up to 65536 rows; a bigger batch
-        # gets the --ws-gb workspace (fewer chunks)
         ws_step_bytes = R.workspace_bytes(R.RFT_OP_PPO_STEP, tok, d, V, dt)
-        if args.ws_gb > 0 and T > 65536:
+        if args.ws_gb > 0:
             ws_step_bytes = max(ws_step_bytes, int(args.ws_gb * 1e9))
         ws_step = torch.empty(ws_step_bytes, dtype=torch.uint8, device=dev)
         # rollout-side log-probs for the old / reference policies (setup, untimed)

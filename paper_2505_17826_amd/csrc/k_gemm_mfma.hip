@@ -21,7 +21,8 @@
 //              tile, rounded to fp16, row-major [rows, Vpad] (the backward
 //              then forms dZ from it instead of recomputing z).
 //   EPI_DZ     backward recompute: dZ = c (onehot(y) - p) + e p (z - mu) in bf16,
-//              written row-major [rows, Vpad] and transposed [Vpad, rows].
+//              written row-major [rows, Vpad] (the weight-gradient GEMM reads
+//              it as its K-by-M operand, see the TR operand layout).
 //   EPI_STORE  fp32 result, optionally scattered to rows through a map and
 //              optionally added to the existing values.
 #include "rft_internal.h"
@@ -71,7 +72,7 @@ struct Args {
   float* pm; float* ps; float* pu; int64_t ldp; float* zy;  // EPI_STATS: partials at p_off + m,
   int64_t p_off;                                            //   zy at rows_off + m
   uint16_t* y; int64_t ldy;                                 // EPI_STATS_Y: fp16 z - tile max
-  uint16_t* dz; int64_t ldz; uint16_t* dzt; int64_t ldzt; int64_t Vvalid;  // EPI_DZ
+  uint16_t* dz; int64_t ldz; int64_t Vvalid;                  // EPI_DZ
   float* C; int64_t ldc; int accumulate; int c_scatter;  // EPI_STORE
 };
 
@@ -124,6 +125,53 @@ __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_b
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES + p * 1024), 16,
                                              vb + (uint32_t)p * lg.sB, 0, 0, 0);
   }
+}
+
+// Operands stored with M (N) contiguous and K across rows ("TR": the weight
+// gradient reads dZ [rows, Vpad] and the compacted hidden rows [rows, d]
+// as they are, with no transposed copies).  A stage holds BK = 64 K-rows of
+// 256 M-values (512 B per row) for A, then the same for B; 16-byte chunk c of
+// K-row k sits at chunk c ^ (4 (k & 3)), so that the transposing fragment
+// reads (ds_read_b64_tr_b16: a 16-lane group reads 4 K-rows x 16 M-values and
+// each lane receives 4 consecutive K of one M) touch 16 distinct 16-byte bank
+// groups per half wave.  Loader wave w fills K-rows [16w, 16w + 16) of A and
+// B with 8 + 8 instructions of two rows each; lane l writes LDS chunk l of
+// its instruction (row l >> 5 of the pair, physical chunk l & 31), so it
+// loads logical chunk (l & 31) ^ 4 ((2 (p & 1) + (l >> 5)) & 3) of instruction
+// p.  The buffer descriptors are rebased on every K step (32-bit offsets) and
+// cover only the valid K-rows: rows past the count read as 0.
+struct LoadGeomTr {
+  uint32_t vA[2], vB[2];  // per-lane byte offsets for even / odd p, K-row 0 of the step
+  uint32_t sA, sB;        // bytes per K-row
+};
+
+__device__ __forceinline__ void load_stage_tr(const uint16_t* A, int64_t lda, const uint16_t* B,
+                                              int64_t ldb, int k0, int Kv, char* dst,
+                                              const LoadGeomTr& lg) {
+  const int rows = Kv - k0 < BK ? (Kv - k0 > 0 ? Kv - k0 : 0) : BK;
+  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A + (int64_t)k0 * lda, (int64_t)rows * lda * 2);
+  const __amdgpu_buffer_rsrc_t rB = make_rsrc(B + (int64_t)k0 * ldb, (int64_t)rows * ldb * 2);
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_ptr)(dst + p * 1024), 16,
+                                             lg.vA[p & 1] + (uint32_t)p * 2u * lg.sA, 0, 0, 0);
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES + p * 1024), 16,
+                                             lg.vB[p & 1] + (uint32_t)p * 2u * lg.sB, 0, 0, 0);
+}
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16* lds_v4i16;
+
+// MFMA operand fragment (32 rows of M or N, 16 K) from a TR tile: two
+// transposing reads of 4 K each; off = the lane's byte offset for the first.
+__device__ __forceinline__ bf16x8 frag_tr(const char* tile, uint32_t off) {
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(tile + off));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(tile + off + 4 * 512));
+  const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3],
+                                                       hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
 }
 
 // Tile order.  Workgroup b runs on XCD x = b % 8 as the j = b / 8-th
@@ -194,7 +242,7 @@ __device__ __forceinline__ uint32_t f16_bits(float f) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
-template <int EPI>
+template <int EPI, bool TR = false>
 __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   constexpr bool kStats = EPI == EPI_STATS || EPI == EPI_STATS_Y;
   __shared__ __attribute__((aligned(16))) char lds[LDS_TOTAL];
@@ -202,12 +250,15 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid >> 1, wn = wid & 1;  // 4 x 2 waves, wave tile 64 x 128
 
-  int M = g.M, K = g.K;
+  int M = g.M, K = g.K, Kv = g.K;  // Kv: valid K (rows of the TR operands)
   if (g.cnt) {
     int64_t c = (int64_t)g.cnt[0] - g.cnt_off;
     c = c < 0 ? 0 : (c > g.cnt_cap ? g.cnt_cap : c);
     if (g.m_from_cnt) M = (int)c;
-    if (g.k_from_cnt) K = (int)((c + BK - 1) / BK * BK);
+    if (g.k_from_cnt) {
+      K = (int)((c + BK - 1) / BK * BK);
+      Kv = (int)c;
+    }
   }
   const int N = g.N;
   const int NB = g.NB > 0 ? g.NB : N;
@@ -233,6 +284,18 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     }
     lg.sA = (uint32_t)(8 * g.lda * 2);
     lg.sB = (uint32_t)(8 * g.ldb * 2);
+  }
+  LoadGeomTr lt;
+  if (TR) {
+    const int r = (wid % NLOAD) * 16 + (lane >> 5);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int c = (lane & 31) ^ (4 * ((2 * q + (lane >> 5)) & 3));
+      lt.vA[q] = (uint32_t)(r * g.lda * 2 + (int64_t)mt * BM * 2 + c * 16);
+      lt.vB[q] = (uint32_t)(r * g.ldb * 2 + (int64_t)nt * BN * 2 + c * 16);
+    }
+    lt.sA = (uint32_t)(g.lda * 2);
+    lt.sB = (uint32_t)(g.ldb * 2);
   }
   // per-lane MFMA operand offsets (row = base + (lane&31), chunk = ks*2 + (lane>>5))
   const int fr = lane & 31, fh = lane >> 5;
@@ -292,23 +355,47 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    char* const ldsw = lds + (wid % NLOAD) * (256 / NLOAD) * 128;
-    if (nk > 0 && loader)
-      load_stage(rA, rB, ldsw, 0, K, lg);
+    char* const ldsw = lds + (wid % NLOAD) * (TR ? 16 * 512 : (256 / NLOAD) * 128);
+    // TR fragment offsets: lane (group half gi, K-half kh, j = K-row in 4, a = M quad)
+    uint32_t oA[2], oB[4];
+    if (TR) {
+      const int gi = (lane >> 4) & 1, kh = lane >> 5, j = (lane >> 2) & 3, aq = lane & 3;
+      const uint32_t kb = (uint32_t)(kh * 8 + j) * 512u + (uint32_t)((aq & 1) * 8);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        oA[i] = kb + ((((wm * 64 + i * 32 + gi * 16 + 4 * aq) >> 3) ^ (4 * j)) << 4);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        oB[jj] = kb + ((((wn * 128 + jj * 32 + gi * 16 + 4 * aq) >> 3) ^ (4 * j)) << 4);
+    }
+    if (nk > 0 && loader) {
+      if (TR) load_stage_tr(g.A, g.lda, g.B, g.ldb, 0, Kv, ldsw, lt);
+      else load_stage(rA, rB, ldsw, 0, K, lg);
+    }
     __syncthreads();  // first stage and the per-row parameters are visible to every wave
     for (int kt = 0; kt < nk; ++kt) {
-      if (kt + 1 < nk && loader)
-        load_stage(rA, rB, ldsw + ((kt + 1) & 1) * STAGE, (kt + 1) * BK, K, lg);
+      if (kt + 1 < nk && loader) {
+        if (TR) load_stage_tr(g.A, g.lda, g.B, g.ldb, (kt + 1) * BK, Kv,
+                              ldsw + ((kt + 1) & 1) * STAGE, lt);
+        else load_stage(rA, rB, ldsw + ((kt + 1) & 1) * STAGE, (kt + 1) * BK, K, lg);
+      }
       const char* As = lds + (kt & 1) * STAGE;
       const char* Bs = As + A_BYTES;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int ch = ((ks * 2 + fh) ^ ((fr >> 1) & 7)) << 4;
         bf16x8 a[2], b[4];
+        if (TR) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(As + (wm * 64 + i * 32 + fr) * 128 + ch);
+          for (int i = 0; i < 2; ++i) a[i] = frag_tr(As, oA[i] + ks * 16 * 512);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Bs + (wn * 128 + j * 32 + fr) * 128 + ch);
+          for (int j = 0; j < 4; ++j) b[j] = frag_tr(Bs, oB[j] + ks * 16 * 512);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(As + (wm * 64 + i * 32 + fr) * 128 + ch);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Bs + (wn * 128 + j * 32 + fr) * 128 + ch);
+        }
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -476,7 +563,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
           }
         }
       }
-      // Stage each layout through LDS and write it with 16-byte stores that
+      // Stage the tile through LDS and write it with 16-byte stores that
       // cover whole lines: a wave writes two 512-byte rows per instruction.
       char* const st = lds;
       __syncthreads();  // every wave is done with the stages and the row parameters
@@ -492,18 +579,6 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
                        hv[i][j][e4]);
       __syncthreads();
       stage_copy_out(st, g.dz + (int64_t)m0 * g.ldz + n0, g.ldz, tid);
-      __syncthreads();
-      // dZ^T [Vpad, rows]: element (col, row) at byte col * pitch + row * 2
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4)
-            *(uint2*)(st + (wn * 128 + j * 32 + fr) * STG_PITCH +
-                      (wm * 64 + i * 32 + e4 * 8 + fh * 4) * 2) = hv[i][j][e4];
-      __syncthreads();
-      stage_copy_out(st, g.dzt + (int64_t)n0 * g.ldzt + m0, g.ldzt, tid);
     } else {  // EPI_STORE
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -573,11 +648,11 @@ hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, in
 }
 
 // Backward recompute of one chunk of compacted rows [c0, c0 + Tc): dZ (bf16)
-// into dz [Tc, ldz] and dzt [Vpad, Tc].
+// into dz [Tc, ldz].
 hipError_t mfma_dz(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
                    const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
-                   int64_t Tc, uint16_t* dz, uint16_t* dzt, hipStream_t s) {
+                   int64_t Tc, uint16_t* dz, hipStream_t s) {
   mf::Args a = {};
   a.A = Hc + c0 * d; a.lda = d;
   a.B = W; a.ldb = d;
@@ -585,10 +660,28 @@ hipError_t mfma_dz(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V, 
   a.cnt = cnt; a.cnt_off = c0; a.cnt_cap = Tc; a.m_from_cnt = 1;
   a.rows = rows; a.rows_off = c0; a.ids = ids; a.lse = lse; a.cgrad = cgrad;
   a.egrad = egrad; a.ent = ent;
-  a.dz = dz; a.ldz = Vpad; a.dzt = dzt; a.ldzt = Tc; a.Vvalid = V;
+  a.dz = dz; a.ldz = Vpad; a.Vvalid = V;
   a.NB = (int)V;  // W has V rows; columns V..Vpad-1 of dZ are written as 0
-  // dz rows are indexed by the chunk-local m (m0 + row), dzt columns likewise
+  // dz rows are indexed by the chunk-local m (m0 + row)
   mf::k_gemm<mf::EPI_DZ><<<grid_for(Tc, Vpad), mf::NT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+// C[M, N] (+)= A^T . B with A [K, lda] (M contiguous) and B [K, ldb] (N
+// contiguous), fp32 output; K (the valid rows of A and B) from the device
+// counter.  Rows of A and B past the count read as 0.
+hipError_t mfma_gemm_store_tr(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
+                              int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
+                              int64_t cnt_cap, float* C, int64_t ldc, int accumulate,
+                              hipStream_t s) {
+  mf::Args a = {};
+  a.A = A; a.lda = lda; a.B = B; a.ldb = ldb;
+  a.M = (int)M; a.N = (int)N; a.K = (int)K;
+  a.cnt = cnt; a.cnt_off = cnt_off; a.cnt_cap = cnt_cap; a.m_from_cnt = 0;
+  a.k_from_cnt = cnt != nullptr ? 1 : 0;
+  a.C = C; a.ldc = ldc; a.rows = nullptr; a.rows_off = 0; a.c_scatter = 0;
+  a.accumulate = accumulate;
+  mf::k_gemm<mf::EPI_STORE, true><<<grid_for(M, N), mf::NT, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -1,5 +1,5 @@
 // fp32 path of the policy head (hidden/weight given in fp32) and the small
-// layout kernels (hidden-row compaction, weight and hidden transposes,
+// layout kernels (hidden-row compaction, weight transpose,
 // masked-row zero fill).
 //
 // The fp32 GEMM is a plain SIMT tile (64x64, K step 16, 4x4 outputs per
@@ -261,30 +261,6 @@ __global__ void __launch_bounds__(256) k_gather_rows16(const uint16_t* __restric
   }
 }
 
-// Ht[d, ldt] = Hc[c0 + t, :]^T for t < count - c0 (device), zero for the
-// remaining columns up to the next multiple of 64 (the K range the weight
-// gradient GEMM reads).
-__global__ void __launch_bounds__(256) k_transpose_hc(const uint16_t* __restrict__ Hc, int64_t d,
-                                                      const int32_t* __restrict__ cnt, int64_t c0,
-                                                      int64_t Tc, uint16_t* __restrict__ Ht,
-                                                      int64_t ldt) {
-  __shared__ uint16_t tile[64][65];
-  int64_t n = (int64_t)cnt[0] - c0;
-  n = n < 0 ? 0 : (n > Tc ? Tc : n);
-  int64_t t0 = (int64_t)blockIdx.x * 64, k0 = (int64_t)blockIdx.y * 64;
-  if (t0 >= (n + 63) / 64 * 64) return;
-  int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int r = ty; r < 64; r += 4) {
-    int64_t t = t0 + r, k = k0 + tx;
-    tile[r][tx] = (t < n && k < d) ? Hc[(c0 + t) * d + k] : (uint16_t)0;
-  }
-  __syncthreads();
-  for (int r = ty; r < 64; r += 4) {
-    int64_t k = k0 + r, t = t0 + tx;
-    if (k < d && t < ldt) Ht[k * ldt + t] = tile[tx][r];
-  }
-}
-
 // Zero the rows of out[T, width] whose mask is 0.
 __global__ void __launch_bounds__(256) k_zero_masked_rows(const uint8_t* __restrict__ mask,
                                                           int64_t T, int64_t width,
@@ -318,13 +294,6 @@ hipError_t launch_transpose_w(const uint16_t* W, int64_t V, int64_t d, uint16_t*
 hipError_t launch_gather_rows16(const uint16_t* H, int64_t d, const int32_t* rows,
                                 const int32_t* cnt, int64_t cap, uint16_t* Hc, hipStream_t s) {
   if (cap > 0) k_gather_rows16<<<(unsigned)(cap < 16384 ? cap : 16384), 256, 0, s>>>(H, d, rows, cnt, cap, Hc);
-  return hipGetLastError();
-}
-
-hipError_t launch_transpose_hc(const uint16_t* Hc, int64_t d, const int32_t* cnt, int64_t c0,
-                               int64_t Tc, uint16_t* Ht, int64_t ldt, hipStream_t s) {
-  dim3 grid((unsigned)((ldt + 63) / 64), (unsigned)((d + 63) / 64));
-  k_transpose_hc<<<grid, 256, 0, s>>>(Hc, d, cnt, c0, Tc, Ht, ldt);
   return hipGetLastError();
 }
 

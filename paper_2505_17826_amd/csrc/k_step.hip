@@ -8,8 +8,8 @@
 //                 mu_t = lse_t - H_t of the row;
 //   k_dz_from_y   dZ = c_t (onehot(y_t) - p) + e_t p (z - mu_t) from the fp16
 //                 y = z - (row maximum over the 256-column tile) that the
-//                 forward GEMM stored, written in place as bf16 [Tc, Vpad] and
-//                 transposed [Vpad, Tc] for the weight-gradient GEMM.
+//                 forward GEMM stored, written in place as bf16 [Tc, Vpad]
+//                 (both backward GEMMs read this one layout).
 // The arithmetic of k_step_rows is that of k_merge_rows and k_loss_fwd (same
 // merge order, same per-token formula), so the step and the separate calls
 // give the same log-probs and gradients bit for bit.
@@ -61,23 +61,19 @@ __global__ void __launch_bounds__(256) k_step_rows(
 // One 512-thread workgroup per 256 x 256 tile of the chunk.  Thread tid owns
 // the 8 x 8 blocks (row block rb, column block cb) with cb = tid % 32 and
 // rb = tid / 32 and tid / 32 + 16: it reads eight 16-byte row pieces (a wave
-// reads two 512-byte rows per instruction), writes dZ back in place, and
-// writes each of its eight columns (eight rows = 16 bytes) into the transposed
-// LDS tile, rows of 512 bytes whose 16-byte chunk k sits at k ^ ((row/8) % 16)
-// (conflict-free 16-byte writes and reads).  Tiles wholly past the chunk's
-// count are skipped: the weight-gradient GEMM reads dZ^T only up to the count
-// rounded to 64, which the tile holding the count covers with zeros.
+// reads two 512-byte rows per instruction) and writes dZ back in place.
+// Tiles wholly past the chunk's count are skipped (the backward GEMMs read
+// rows only up to the count).
 constexpr int kDzT = 512;
 
 __device__ __forceinline__ uint32_t bf16_bits(float f) { return (uint32_t)f32_to_bf16(f); }
 
 __global__ void __launch_bounds__(kDzT) k_dz_from_y(
-    uint16_t* __restrict__ yz, int64_t Vpad, uint16_t* __restrict__ dzt, int64_t Tc, int64_t V,
+    uint16_t* __restrict__ yz, int64_t Vpad, int64_t Tc, int64_t V,
     const int32_t* __restrict__ rows, const int32_t* __restrict__ ids,
     const int32_t* __restrict__ meta, int64_t c0, const float* __restrict__ pm,
     const float* __restrict__ lse, const float* __restrict__ grad, const float* __restrict__ ce,
     const float* __restrict__ cmu, int ntc) {
-  __shared__ __attribute__((aligned(16))) char st[256 * 512];
   __shared__ float rL[256], rC[256], rM[256], rE[256], rD[256];
   __shared__ int rY[256];
   const int tid = threadIdx.x;
@@ -118,8 +114,6 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
     uint4 in[8];
 #pragma unroll
     for (int r = 0; r < 8; ++r) in[r] = *(const uint4*)(src + r * Vpad);
-    uint32_t out[8][4];  // [row][column pair], bf16 pairs
-    uint16_t colv[8][8];  // [column][row], bf16
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
       const int rl = rb * 8 + r;
@@ -127,42 +121,25 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
       const int Yk = rY[rl];
       const bool rv = r0 + rl < count;
       const uint32_t w[4] = {in[r].x, in[r].y, in[r].z, in[r].w};
+      uint32_t o[4];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int64_t col = n0 + cb * 8 + q;
-        const uint16_t hb = (uint16_t)(w[q >> 1] >> ((q & 1) * 16));
-        const float yv = (float)__builtin_bit_cast(_Float16, hb);
-        const float p = exp2f(fmaf(yv, kLog2e, Mk - Lk));
-        float d = dlogit(Ck, Ek, -Dk, p, yv, col == (int64_t)Yk);
-        d = (rv && col < V) ? d : 0.f;
-        colv[q][r] = (uint16_t)bf16_bits(d);
+      for (int q2 = 0; q2 < 4; ++q2) {
+        uint32_t pair = 0;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int q = 2 * q2 + hh;
+          const int64_t col = n0 + cb * 8 + q;
+          const uint16_t hb = (uint16_t)(w[q2] >> (hh * 16));
+          const float yv = (float)__builtin_bit_cast(_Float16, hb);
+          const float p = exp2f(fmaf(yv, kLog2e, Mk - Lk));
+          float d = dlogit(Ck, Ek, -Dk, p, yv, col == (int64_t)Yk);
+          d = (rv && col < V) ? d : 0.f;
+          pair |= bf16_bits(d) << (hh * 16);
+        }
+        o[q2] = pair;
       }
-#pragma unroll
-      for (int q2 = 0; q2 < 4; ++q2)
-        out[r][q2] = (uint32_t)colv[2 * q2][r] | ((uint32_t)colv[2 * q2 + 1][r] << 16);
+      *(uint4*)(src + r * Vpad) = make_uint4(o[0], o[1], o[2], o[3]);
     }
-#pragma unroll
-    for (int r = 0; r < 8; ++r)
-      *(uint4*)(src + r * Vpad) = make_uint4(out[r][0], out[r][1], out[r][2], out[r][3]);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int row = cb * 8 + q;  // column of dZ = row of dZ^T
-      const int phys = rb ^ (cb & 15);
-      uint4 v;
-      v.x = (uint32_t)colv[q][0] | ((uint32_t)colv[q][1] << 16);
-      v.y = (uint32_t)colv[q][2] | ((uint32_t)colv[q][3] << 16);
-      v.z = (uint32_t)colv[q][4] | ((uint32_t)colv[q][5] << 16);
-      v.w = (uint32_t)colv[q][6] | ((uint32_t)colv[q][7] << 16);
-      *(uint4*)(st + row * 512 + phys * 16) = v;
-    }
-  }
-  __syncthreads();
-  // dZ^T rows n0 .. n0 + 255, columns r0 .. r0 + 255
-#pragma unroll 4
-  for (int it = 0; it < 16; ++it) {
-    const int c = it * kDzT + tid, row = c >> 5, k = c & 31;
-    const uint4 v = *(const uint4*)(st + row * 512 + ((k ^ ((row >> 3) & 15)) * 16));
-    *(uint4*)(dzt + (n0 + row) * Tc + r0 + k * 8) = v;
   }
 }
 
@@ -177,14 +154,14 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
   return hipGetLastError();
 }
 
-hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, uint16_t* dzt, int64_t Tc, int64_t V,
+hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
                             const int32_t* rows, const int32_t* ids, const int32_t* meta,
                             int64_t c0, const float* pm, const float* lse, const float* grad,
                             const float* ce, const float* cmu, hipStream_t s) {
   const int ntc = (int)(Vpad / 256);
   const int64_t nb = (Tc / 256) * ntc;
-  k_dz_from_y<<<(unsigned)nb, kDzT, 0, s>>>(yz, Vpad, dzt, Tc, V, rows, ids, meta, c0, pm, lse,
-                                            grad, ce, cmu, ntc);
+  k_dz_from_y<<<(unsigned)nb, kDzT, 0, s>>>(yz, Vpad, Tc, V, rows, ids, meta, c0, pm, lse, grad,
+                                            ce, cmu, ntc);
   return hipGetLastError();
 }
 

@@ -184,14 +184,14 @@ DpoCarve carve_dpo(void* base, const rft_tokens& tok) {
 
 struct BwdWs {
   TokMeta m;
-  uint16_t *hc, *wt, *dz, *dzt, *ht;  // bf16 path
+  uint16_t *hc, *wt, *dz;  // bf16 path
   float* dz32;                   // fp32 path
   int64_t Tc, Vpad;
   size_t bytes;
 };
 constexpr int64_t kBf16Align = 256;   // row chunk / vocabulary padding of the bf16 path
 constexpr int64_t kF32Align = 64;
-constexpr int64_t kRecommendTc = 65536;
+constexpr int64_t kRecommendTc = 131072;
 
 BwdWs carve_bwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dtype, int64_t Tc) {
   Carver c(base);
@@ -203,8 +203,6 @@ BwdWs carve_bwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dty
     w.hc = c.take<uint16_t>((size_t)(tok.T > 0 ? tok.T : 1) * d);
     w.wt = c.take<uint16_t>((size_t)d * w.Vpad);
     w.dz = c.take<uint16_t>((size_t)Tc * w.Vpad);
-    w.dzt = c.take<uint16_t>((size_t)w.Vpad * Tc);
-    w.ht = c.take<uint16_t>((size_t)d * Tc);
   } else {
     w.Vpad = round_up(V, kF32Align);
     w.dz32 = c.take<float>((size_t)Tc * w.Vpad);
@@ -236,10 +234,10 @@ int64_t bwd_tc_for(const rft_tokens& tok, int64_t d, int64_t V, int dtype, size_
 
 // Fused step (bf16): compacted hidden rows, transposed weight, per-chunk
 // log-sum-exp partials, the sampled logits, the loss partials and the chunk
-// buffers (fp16 y, then bf16 dZ, in dz).
+// buffer (fp16 y, then bf16 dZ, in dz).
 struct StepWs {
   TokMeta m;
-  uint16_t *hc, *wt, *dz, *dzt, *ht;
+  uint16_t *hc, *wt, *dz;
   float *pm, *ps, *pu, *zy;
   float *ce, *cmu;  // per chunk row: entropy-bonus coefficient and softmax mean
   LossPartial* parts;
@@ -265,8 +263,6 @@ StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64
   w.cmu = c.take<float>((size_t)Tc);
   w.parts = c.take<LossPartial>((size_t)((T1 + 255) / 256));
   w.dz = c.take<uint16_t>((size_t)Tc * w.Vpad);
-  w.dzt = c.take<uint16_t>((size_t)w.Vpad * Tc);
-  w.ht = c.take<uint16_t>((size_t)d * Tc);
   w.bytes = c.bytes();
   return w;
 }
@@ -508,16 +504,15 @@ rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, cons
     for (int64_t ci = 0; ci < nchunks; ++ci) {
       int64_t c0 = ci * Tc;
       RFT_HIP(mfma_dz(w.hc, d, W, V, w.Vpad, w.m.rows, tok->token_ids, lse, grad_logp,
-                      grad_entropy, entropy, cnt, c0, Tc, w.dz, w.dzt, s),
+                      grad_entropy, entropy, cnt, c0, Tc, w.dz, s),
               fn);
       // dH rows of this chunk: dZ [count, Vpad] . Wt[d, Vpad]^T, scattered to token rows
       RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
                               d_hidden, d, w.m.rows, c0, 0, s),
               fn);
-      RFT_HIP(launch_transpose_hc(w.hc, d, cnt, c0, Tc, w.ht, Tc, s), fn);
-      // dW += dZt [V, count] . Ht[d, count]^T
-      RFT_HIP(mfma_gemm_store(w.dzt, Tc, w.ht, Tc, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight, d,
-                              nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s),
+      // dW += dZ^T . Hc over the chunk's rows (both read as stored: K = rows)
+      RFT_HIP(mfma_gemm_store_tr(w.dz, w.Vpad, w.hc + c0 * d, d, V, d, Tc, cnt, c0, Tc, d_weight,
+                                 d, (ci > 0 || accumulate_dw) ? 1 : 0, s),
               fn);
     }
     if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);
@@ -662,15 +657,14 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
                              old_logp, ref, adv, c, logp, entropy, lse, grad_logp,
                              bonus ? w.ce : nullptr, w.cmu, s),
             fn);
-    RFT_HIP(launch_dz_from_y(w.dz, w.Vpad, w.dzt, Tc, V, w.m.rows, tok->token_ids, cnt, c0, w.pm,
-                             lse, grad_logp, bonus ? w.ce : nullptr, w.cmu, s),
+    RFT_HIP(launch_dz_from_y(w.dz, w.Vpad, Tc, V, w.m.rows, tok->token_ids, cnt, c0, w.pm, lse,
+                             grad_logp, bonus ? w.ce : nullptr, w.cmu, s),
             fn);
     RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
                             d_hidden, d, w.m.rows, c0, 0, s),
             fn);
-    RFT_HIP(launch_transpose_hc(w.hc, d, cnt, c0, Tc, w.ht, Tc, s), fn);
-    RFT_HIP(mfma_gemm_store(w.dzt, Tc, w.ht, Tc, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight, d,
-                            nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s),
+    RFT_HIP(mfma_gemm_store_tr(w.dz, w.Vpad, w.hc + c0 * d, d, V, d, Tc, cnt, c0, Tc, d_weight, d,
+                               (ci > 0 || accumulate_dw) ? 1 : 0, s),
             fn);
   }
   if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);

@@ -273,14 +273,18 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
                             int ntiles, const float* zy, const float* old, const float* ref,
                             const float* adv, const LossConst& c, float* logp, float* ent,
                             float* lse, float* grad, float* ce, float* cmu, hipStream_t s);
-hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, uint16_t* dzt, int64_t Tc, int64_t V,
+hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
                             const int32_t* rows, const int32_t* ids, const int32_t* meta,
                             int64_t c0, const float* pm, const float* lse, const float* grad,
                             const float* ce, const float* cmu, hipStream_t s);
 hipError_t mfma_dz(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
                    const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
-                   int64_t Tc, uint16_t* dz, uint16_t* dzt, hipStream_t s);
+                   int64_t Tc, uint16_t* dz, hipStream_t s);
+hipError_t mfma_gemm_store_tr(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
+                              int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
+                              int64_t cnt_cap, float* C, int64_t ldc, int accumulate,
+                              hipStream_t s);
 hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
                            int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
                            int64_t cnt_cap, int m_from_cnt, int k_from_cnt, float* C, int64_t ldc,
@@ -301,8 +305,6 @@ hipError_t launch_transpose_w(const uint16_t* W, int64_t V, int64_t d, uint16_t*
                               hipStream_t s);
 hipError_t launch_gather_rows16(const uint16_t* H, int64_t d, const int32_t* rows,
                                 const int32_t* cnt, int64_t cap, uint16_t* Hc, hipStream_t s);
-hipError_t launch_transpose_hc(const uint16_t* Hc, int64_t d, const int32_t* cnt, int64_t c0,
-                               int64_t Tc, uint16_t* Ht, int64_t ldt, hipStream_t s);
 hipError_t launch_fill_zero(float* out, int64_t n, hipStream_t s);
 hipError_t launch_zero_masked_rows(const uint8_t* mask, int64_t T, int64_t width, float* out,
                                    hipStream_t s);
