@@ -32,16 +32,16 @@ WORKLOADS = {"tiny": 0, "1.5b": 1, "7b": 2, "longcot": 3, "lossonly": 4}
 # sources they were taken with: a changed source reports null.
 TRAFFIC = {
     # forward GEMM alone (k_gemm<EPI_STATS>, one launch over all valid rows)
-    "7b": {"sources": {"k_gemm_mfma.hip": "33e83883c1b77632", "rft_internal.h": "d4afb7b9d53163d9"},
-           "bytes": 140098969.9 * 1024 * 2.0 + 1174403.5 * 1024 * 1.0},
-    # every kernel of one rft_ppo_clip_step call (61 dispatches)
-    "step_7b": {"sources": {"k_gemm_mfma.hip": "33e83883c1b77632", "k_step.hip": "27a57f79590796cd",
-                            "k_simt.hip": "39b59b05fec7c4a9", "k_adv_loss.hip": "89c106eddf61614c",
-                            "k_tokens.hip": "e51f94fd7c00a519", "rft_internal.h": "d4afb7b9d53163d9",
-                            "rft_abi.hip": "211fd54856f9c75a"},
-                "bytes": 478981373.625 * 1024 * 2.0 + 170902337.53125 * 1024 * 1.0},
-    "lossonly": {"sources": {"k_logits.hip": "4aa7d762e0d14af6", "rft_internal.h": "d4afb7b9d53163d9"},
-                 "bytes": 8759344.9 * 1024 * 2.0 + 19461397.0 * 1024 * 1.0},
+    "7b": {"sources": {"k_gemm_mfma.hip": "a4594bfb92840375", "rft_internal.h": "a9912954a57ce531"},
+           "bytes": 140472034.453125 * 1024 * 2.0 + 1174403.5703125 * 1024 * 1.0},
+    # every kernel of one rft_ppo_clip_step call (23 dispatches, two row chunks)
+    "step_7b": {"sources": {"k_gemm_mfma.hip": "a4594bfb92840375", "k_step.hip": "de4f257d400d42e8",
+                            "k_simt.hip": "44616b4b548e8d1d", "k_adv_loss.hip": "936c78be1bd3081a",
+                            "k_tokens.hip": "d52b04cf394f6696", "rft_internal.h": "a9912954a57ce531",
+                            "rft_abi.hip": "8be3ec3097a92586"},
+                "bytes": 505081928.3 * 1024 * 2.0 + 111257781.1 * 1024 * 1.0},
+    "lossonly": {"sources": {"k_logits.hip": "3386de2d13ece5b6", "rft_internal.h": "a9912954a57ce531"},
+                 "bytes": 8759347.3 * 1024 * 2.0 + 19471427.7 * 1024 * 1.0},
 }
 
 
