@@ -38,7 +38,7 @@ TRAFFIC = {
     "step_7b": {"sources": {"k_gemm_mfma.hip": "a4594bfb92840375", "k_step.hip": "de4f257d400d42e8",
                             "k_simt.hip": "44616b4b548e8d1d", "k_adv_loss.hip": "936c78be1bd3081a",
                             "k_tokens.hip": "d52b04cf394f6696", "rft_internal.h": "a9912954a57ce531",
-                            "rft_abi.hip": "8be3ec3097a92586"},
+                            "rft_abi.hip": "dbccae017e695cd8"},
                 "bytes": 505081928.3 * 1024 * 2.0 + 111257781.1 * 1024 * 1.0},
     "lossonly": {"sources": {"k_logits.hip": "3386de2d13ece5b6", "rft_internal.h": "a9912954a57ce531"},
                  "bytes": 8759347.3 * 1024 * 2.0 + 19471427.7 * 1024 * 1.0},

@@ -41,7 +41,7 @@
  *    (mean of -logp over their valid tokens).
  *  - Matrices are row-major.  hidden is [T, d], weight is [V, d] (the
  *    nn.Linear layout; logits z_t = weight . hidden_t), logits are [T, V].
- *    bf16 data requires d % 8 == 0.
+ *    bf16 data requires d % 8 == 0 and V <= 4194048 (2^22 - 256).
  */
 #ifndef RFT_H_
 #define RFT_H_

@@ -65,6 +65,10 @@ rft_status check_hw(const char* fn, int64_t T, const void* hidden, const void* w
   if (!weight || (T > 0 && !hidden)) return fail(RFT_E_NULL, "%s: hidden / weight is NULL", fn);
   if (dtype == RFT_BF16) {
     if (d % 8) return fail(RFT_E_SHAPE, "%s: bf16 needs d %% 8 == 0 (d=%lld)", fn, (long long)d);
+    // a 256-row tile of dZ [rows, Vpad] is one buffer descriptor (< 2^31 bytes)
+    if (round_up(V, 256) * 2 * 256 >= ((int64_t)1 << 31))
+      return fail(RFT_E_SHAPE, "%s: bf16 supports V <= %lld (V=%lld)", fn,
+                  (long long)(((int64_t)1 << 22) - 256), (long long)V);
     if ((hidden && !aligned16(hidden)) || !aligned16(weight))
       return fail(RFT_E_SHAPE, "%s: bf16 hidden / weight must be 16-byte aligned", fn);
   }

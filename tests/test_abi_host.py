@@ -85,6 +85,12 @@ def test_argument_validation_returns_codes():
                                 fake, fake, 1 << 30, s) == R.RFT_E_SHAPE      # d % 8
     assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 0, fake, fake, fake,
                                 fake, 1 << 30, s) == R.RFT_E_SHAPE
+    # largest bf16 vocabulary: one 256-row dZ tile must fit a 2^31-byte descriptor
+    assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, (1 << 22) - 255,
+                                fake, fake, fake, fake, 1 << 30, s) == R.RFT_E_SHAPE
+    assert L.rft_ppo_clip_step(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, (1 << 22) - 255,
+                               fake, fake, fake, ctypes.byref(R.ppo_params()), fake, fake, fake,
+                               fake, fake, fake, 0, fake, fake, 1 << 30, s) == R.RFT_E_SHAPE
     assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
                                 fake, fake, 16, s) == R.RFT_E_WORKSPACE
     assert L.rft_token_logprobs(ctypes.byref(tk), fake, fake, R.RFT_BF16, 64, 100, fake, fake,
