@@ -13,8 +13,8 @@ import torch
 import paper_2505_17826_amd as R
 from gen import synth
 from oracle import rft_oracle as O
-from tests.gpu_cases import (TOL_GRAD_FRO, TOL_LOGP, TOL_LOSS_ABS, TOL_LOSS_REL, cpu, oracle_eps,
-                             params_of, rel_fro, requires_gpu)
+from tests.gpu_cases import (TOL_GRAD_FRO, TOL_LOGP, TOL_LOSS_ABS, TOL_LOSS_REL, cpu, f32,
+                             oracle_eps, params_of, rel_fro, requires_gpu)
 
 pytestmark = [pytest.mark.gpu, requires_gpu]
 DEV = torch.device("cuda")
@@ -220,3 +220,58 @@ def test_fullsize_step(cid):
     print(f"[fullsize-step] {cfg.name}: dH sampled rel {e1:.2e}; step vs separate backward "
           f"dW {e2:.2e} dH {e3:.2e}", flush=True)
     assert e1 <= TOL_GRAD_FRO and e2 <= 5e-3 and e3 <= 5e-3
+
+
+def test_fullsize_step_mix_entropy():
+    """The fused step at the 7B shape with expert rollouts (MIX, mu = 0.1) and an
+    entropy bonus: sampled rows of the per-token gradients and of dH against the
+    oracle, the expert count, and the zero column sums of dW (the bonus term
+    p (z - mu) sums to zero over the vocabulary like onehot - p)."""
+    cid = 2
+    cfg = synth.config(cid)
+    print(f"[fullsize-step-mix-entropy] {cfg.name}", flush=True)
+    b = synth.make_batch(cfg, DEV)
+    ex = (np.arange(cfg.n_seq) % 4 == 1).astype(np.uint8)
+    tok = R.Tokens(b.seq_start, b.mask, b.ids, torch.from_numpy(ex).to(DEV))
+    T, d, V = b.T, cfg.d, cfg.V
+    m = b.mask.bool()
+    lp0 = -math.log(V)
+    old = torch.where(m, lp0 + synth.extra_normal(T, (cid, 5), DEV, std=1.0), torch.zeros(T, device=DEV))
+    ref = torch.where(m, old + synth.extra_normal(T, (cid, 6), DEV, std=0.1), torch.zeros(T, device=DEV))
+    adv = R.rft_group_advantages(b.rewards, cfg.group)
+    mu, coef = 0.1, 0.01
+    ws = _ws(R.RFT_OP_PPO_STEP, tok, d, V, R.RFT_BF16)
+    logp, ent, lse, grad, dH, dW, st = R.rft_ppo_clip_step(
+        tok, b.H, b.W, old, ref, adv, params_of(cfg, mix_mu=mu, ent=coef), ws=ws)
+    torch.cuda.synchronize()
+    s = R.stats_to_dict(st)
+    cnt = O.token_counts(b.mask, b.seq_start)
+    n_exp = int(sum(cnt["n"][i] for i in range(cfg.n_seq) if ex[i]))
+    assert s["n_valid"] == cnt["N"] and s["n_expert"] == n_exp and n_exp > 0
+    assert math.isfinite(s["loss"]) and s["entropy_loss"] > 0
+    rows = _sample_rows(b.mask, 24, 41)
+    olp, oent, olse = O.token_logprobs(b.H, b.W, b.ids, b.mask, rows=rows)
+    for name, g, o in (("logp", logp, olp), ("entropy", ent, oent), ("lse", lse, olse)):
+        err = np.abs(cpu(g)[rows] - o[rows]).max()
+        assert err <= TOL_LOGP, (name, err)
+    el, eh, be = oracle_eps(cfg)
+    advo = O.group_advantages(b.rewards.cpu().numpy(), cfg.group)
+    of = O.ppo_clip_loss_fwd(olp, cpu(old), cpu(ref), advo, b.mask, b.seq_start, b.ids, V, el, eh,
+                             be, cfg.agg, entropy=oent, is_expert=ex, mix_mu=f32(mu),
+                             entropy_coef=f32(coef))
+    # tokens near a clip bound are left out (either branch is valid there)
+    g_o = of["grad_logp"][rows]
+    lo, hi = O.clip_thresholds(el, eh)
+    dl = (np.float32(cpu(logp)[rows]) - np.float32(cpu(old)[rows])).astype(np.float64)
+    near = np.minimum(np.abs(dl - float(hi)), np.abs(dl - float(lo))) < 1e-4
+    gg = cpu(grad)[rows]
+    np.testing.assert_allclose(gg[~near], g_o[~near], rtol=1e-3, atol=1e-7 * np.abs(g_o).max())
+    hrows = rows[~near][:12]
+    odH, _ = O.ppo_clip_loss_bwd(b.H, b.W, olse, of["grad_logp"], b.ids, b.mask, rows=hrows,
+                                 want_dw=False, grad_entropy=of["grad_entropy"], entropy=oent)
+    e1 = rel_fro(cpu(dH)[hrows], odH[hrows])
+    dWn = dW.double()
+    colsum = dWn.sum(dim=0).norm().item()
+    assert colsum <= 2e-2 * dWn.norm().item(), (colsum, dWn.norm().item())
+    print(f"[fullsize-step-mix-entropy] dH sampled rel {e1:.2e}", flush=True)
+    assert e1 <= TOL_GRAD_FRO
