@@ -34,8 +34,9 @@ Readings where the paper is silent (it prints no formula):
   R2 Aggregation: mode 0 = mean over rollouts of the per-rollout token mean
      (weight 1/(S n_i)); mode 1 = mean over all valid tokens (weight 1/N).
      ``denom_override > 0`` replaces S (mode 0) or N (mode 1).
-  R3 Group std: sample std (divisor G-1), eps = 1e-6 added to the std; a group
-     whose rewards are all equal (or G = 1) gets advantage exactly 0.
+  R3 Group std: sample std (divisor G-1) by default, the population std
+     (divisor G) on request; eps = 1e-6 added to the std; a group whose rewards
+     are all equal (or G = 1) gets advantage exactly 0.
   R4 Clip decision: strict inequalities, taken in fp32 on ``logp - old``
      against ``fp32(log(1 +/- eps))`` so that a GPU fed the same fp32 inputs
      takes the same decision; values are fp64.
@@ -134,11 +135,12 @@ def token_counts(mask, seq_start):
 
 
 # ------------------------------------------------------------ advantages ----
-def group_advantages(rewards, group_size, eps=1e-6):
+def group_advantages(rewards, group_size, eps=1e-6, unbiased=True):
     """GRPO advantages (Sec. 3.2 Listing 4 ``advantage_fn: "grpo"``; reading R3).
 
     Rewards of consecutive rollouts ``[g*G, (g+1)*G)`` form one group:
-    ``A_i = (r_i - mean) / (std + eps)`` with the sample standard deviation.
+    ``A_i = (r_i - mean) / (std + eps)`` with the sample standard deviation
+    (divisor G - 1), or the population one (divisor G) when not ``unbiased``.
     """
     r = _f64(rewards)
     G = int(group_size)
@@ -149,7 +151,7 @@ def group_advantages(rewards, group_size, eps=1e-6):
         if G < 2 or np.all(grp == grp[0]):
             continue                      # degenerate group: advantage 0
         mu = grp.sum() / G
-        sd = math.sqrt(((grp - mu) ** 2).sum() / (G - 1))
+        sd = math.sqrt(((grp - mu) ** 2).sum() / (G - 1 if unbiased else G))
         out[g0:g0 + G] = (grp - mu) / (sd + eps)
     return out
 
@@ -157,7 +159,8 @@ def group_advantages(rewards, group_size, eps=1e-6):
 ADV_GRPO, ADV_MEAN_CENTER, ADV_LEAVE_ONE_OUT = 0, 1, 2
 
 
-def group_advantages_ids(rewards, group_id, mode=ADV_GRPO, eps=1e-6, n_groups=None):
+def group_advantages_ids(rewards, group_id, mode=ADV_GRPO, eps=1e-6, n_groups=None,
+                         unbiased=True):
     """Advantages over explicit, variable-size groups (reading R14); with
     ``n_groups`` given, ids at or above it also leave their rollout out."""
     r = _f64(rewards)
@@ -175,7 +178,7 @@ def group_advantages_ids(rewards, group_id, mode=ADV_GRPO, eps=1e-6, n_groups=No
         vals = [r[i] for i in members]
         total = sum(vals)
         mu = total / G
-        sd = math.sqrt(sum((v - mu) ** 2 for v in vals) / (G - 1))
+        sd = math.sqrt(sum((v - mu) ** 2 for v in vals) / (G - 1 if unbiased else G))
         tied = all(v == vals[0] for v in vals)
         for i in members:
             if mode == ADV_GRPO:

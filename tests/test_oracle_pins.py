@@ -924,3 +924,24 @@ def test_advantages_ids_contiguous_equals_grpo_and_identities():
         np.testing.assert_allclose(a7[k7], O.group_advantages_ids(r[k7], gid2[k7], mode),
                                    rtol=1e-13, atol=1e-15)
         assert np.all(a7[~k7] == 0)
+
+
+def test_advantages_population_std():
+    """Population std (divisor G): numpy's std with ddof=0 (library routine),
+    the G = 2 closed form (std 1/2), and A_pop = A_sample sqrt(G / (G - 1))
+    at eps = 0."""
+    rng = np.random.default_rng(91)
+    G = 8
+    r = rng.random(G * 5)
+    a = O.group_advantages(r, G, 0.0, unbiased=False)
+    for g0 in range(0, r.size, G):
+        grp = r[g0:g0 + G]
+        np.testing.assert_allclose(a[g0:g0 + G], (grp - grp.mean()) / np.std(grp, ddof=0),
+                                   rtol=1e-12)
+    np.testing.assert_allclose(a, O.group_advantages(r, G, 0.0) * math.sqrt(G / (G - 1)),
+                               rtol=1e-12)
+    two = O.group_advantages(np.array([0.0, 1.0]), 2, 1e-6, unbiased=False)
+    np.testing.assert_allclose(two, [-0.5 / (0.5 + 1e-6), 0.5 / (0.5 + 1e-6)], rtol=1e-15)
+    gid = np.repeat(np.arange(5), G)
+    np.testing.assert_allclose(O.group_advantages_ids(r, gid, O.ADV_GRPO, 0.0, unbiased=False),
+                               a, rtol=1e-12)
