@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define RFT_ABI_VERSION 5
+#define RFT_ABI_VERSION 6
 
 typedef enum {
   RFT_OK = 0,
@@ -178,19 +178,21 @@ size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t
  * repeat_times 8; Sec. 3.3.1: 8 rollouts per task).
  * rewards[n_groups * group_size] (f32); rollouts g*G .. g*G+G-1 form group g.
  * adv_i = (r_i - mean_g) / (std_g + eps), std the sample standard deviation
- * (divisor G - 1); a group whose rewards are all equal (or G == 1) gets 0.
+ * (divisor G - 1) when unbiased != 0, else the population one (divisor G); a
+ * group whose rewards are all equal (or G == 1) gets 0.
  * adv[n_groups * group_size] (f32) may not alias rewards.
  * Errors: RFT_E_NULL, RFT_E_SHAPE (n_groups < 0, group_size < 1),
  * RFT_E_PARAM (eps < 0 or not finite). */
 rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t group_size,
-                                float eps, float* adv, void* stream);
+                                float eps, int32_t unbiased, float* adv, void* stream);
 
 /* Advantages over explicit, variable-size groups (Sec. 2.2: rollouts that
  * failed, were skipped or wait for a lagged reward leave their group smaller;
  * Sec. 3.2, Listing 4: advantage_fn grpo).  group_id[i] in [0, n_groups) puts
  * rollout i in that group; an id outside that range leaves the rollout out
  * (advantage 0).  G = the number of rollouts of the group; groups with G < 2
- * give 0.  mode: RFT_ADV_GRPO (as rft_group_advantages, sample std + eps),
+ * give 0.  mode: RFT_ADV_GRPO (as rft_group_advantages: std + eps, the std
+ * unbiased as there),
  * RFT_ADV_MEAN_CENTER, RFT_ADV_LEAVE_ONE_OUT (r_i - (sum_g - r_i) / (G - 1)).
  * Sums in fp64 in index order.  The work grows as n * n_groups (each group
  * scans the ids), meant for batches of up to about 1e5 rollouts.
@@ -198,8 +200,8 @@ rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t 
  * Errors: RFT_E_NULL, RFT_E_SHAPE (n < 0, n_groups < 0 or > 2^31 - 1),
  * RFT_E_PARAM (mode unknown, eps < 0 or not finite). */
 rft_status rft_group_advantages_ids(const float* rewards, const int32_t* group_id, int64_t n,
-                                    int64_t n_groups, int32_t mode, float eps, float* adv,
-                                    void* stream);
+                                    int64_t n_groups, int32_t mode, float eps, int32_t unbiased,
+                                    float* adv, void* stream);
 
 /* Per-token log-probability of the sampled id, entropy and log-sum-exp of the
  * policy head z_t = weight . hidden_t over the whole vocabulary (Sec. 3.1.1:

@@ -71,9 +71,10 @@ _SIGS = {
                                               ctypes.c_int]),
     "rft_workspace_min_bytes": (ctypes.c_size_t, [ctypes.c_int, ctypes.POINTER(rft_tokens), _i64,
                                                   _i64, ctypes.c_int]),
-    "rft_group_advantages": (ctypes.c_int, [_p, _i64, ctypes.c_int32, ctypes.c_float, _p, _p]),
+    "rft_group_advantages": (ctypes.c_int, [_p, _i64, ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
+                                            _p, _p]),
     "rft_group_advantages_ids": (ctypes.c_int, [_p, _p, _i64, _i64, ctypes.c_int32, ctypes.c_float,
-                                                _p, _p]),
+                                                ctypes.c_int32, _p, _p]),
     "rft_token_logprobs": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _p, ctypes.c_int, _i64,
                                           _i64, _p, _p, _p, _p, ctypes.c_size_t, _p]),
     "rft_token_logprobs_from_logits": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _i64, _p,
@@ -214,21 +215,22 @@ def _workspace(nbytes, device, ws=None):
 
 
 # ------------------------------------------------------------ entry points --
-def rft_group_advantages(rewards, group_size, eps=1e-6, out=None, stream=None):
+def rft_group_advantages(rewards, group_size, eps=1e-6, out=None, stream=None, unbiased=True):
     _need_gpu(rewards)
     out = torch.empty_like(rewards) if out is None else out
     n_groups = rewards.numel() // group_size if group_size > 0 else 0
-    _check(lib().rft_group_advantages(_ptr(rewards), n_groups, group_size, eps, _ptr(out),
-                                      _stream(stream)))
+    _check(lib().rft_group_advantages(_ptr(rewards), n_groups, group_size, eps,
+                                      1 if unbiased else 0, _ptr(out), _stream(stream)))
     return out
 
 
 def rft_group_advantages_ids(rewards, group_id, n_groups, mode=RFT_ADV_GRPO, eps=1e-6, out=None,
-                             stream=None):
+                             stream=None, unbiased=True):
     _need_gpu(rewards, group_id)
     out = torch.empty_like(rewards) if out is None else out
     _check(lib().rft_group_advantages_ids(_ptr(rewards), _ptr(group_id), rewards.numel(), n_groups,
-                                          mode, eps, _ptr(out), _stream(stream)))
+                                          mode, eps, 1 if unbiased else 0, _ptr(out),
+                                          _stream(stream)))
     return out
 
 

@@ -7,9 +7,10 @@ namespace rft {
 
 // ---------------------------------------------------------- advantages ----
 // GRPO (Sec. 3.2, Listing 4, advantage_fn "grpo"): one wavefront per group;
-// mean and sample std by wavefront shuffles, computed in fp64.
+// mean and sample (or population) std by wavefront shuffles, computed in fp64.
 __global__ void __launch_bounds__(256) k_group_adv(const float* __restrict__ r, int64_t n_groups,
-                                                   int G, float eps, float* __restrict__ adv) {
+                                                   int G, float eps, int unbiased,
+                                                   float* __restrict__ adv) {
   int lane = threadIdx.x & 63;
   int64_t g = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (g >= n_groups) return;
@@ -33,14 +34,15 @@ __global__ void __launch_bounds__(256) k_group_adv(const float* __restrict__ r, 
   }
   q = wave_sum_d(q);
   bool degenerate = (G < 2) || (mn == mx);
-  double sd = degenerate ? 0.0 : sqrt(q / (double)(G - 1));
+  double sd = degenerate ? 0.0 : sqrt(q / (double)(unbiased ? G - 1 : G));
   for (int j = lane; j < G; j += 64)
     adv[g * G + j] = degenerate ? 0.f : (float)(((double)rg[j] - mu) / (sd + (double)eps));
 }
 
-hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, float* adv,
-                            hipStream_t s) {
-  if (n_groups > 0) k_group_adv<<<(unsigned)((n_groups + 3) / 4), 256, 0, s>>>(r, n_groups, G, eps, adv);
+hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, int unbiased,
+                            float* adv, hipStream_t s) {
+  if (n_groups > 0)
+    k_group_adv<<<(unsigned)((n_groups + 3) / 4), 256, 0, s>>>(r, n_groups, G, eps, unbiased, adv);
   return hipGetLastError();
 }
 
@@ -68,7 +70,8 @@ __global__ void __launch_bounds__(256) k_adv_left_out(const int32_t* __restrict_
 
 __global__ void __launch_bounds__(256) k_adv_groups(const float* __restrict__ r,
                                                     const int32_t* __restrict__ gid, int64_t n,
-                                                    int mode, float eps, float* __restrict__ adv) {
+                                                    int mode, float eps, int unbiased,
+                                                    float* __restrict__ adv) {
   __shared__ double shd[4];
   __shared__ int shi[4];
   __shared__ float shf[4];
@@ -106,7 +109,7 @@ __global__ void __launch_bounds__(256) k_adv_groups(const float* __restrict__ r,
       q += dv * dv;
     }
     q = block_sum256(q, shd);
-    sd = cnt > 1 ? sqrt(q / (G - 1.0)) : 0.0;
+    sd = cnt > 1 ? sqrt(q / (unbiased ? G - 1.0 : G)) : 0.0;
   }
   const bool degenerate = cnt < 2 || (mode == RFT_ADV_GRPO && mn == mx);
   for (int64_t i = threadIdx.x; i < n; i += 256) {
@@ -123,10 +126,11 @@ __global__ void __launch_bounds__(256) k_adv_groups(const float* __restrict__ r,
 }
 
 hipError_t launch_group_adv_ids(const float* r, const int32_t* gid, int64_t n, int64_t n_groups,
-                                int mode, float eps, float* adv, hipStream_t s) {
+                                int mode, float eps, int unbiased, float* adv, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   k_adv_left_out<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(gid, n, n_groups, adv);
-  if (n_groups > 0) k_adv_groups<<<(unsigned)n_groups, 256, 0, s>>>(r, gid, n, mode, eps, adv);
+  if (n_groups > 0)
+    k_adv_groups<<<(unsigned)n_groups, 256, 0, s>>>(r, gid, n, mode, eps, unbiased, adv);
   return hipGetLastError();
 }
 

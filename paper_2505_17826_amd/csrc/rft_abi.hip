@@ -366,20 +366,22 @@ size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t
 }
 
 rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t group_size,
-                                float eps, float* adv, void* stream) {
+                                float eps, int32_t unbiased, float* adv, void* stream) {
   const char* fn = "rft_group_advantages";
   if (n_groups < 0 || group_size < 1)
     return fail(RFT_E_SHAPE, "%s: n_groups=%lld group_size=%d", fn, (long long)n_groups, group_size);
   if (n_groups > 0 && (!rewards || !adv)) return fail(RFT_E_NULL, "%s: rewards / adv is NULL", fn);
   if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(RFT_E_PARAM, "%s: eps=%g", fn, (double)eps);
   if (n_groups > 0 && rewards == adv) return fail(RFT_E_PARAM, "%s: adv may not alias rewards", fn);
-  RFT_HIP(launch_group_adv(rewards, n_groups, group_size, eps, adv, (hipStream_t)stream), fn);
+  RFT_HIP(launch_group_adv(rewards, n_groups, group_size, eps, unbiased ? 1 : 0, adv,
+                           (hipStream_t)stream),
+          fn);
   return RFT_OK;
 }
 
 rft_status rft_group_advantages_ids(const float* rewards, const int32_t* group_id, int64_t n,
-                                    int64_t n_groups, int32_t mode, float eps, float* adv,
-                                    void* stream) {
+                                    int64_t n_groups, int32_t mode, float eps, int32_t unbiased,
+                                    float* adv, void* stream) {
   const char* fn = "rft_group_advantages_ids";
   if (n < 0 || n_groups < 0 || n_groups > (int64_t)std::numeric_limits<int32_t>::max())
     return fail(RFT_E_SHAPE, "%s: n=%lld n_groups=%lld", fn, (long long)n, (long long)n_groups);
@@ -389,7 +391,7 @@ rft_status rft_group_advantages_ids(const float* rewards, const int32_t* group_i
     return fail(RFT_E_PARAM, "%s: mode=%d unknown", fn, mode);
   if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(RFT_E_PARAM, "%s: eps=%g", fn, (double)eps);
   if (n > 0 && rewards == adv) return fail(RFT_E_PARAM, "%s: adv may not alias rewards", fn);
-  RFT_HIP(launch_group_adv_ids(rewards, group_id, n, n_groups, mode, eps, adv,
+  RFT_HIP(launch_group_adv_ids(rewards, group_id, n, n_groups, mode, eps, unbiased ? 1 : 0, adv,
                                (hipStream_t)stream),
           fn);
   return RFT_OK;

@@ -249,10 +249,10 @@ hipError_t launch_dpo(const rft_tokens& tok, const TokMeta& m, int64_t V, const 
                       float* seq_logp, rft_dpo_stats* st, hipStream_t s);
 
 // ------------------------------------------------------------ launchers --
-hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, float* adv,
-                            hipStream_t s);
+hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, int unbiased,
+                            float* adv, hipStream_t s);
 hipError_t launch_group_adv_ids(const float* r, const int32_t* gid, int64_t n, int64_t n_groups,
-                                int mode, float eps, float* adv, hipStream_t s);
+                                int mode, float eps, int unbiased, float* adv, hipStream_t s);
 hipError_t launch_loss_fwd(const rft_tokens& tok, const TokMeta& m, const float* logp,
                            const float* old, const float* ref, const float* adv, const float* ent,
                            const LossConst& c, float* grad, float* egrad, LossPartial* parts,

@@ -65,11 +65,11 @@ def test_argument_validation_returns_codes():
     s = None
     fake = ctypes.c_void_p(0x1000)
     # advantages
-    assert L.rft_group_advantages(fake, -1, 8, 1e-6, fake, s) == R.RFT_E_SHAPE
-    assert L.rft_group_advantages(fake, 4, 0, 1e-6, fake, s) == R.RFT_E_SHAPE
-    assert L.rft_group_advantages(None, 4, 8, 1e-6, fake, s) == R.RFT_E_NULL
-    assert L.rft_group_advantages(fake, 4, 8, -1.0, ctypes.c_void_p(0x2000), s) == R.RFT_E_PARAM
-    assert L.rft_group_advantages(fake, 4, 8, 1e-6, fake, s) == R.RFT_E_PARAM  # aliasing
+    assert L.rft_group_advantages(fake, -1, 8, 1e-6, 1, fake, s) == R.RFT_E_SHAPE
+    assert L.rft_group_advantages(fake, 4, 0, 1e-6, 1, fake, s) == R.RFT_E_SHAPE
+    assert L.rft_group_advantages(None, 4, 8, 1e-6, 1, fake, s) == R.RFT_E_NULL
+    assert L.rft_group_advantages(fake, 4, 8, -1.0, 1, ctypes.c_void_p(0x2000), s) == R.RFT_E_PARAM
+    assert L.rft_group_advantages(fake, 4, 8, 1e-6, 0, fake, s) == R.RFT_E_PARAM  # aliasing
     assert b"alias" in L.rft_last_error()
     # log-probs
     tk = _tok()
@@ -135,13 +135,13 @@ def test_argument_validation_returns_codes():
                                ctypes.byref(P(entropy_coef=0.01)), fake, None, fake, fake, fake,
                                fake, 0, fake, fake, 1 << 30, s) == R.RFT_E_NULL
     # advantages over group ids
-    for args, code in [((fake, fake, -1, 4, 0, 1e-6, fake), R.RFT_E_SHAPE),
-                       ((fake, fake, 8, -1, 0, 1e-6, fake), R.RFT_E_SHAPE),
-                       ((fake, fake, 8, 1 << 31, 0, 1e-6, fake), R.RFT_E_SHAPE),
-                       ((fake, None, 8, 4, 0, 1e-6, fake), R.RFT_E_NULL),
-                       ((fake, fake, 8, 4, 3, 1e-6, fake), R.RFT_E_PARAM),
-                       ((fake, fake, 8, 4, 0, -1.0, fake), R.RFT_E_PARAM),
-                       ((fake, fake, 8, 4, 0, 1e-6, fake), R.RFT_E_PARAM)]:   # adv aliases rewards
+    for args, code in [((fake, fake, -1, 4, 0, 1e-6, 1, fake), R.RFT_E_SHAPE),
+                       ((fake, fake, 8, -1, 0, 1e-6, 1, fake), R.RFT_E_SHAPE),
+                       ((fake, fake, 8, 1 << 31, 0, 1e-6, 1, fake), R.RFT_E_SHAPE),
+                       ((fake, None, 8, 4, 0, 1e-6, 1, fake), R.RFT_E_NULL),
+                       ((fake, fake, 8, 4, 3, 1e-6, 1, fake), R.RFT_E_PARAM),
+                       ((fake, fake, 8, 4, 0, -1.0, 1, fake), R.RFT_E_PARAM),
+                       ((fake, fake, 8, 4, 0, 1e-6, 1, fake), R.RFT_E_PARAM)]:  # adv aliases rewards
         assert L.rft_group_advantages_ids(*args, s) == code, args
     # SFT / DPO parameters and layout
     assert L.rft_sft_loss_fwd(ctypes.byref(tk), 100, fake, 7, 0.0, fake, fake, fake, 1 << 30,

@@ -34,6 +34,10 @@ def test_advantages_ids(mode, n, n_groups):
     a = R.rft_group_advantages_ids(_t(r), _t(gid), n_groups, mode, eps=1e-6)
     o = O.group_advantages_ids(r, gid, mode, f32(1e-6), n_groups=n_groups)
     np.testing.assert_allclose(cpu(a), o, atol=TOL_ADV, rtol=0)
+    if mode == R.RFT_ADV_GRPO:
+        a0 = R.rft_group_advantages_ids(_t(r), _t(gid), n_groups, mode, eps=1e-6, unbiased=False)
+        o0 = O.group_advantages_ids(r, gid, mode, f32(1e-6), n_groups=n_groups, unbiased=False)
+        np.testing.assert_allclose(cpu(a0), o0, atol=TOL_ADV, rtol=0)
     ga = cpu(a)
     out = (gid < 0) | (gid >= n_groups)
     assert np.all(ga[out] == 0.0)

@@ -47,12 +47,13 @@ def test_group_advantages(G):
     r[:G] = 0.25                                   # degenerate group
     if G >= 4:
         r[G:2 * G] = (rng.random(G) < 0.5).astype(np.float32)   # binary rewards
-    a = R.rft_group_advantages(torch.from_numpy(r).to(DEV), G)
-    torch.cuda.synchronize()
-    got = cpu(a)
-    exp = O.group_advantages(r.astype(np.float64), G)
-    assert np.all(got[:G] == 0.0)
-    np.testing.assert_allclose(got, exp, atol=TOL_ADV, rtol=0)
+    for unbiased in (True, False):
+        a = R.rft_group_advantages(torch.from_numpy(r).to(DEV), G, unbiased=unbiased)
+        torch.cuda.synchronize()
+        got = cpu(a)
+        exp = O.group_advantages(r.astype(np.float64), G, f32(1e-6), unbiased=unbiased)
+        assert np.all(got[:G] == 0.0)
+        np.testing.assert_allclose(got, exp, atol=TOL_ADV, rtol=0)
 
 
 # -------------------------------------------------------------- whole step --
