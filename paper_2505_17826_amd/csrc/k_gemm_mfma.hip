@@ -402,7 +402,11 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
           for (int j = 0; j < 4; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
       }
+      // Before the barrier: this wave's loads of the next stage have landed
+      // and its fragment reads of this stage are complete, so after the
+      // barrier no wave still reads the buffer that the next loads overwrite.
       wait_vm();
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
       barrier_lds();
     }
 
