@@ -60,6 +60,40 @@ def test_workspace_sizes_are_consistent():
     assert L.rft_workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, None, 256, 5000, R.RFT_BF16) == 0
 
 
+def test_chunked_workspace_sizes():
+    """The step / backward workspace: the recommended size holds every row in one
+    chunk up to 131072 rows and stays flat beyond; the minimum (256-row chunk)
+    is below it; the chunk buffer dominates (about 2 Vpad bytes per row); the
+    new losses and the advantages need no more than the PPO loss."""
+    L = R.lib()
+    d, V = 3584, 152064
+    Vpad = (V + 255) // 256 * 256
+
+    def rec(op, T, dt=R.RFT_BF16):
+        tk = _tok(T=T, n_seq=8)
+        return L.rft_workspace_bytes(op, ctypes.byref(tk), d, V, dt)
+
+    def mn(op, T, dt=R.RFT_BF16):
+        tk = _tok(T=T, n_seq=8)
+        return L.rft_workspace_min_bytes(op, ctypes.byref(tk), d, V, dt)
+
+    for op in (R.RFT_OP_PPO_STEP, R.RFT_OP_PPO_BWD):
+        r1, r2, r3 = rec(op, 65536), rec(op, 131072), rec(op, 262144)
+        assert r1 < r2 < r3
+        # growth from 131072 to 262144 rows is the per-row arrays only (no larger chunk)
+        assert r3 - r2 < 0.2 * (r2 - r1)
+        assert r2 - r1 >= 65536 * 2 * Vpad            # the chunk buffer of 65536 more rows
+        assert mn(op, 262144) < r3
+    # fp32 step: the three separate calls share the workspace, plus the bonus coefficients
+    s32 = rec(R.RFT_OP_PPO_STEP, 4096, R.RFT_F32)
+    b32 = rec(R.RFT_OP_PPO_BWD, 4096, R.RFT_F32)
+    assert s32 >= b32 + 4096 * 4
+    tk = _tok(T=4096, n_seq=8)
+    ppo = L.rft_workspace_bytes(R.RFT_OP_PPO_FWD, ctypes.byref(tk), 0, V, 0)
+    assert L.rft_workspace_bytes(R.RFT_OP_SFT_FWD, ctypes.byref(tk), 0, V, 0) == ppo
+    assert 0 < L.rft_workspace_bytes(R.RFT_OP_DPO_FWD, ctypes.byref(tk), 0, V, 0) <= 2 * ppo
+
+
 def test_argument_validation_returns_codes():
     L = R.lib()
     s = None
