@@ -30,9 +30,17 @@ CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,
           "-Wall", "-Wno-unused-function", "-Wno-unused-variable"]
 
 
+# Per-source flags. The GEMM epilogues take maxima over accumulators and
+# cross-lane moves; without NaN semantics the compiler drops the quieting of
+# each operand before every max (the hardware max still returns the non-NaN
+# operand, and exp/add still propagate a NaN into the sums).
+SOURCE_FLAGS = {"k_gemm_mfma.hip": ["-fno-honor-nans"]}
+
+
 def _compile(src, verbose=False, extra=()):
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *CFLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *CFLAGS, *SOURCE_FLAGS.get(src, []), *extra, "-c", os.path.join(CSRC, src),
+           "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     out = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
                     if "packed-fp32-ops" not in l)

@@ -420,49 +420,75 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       bool cv[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) cv[j] = colb + j * 32 < N;
+      // tiles wholly inside N (all but at most the last column of tiles) skip
+      // the column masks; the exponent is the hardware exp2 (arguments <= 0,
+      // results below 2^-126 flush to 0)
+      const bool full = n0 + BN <= N;
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         __builtin_amdgcn_sched_barrier(0);  // keep the accumulator reads of one tile row together
         float mx[16], sm[16], um[16];
+        if (full) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          float v = -INFINITY;
+          for (int e = 0; e < 16; ++e)
+            mx[e] = fmaxf(fmaxf(acc[i][0][e], acc[i][1][e]), fmaxf(acc[i][2][e], acc[i][3][e]));
+        } else {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v = cv[j] ? fmaxf(v, acc[i][j][e]) : v;
-          mx[e] = v;
-        }
+          for (int e = 0; e < 16; ++e) {
+            float v = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) mx[e] = half_max(mx[e]);
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          float s = 0.f, u = 0.f;
-          float mk = mx[e] == -INFINITY ? 0.f : mx[e] * kLog2e;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            float z = acc[i][j][e];
-            float p = cv[j] ? exp2f(z * kLog2e - mk) : 0.f;
-            s += p;
-            u += cv[j] ? p * z : 0.f;
+            for (int j = 0; j < 4; ++j) v = cv[j] ? fmaxf(v, acc[i][j][e]) : v;
+            mx[e] = v;
           }
-          sm[e] = s;
-          um[e] = u;
         }
+        half_max_n(mx);
+        if (full) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          sm[e] = half_sum(sm[e]);
-          um[e] = half_sum(um[e]);
+          for (int e = 0; e < 16; ++e) {
+            float s = 0.f, u = 0.f;
+            const float mk = mx[e] * kLog2e;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const float z = acc[i][j][e];
+              const float p = __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mk));
+              s += p;
+              u = fmaf(p, z, u);
+            }
+            sm[e] = s;
+            um[e] = u;
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            float s = 0.f, u = 0.f;
+            const float mk = mx[e] == -INFINITY ? 0.f : mx[e] * kLog2e;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const float z = acc[i][j][e];
+              const float p = cv[j] ? __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mk)) : 0.f;
+              s += p;
+              u = cv[j] ? fmaf(p, z, u) : u;
+            }
+            sm[e] = s;
+            um[e] = u;
+          }
         }
+        half_sum_n(sm);
+        half_sum_n(um);
         // logit of the sampled token
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           int rl = wm * 64 + i * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
           int y = rp_i[rl];
           int yl = y - (n0 + wn * 128);
-          if (yl >= 0 && yl < 128 && (yl & 31) == fr) {
-            int jj = yl >> 5;
-            float z = jj == 0 ? acc[i][0][e] : jj == 1 ? acc[i][1][e] : jj == 2 ? acc[i][2][e] : acc[i][3][e];
-            g.zy[g.rows_off + m0 + rl] = z;
-          }
+          // the value is picked with selects outside the store's branch, so
+          // no register copies of the accumulator tiles are made there
+          const int jj = yl >> 5;
+          float z = acc[i][0][e];
+          z = jj == 1 ? acc[i][1][e] : z;
+          z = jj == 2 ? acc[i][2][e] : z;
+          z = jj == 3 ? acc[i][3][e] : z;
+          if (yl >= 0 && yl < 128 && (yl & 31) == fr) g.zy[g.rows_off + m0 + rl] = z;
         }
         // lane (fr) < 16 owns row e = fr of its half
         float om = mx[0], os = sm[0], ou = um[0];
