@@ -79,6 +79,12 @@ Readings where the paper is silent (it prints no formula):
      its rollouts.  Modes: GRPO (R3 on
      the group); mean-centred r_i - mean; leave-one-out r_i - (mean of the
      other G - 1 rewards).  Groups of one rollout give 0 in every mode.
+  R15 Masked vocabulary entries: a given logit of -inf (an entry the caller
+     excludes) has p = 0, and the products p log p in the entropy and
+     p (z - mu) in its gradient are taken as their limit 0 (the convention
+     0 log 0 = 0 of the entropy's definition), so masking entries by -inf gives
+     the statistics and gradient of the vocabulary without them (and 0 at
+     their columns).  A row needs one finite logit.
 """
 from __future__ import annotations
 
@@ -193,13 +199,18 @@ def group_advantages_ids(rewards, group_id, mode=ADV_GRPO, eps=1e-6, n_groups=No
 
 
 # ------------------------------------------------------------- log-probs ----
+def _plogp(p, x):
+    """p * x with 0 where p == 0 (x may then be -inf: reading R15)."""
+    return np.where(p > 0, p * np.where(p > 0, x, 0.0), 0.0)
+
+
 def _row_stats(z, y, V):
     """Plain two-pass log-softmax statistics of one block of logit rows."""
     M = z.max(axis=1, keepdims=True)
     lse = (M + np.log(np.exp(z - M).sum(axis=1, keepdims=True)))[:, 0]
     logp_all = z - lse[:, None]
     p = np.exp(logp_all)
-    ent = -(p * logp_all).sum(axis=1)
+    ent = -_plogp(p, logp_all).sum(axis=1)
     ok = (y >= 0) & (y < V)
     logp = np.full(z.shape[0], np.nan)
     idx = np.nonzero(ok)[0]
@@ -516,7 +527,7 @@ def logit_grad_rows(z, y, lse, c, e=None, ent=None):
     out = c[:, None] * dz
     if e is not None:
         mu = lse - ent
-        out += e[:, None] * p * (z - mu[:, None])
+        out += e[:, None] * _plogp(p, z - mu[:, None])
     return out
 
 

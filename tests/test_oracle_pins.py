@@ -945,3 +945,41 @@ def test_advantages_population_std():
     gid = np.repeat(np.arange(5), G)
     np.testing.assert_allclose(O.group_advantages_ids(r, gid, O.ADV_GRPO, 0.0, unbiased=False),
                                a, rtol=1e-12)
+
+
+def test_masked_vocabulary_equals_removed_entries():
+    """Reading R15: logits of -inf act as entries removed from the vocabulary.
+    Log-prob, entropy and lse equal those of the reduced rows; the logit
+    gradient with the entropy bonus is the reduced rows' gradient, with 0 at
+    the masked columns; the entropy equals scipy's entr (0 log 0 = 0) summed
+    over the softmax."""
+    rng = np.random.default_rng(15)
+    T, V = 9, 40
+    z = rng.standard_normal((T, V)) * 2
+    ids = rng.integers(0, V, size=T)
+    keep = np.ones((T, V), bool)
+    for t in range(T):                                   # row 0 stays unmasked
+        others = np.setdiff1d(np.arange(V), [ids[t]])
+        keep[t, rng.choice(others, size=4 * t, replace=False)] = False
+    zm = np.where(keep, z, -np.inf)
+    mask = np.ones(T, np.uint8)
+    lp, en, ls = O.token_logprobs_from_logits(zm, ids, mask)
+    assert np.all(np.isfinite(lp)) and np.all(np.isfinite(en)) and np.all(np.isfinite(ls))
+    np.testing.assert_allclose(en, scipy.special.entr(scipy.special.softmax(zm, axis=1)).sum(1),
+                               rtol=1e-12)
+    np.testing.assert_allclose(ls, scipy.special.logsumexp(zm, axis=1), rtol=1e-13)
+    c = rng.standard_normal(T)
+    e = rng.random(T)
+    g = O.bwd_logits(zm, ls, c, ids, mask, grad_entropy=e, entropy=en)
+    for t in range(T):
+        zr = z[t, keep[t]][None, :]
+        yr = np.array([np.count_nonzero(keep[t, :ids[t]])])
+        one = np.ones(1, np.uint8)
+        lp_r, en_r, ls_r = O.token_logprobs_from_logits(zr, yr, one)
+        assert lp[t] == pytest.approx(lp_r[0], abs=1e-12)
+        assert en[t] == pytest.approx(en_r[0], abs=1e-12)
+        assert ls[t] == pytest.approx(ls_r[0], abs=1e-12)
+        g_r = O.bwd_logits(zr, ls_r, c[t:t + 1], yr, one, grad_entropy=e[t:t + 1],
+                           entropy=en_r)[0]
+        np.testing.assert_allclose(g[t][keep[t]], g_r, rtol=0, atol=1e-13)
+        assert np.all(g[t][~keep[t]] == 0.0)
