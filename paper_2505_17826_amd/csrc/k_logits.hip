@@ -23,31 +23,40 @@ struct RowStats {
   float m, s, u;
 };
 
+// Online (max, sum exp, sum exp * z) over a thread's logits.  Every exponent
+// argument is <= 0 (hardware exp2; results below 2^-126 flush to 0).  Logits
+// of -inf (masked entries) add nothing: while the running max is still -inf
+// the exponents are taken against 0, and z is clamped to the finite range in
+// the product exp * z (0 * z stays 0).
+__device__ __forceinline__ float zfin(float z) { return fmaxf(z, -FLT_MAX); }
+
 __device__ __forceinline__ void acc4(RowStats& r, float4 q) {
   float mq = fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w));
   if (mq > r.m) {  // rescale to the new running max
-    float sc = exp2f((r.m - mq) * kLog2e);
+    float sc = __builtin_amdgcn_exp2f((r.m - mq) * kLog2e);
     r.s *= sc;
     r.u *= sc;
     r.m = mq;
   }
-  float mk = r.m * kLog2e;
-  float e0 = exp2f(fmaf(q.x, kLog2e, -mk)), e1 = exp2f(fmaf(q.y, kLog2e, -mk));
-  float e2 = exp2f(fmaf(q.z, kLog2e, -mk)), e3 = exp2f(fmaf(q.w, kLog2e, -mk));
+  float mk = r.m == -INFINITY ? 0.f : r.m * kLog2e;
+  float e0 = __builtin_amdgcn_exp2f(fmaf(q.x, kLog2e, -mk));
+  float e1 = __builtin_amdgcn_exp2f(fmaf(q.y, kLog2e, -mk));
+  float e2 = __builtin_amdgcn_exp2f(fmaf(q.z, kLog2e, -mk));
+  float e3 = __builtin_amdgcn_exp2f(fmaf(q.w, kLog2e, -mk));
   r.s += (e0 + e1) + (e2 + e3);
-  r.u += (e0 * q.x + e1 * q.y) + (e2 * q.z + e3 * q.w);
+  r.u += (e0 * zfin(q.x) + e1 * zfin(q.y)) + (e2 * zfin(q.z) + e3 * zfin(q.w));
 }
 
 __device__ __forceinline__ void acc1(RowStats& r, float z) {
   if (z > r.m) {
-    float sc = exp2f((r.m - z) * kLog2e);
+    float sc = __builtin_amdgcn_exp2f((r.m - z) * kLog2e);
     r.s *= sc;
     r.u *= sc;
     r.m = z;
   }
-  float e = exp2f((z - r.m) * kLog2e);
+  float e = __builtin_amdgcn_exp2f(fmaf(z, kLog2e, r.m == -INFINITY ? 0.f : -r.m * kLog2e));
   r.s += e;
-  r.u += e * z;
+  r.u += e * zfin(z);
 }
 
 // Workgroup reduction of the per-thread online partials, in a fixed order.
@@ -55,7 +64,7 @@ template <int NTH = NT>
 __device__ RowStats block_stats(RowStats r, RowStats* sh) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   float M = wave_max_f(r.m);
-  float sc = (r.s > 0.f) ? exp2f((r.m - M) * kLog2e) : 0.f;
+  float sc = (r.s > 0.f) ? __builtin_amdgcn_exp2f((r.m - M) * kLog2e) : 0.f;
   float s = wave_sum_f(r.s * sc), u = wave_sum_f(r.u * sc);
   if (lane == 0) sh[w] = RowStats{M, s, u};
   __syncthreads();
@@ -104,15 +113,15 @@ __device__ void row_pass2(const float* __restrict__ z, int64_t V, float lse, flo
       float4 q = z4[j];
       const int hot = (y >> 2) == j ? (y & 3) : -1;
       floatx4 d;
-      d[0] = dlogit(c, e, mu, exp2f(fmaf(q.x, kLog2e, -lk)), q.x, hot == 0);
-      d[1] = dlogit(c, e, mu, exp2f(fmaf(q.y, kLog2e, -lk)), q.y, hot == 1);
-      d[2] = dlogit(c, e, mu, exp2f(fmaf(q.z, kLog2e, -lk)), q.z, hot == 2);
-      d[3] = dlogit(c, e, mu, exp2f(fmaf(q.w, kLog2e, -lk)), q.w, hot == 3);
+      d[0] = dlogit(c, e, mu, __builtin_amdgcn_exp2f(fmaf(q.x, kLog2e, -lk)), q.x, hot == 0);
+      d[1] = dlogit(c, e, mu, __builtin_amdgcn_exp2f(fmaf(q.y, kLog2e, -lk)), q.y, hot == 1);
+      d[2] = dlogit(c, e, mu, __builtin_amdgcn_exp2f(fmaf(q.z, kLog2e, -lk)), q.z, hot == 2);
+      d[3] = dlogit(c, e, mu, __builtin_amdgcn_exp2f(fmaf(q.w, kLog2e, -lk)), q.w, hot == 3);
       __builtin_nontemporal_store(d, o4 + j);
     }
   } else {
     for (int64_t j = threadIdx.x; j < V; j += NT)
-      out[j] = dlogit(c, e, mu, exp2f(fmaf(z[j], kLog2e, -lk)), z[j], j == y);
+      out[j] = dlogit(c, e, mu, __builtin_amdgcn_exp2f(fmaf(z[j], kLog2e, -lk)), z[j], j == y);
   }
 }
 
@@ -263,7 +272,7 @@ __device__ __forceinline__ floatx4 dlogit4(floatx4 q, float lk, float c, float e
   floatx4 d;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const float p = exp2f(fmaf(q[i], kLog2e, -lk));
+    const float p = __builtin_amdgcn_exp2f(fmaf(q[i], kLog2e, -lk));
     d[i] = ENT ? dlogit(c, e, mu, p, q[i], hot == i) : c * ((hot == i ? 1.f : 0.f) - p);
   }
   return d;
@@ -382,7 +391,7 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
   for (int u = 0; u < REGS; ++u)
     __builtin_amdgcn_raw_buffer_store_b128(
         (v4i)dlogit4<ENT>(regs[u], lk, c, e, mu, tid + (int64_t)u * NTC, y), rout,
-        u < nv2 ? vo2 : 0x80000000u, (uint32_t)u * SU, 2);
+        u < nv2 ? vo2 + (uint32_t)u * SU : 0x80000000u, 0, 2);
   for (int64_t j = j_lds + tid, s_ = tid; j < n4 && s_ < LCAP; j += NTC, s_ += NTC)
     __builtin_amdgcn_raw_buffer_store_b128((v4i)dlogit4<ENT>(row_lds[s_], lk, c, e, mu, j, y), rout,
                                            (uint32_t)(j * 16), 0, 2);

@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <float.h>
 #include <math.h>
 
 #include "rft.h"
@@ -260,8 +261,12 @@ __device__ __forceinline__ float row_loss(float lp, float old, float ref, float 
 // d loss / d z_j of one row: c (onehot - p_j) + e p_j (z_j - mu), with p_j the
 // softmax probability, c = d loss / d logp, e the entropy-bonus coefficient
 // and mu = lse - H the softmax mean of z (d H / d z_j = -p_j (z_j - mu)).
+// The entropy term is taken as 0 where p = 0 (its value for any finite z, and
+// its limit for a masked vocabulary entry z = -inf, where 0 * (z - mu) would
+// be NaN).
 __device__ __forceinline__ float dlogit(float c, float e, float mu, float p, float z, bool hot) {
-  return c * ((hot ? 1.f : 0.f) - p) + e * p * (z - mu);
+  const float t = e * p * (z - mu);
+  return c * ((hot ? 1.f : 0.f) - p) + (p > 0.f ? t : 0.f);
 }
 
 #define RFT_ZERO_PARTIAL LossPartial{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0}

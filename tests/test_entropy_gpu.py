@@ -156,3 +156,75 @@ def test_entropy_loss_only_paths():
     assert abs(s2["loss"] - o["fwd"]["loss"]) <= TOL_LOSS_REL * abs(o["fwd"]["loss"]) + TOL_LOSS_ABS
     # the two paths agree far inside the tolerance
     assert rel_fro(cpu(dl), cpu(dl2)) <= 1e-5
+
+
+def _mask_vocab(logits, ids, mask, seed):
+    """Set vocabulary entries to -inf (masked), never the sampled id: row
+    kinds by index mod 3: 30% of the entries at random; all but a window of
+    64 entries (most threads then see only -inf); none."""
+    z = logits.numpy().copy()
+    rng = np.random.default_rng(seed)
+    T, V = z.shape
+    for t in range(T):
+        if t % 3 == 0:
+            z[t, rng.random(V) < 0.3] = -np.inf
+        elif t % 3 == 1:
+            w0 = int(rng.integers(0, V - 64))
+            keep = z[t, w0:w0 + 64].copy()
+            z[t, :] = -np.inf
+            z[t, w0:w0 + 64] = keep
+        y = int(ids[t])
+        if mask[t] and 0 <= y < V:
+            z[t, y] = float(logits[t, y])
+    return torch.from_numpy(z)
+
+
+@pytest.mark.parametrize("V,group", [(8192, 8), (8190, 8), (160000, 2)])
+def test_masked_vocabulary_logits(V, group):
+    """Loss-only paths on logits with -inf entries (reading R15): fused and
+    separate calls against the oracle, no NaN anywhere, and d_logits exactly
+    0 in the masked columns.  V = 8190 takes the scalar path, V = 160000
+    exceeds the on-chip row cache."""
+    cfg = synth.config(4, n_prompts=1, group=group, V=V)
+    b = synth.make_batch(cfg, "cpu", seed_key=(4, 151, V))
+    zm = _mask_vocab(b.logits, b.ids.numpy(), b.mask.numpy(), V)
+    lp, _, _ = O.token_logprobs_from_logits(zm, b.ids, b.mask)
+    old, ref = perturbed_logprobs(lp, b)
+    el, eh, be = oracle_eps(cfg)
+    coef = 0.5
+    print(f"[masked vocab] V={V} T={b.T}", flush=True)
+    o = O.loss_only_step(zm, b.ids, b.mask, b.seq_start, b.rewards, cfg.group,
+                         old.astype(np.float64), ref.astype(np.float64), el, eh, be, cfg.agg,
+                         entropy_coef=f32(coef))
+    dl_o = np.zeros(zm.shape)
+    for r_, v in o["dlogits"].items():
+        dl_o[r_] = v
+    masked = ~np.isfinite(zm.numpy())
+    assert masked.any() and np.all(dl_o[masked] == 0)
+    tok = tokens_of(b)
+    adv = R.rft_group_advantages(b.rewards.to(DEV), cfg.group)
+    logits = zm.to(DEV)
+    p = params_of(cfg, ent=coef)
+    ent_f = torch.empty(b.T, device=DEV)
+    lpg, dl, st = R.rft_ppo_clip_fused_logits(tok, logits, _t(old), _t(ref), adv, p,
+                                              entropy=ent_f)
+    lp2, ent2, lse2, _ = R.rft_token_logprobs_from_logits(tok, logits)
+    eg = torch.empty_like(lp2)
+    grad, st2 = R.rft_ppo_clip_loss_fwd(tok, cfg.V, lp2, _t(old), _t(ref), adv, p, entropy=ent2,
+                                        grad_entropy=eg)
+    dl2 = R.rft_ppo_clip_loss_bwd_logits(tok, logits, lse2, grad, grad_entropy=eg, entropy=ent2)
+    torch.cuda.synchronize()
+    mk = b.mask.numpy() != 0
+    lp_o, ent_o, lse_o = O.token_logprobs_from_logits(zm, b.ids, b.mask)
+    for name, g in (("fused", dl), ("separate", dl2)):
+        gd = cpu(g)
+        assert np.all(np.isfinite(gd)), name
+        assert np.all(gd[masked] == 0.0), name
+        assert rel_fro(gd, dl_o) <= TOL_GRAD_FRO, name
+    for x, ref_ in ((lpg, lp_o), (lp2, lp_o), (ent_f, ent_o), (ent2, ent_o), (lse2, lse_o)):
+        xv = cpu(x)
+        assert np.all(np.isfinite(xv[mk]))
+        np.testing.assert_allclose(xv[mk], ref_[mk], rtol=0, atol=2e-3)
+    for s in (R.stats_to_dict(st), R.stats_to_dict(st2)):
+        for k in ("loss", "entropy_loss"):
+            assert abs(s[k] - o["fwd"][k]) <= TOL_LOSS_REL * abs(o["fwd"][k]) + TOL_LOSS_ABS, k
