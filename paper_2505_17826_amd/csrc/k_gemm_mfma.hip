@@ -245,6 +245,10 @@ __device__ __forceinline__ uint32_t f16_bits(float f) {
 template <int EPI, bool TR = false>
 __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   constexpr bool kStats = EPI == EPI_STATS || EPI == EPI_STATS_Y;
+  // MFMA shape: the plain fp32-store GEMM with K-contiguous operands uses
+  // v_mfma_f32_16x16x32_bf16 (4 x 8 tiles of 16 x 16 per wave; measured 3-4%
+  // faster than 32x32x16 on the same main loop), the others 32x32x16.
+  constexpr bool kM16 = EPI == EPI_STORE && !TR;
   __shared__ __attribute__((aligned(16))) char lds[LDS_TOTAL];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -347,13 +351,21 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       }
     }
 
-    floatx16 acc[2][4];
+    floatx16 acc[kM16 ? 1 : 2][4];
+    floatx4 acc4[kM16 ? 4 : 1][8];
+    if constexpr (kM16) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 8; ++j) acc4[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
+    } else {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    }
 
     char* const ldsw = lds + (wid % NLOAD) * (TR ? 16 * 512 : (256 / NLOAD) * 128);
     // TR fragment offsets: lane (group half gi, K-half kh, j = K-row in 4, a = M quad)
@@ -381,6 +393,30 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       }
       const char* As = lds + (kt & 1) * STAGE;
       const char* Bs = As + A_BYTES;
+      if constexpr (kM16) {
+        // 16x16x32: lane l holds row (l & 15) of a fragment, K-chunk
+        // ks * 4 + (l >> 4) of the stage's eight 16-byte chunks
+        const int r16 = lane & 15, q4 = lane >> 4;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          bf16x8 a[4], b[8];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int row = wm * 64 + i * 16 + r16;
+            a[i] = *(const bf16x8*)(As + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
+          }
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int row = wn * 128 + j * 16 + r16;
+            b[j] = *(const bf16x8*)(Bs + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              acc4[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc4[i][j], 0, 0, 0);
+        }
+      } else
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int ch = ((ks * 2 + fh) ^ ((fr >> 1) & 7)) << 4;
@@ -609,6 +645,30 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
                        hv[i][j][e4]);
       __syncthreads();
       stage_copy_out(st, g.dz + (int64_t)m0 * g.ldz + n0, g.ldz, tid);
+    } else if constexpr (kM16) {  // EPI_STORE, 16x16 tiles
+      // element q of tile (i, j): row wm*64 + i*16 + (lane>>4)*4 + q,
+      // column wn*128 + j*16 + (lane & 15)
+      const int r16 = lane & 15, q4 = lane >> 4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int rl = wm * 64 + i * 16 + q4 * 4 + q;
+          const int m = m0 + rl;
+          if (m >= M) continue;
+          const int64_t dst = (int64_t)rp_i[rl] * g.ldc;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int col = n0 + wn * 128 + j * 16 + r16;
+            if (col < N) {
+              float v = acc4[i][j][q];
+              if (g.accumulate) v += g.C[dst + col];
+              g.C[dst + col] = v;
+            }
+          }
+        }
+      }
     } else {  // EPI_STORE
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
