@@ -131,17 +131,20 @@ __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_b
 // gradient reads dZ [rows, Vpad] and the compacted hidden rows [rows, d]
 // as they are, with no transposed copies).  A stage holds BK = 64 K-rows of
 // 256 M-values (512 B per row) for A, then the same for B; 16-byte chunk c of
-// K-row k sits at chunk c ^ (4 (k & 3)), so that the transposing fragment
-// reads (ds_read_b64_tr_b16: a 16-lane group reads 4 K-rows x 16 M-values and
-// each lane receives 4 consecutive K of one M) touch 16 distinct 16-byte bank
-// groups per half wave.  Loader wave w fills K-rows [16w, 16w + 16) of A and
-// B with 8 + 8 instructions of two rows each; lane l writes LDS chunk l of
-// its instruction (row l >> 5 of the pair, physical chunk l & 31), so it
-// loads logical chunk (l & 31) ^ 4 ((2 (p & 1) + (l >> 5)) & 3) of instruction
+// K-row k sits at chunk c ^ 4 (k & 3) ^ 2 ((k >> 3) & 1).  The fragments of
+// the 16x16x32 MFMA come from transposing reads (ds_read_b64_tr_b16: a
+// 16-lane group reads 4 K-rows x 16 M-values and each lane receives 4
+// consecutive K of one M); the two groups of a half wave read K-rows 8
+// apart, and with this swizzle the two touch disjoint halves of the 16
+// bank groups, so the reads are conflict-free.  Loader wave w fills K-rows
+// [16w, 16w + 16) of A and B with 8 + 8 instructions of two rows each; lane l
+// writes LDS chunk l of its instruction (row l >> 5 of the pair, physical
+// chunk l & 31), so it loads logical chunk
+// (l & 31) ^ 4 ((2 (p & 1) + (l >> 5)) & 3) ^ 2 ((p >> 2) & 1) of instruction
 // p.  The buffer descriptors are rebased on every K step (32-bit offsets) and
 // cover only the valid K-rows: rows past the count read as 0.
 struct LoadGeomTr {
-  uint32_t vA[2], vB[2];  // per-lane byte offsets for even / odd p, K-row 0 of the step
+  uint32_t vA[4], vB[4];  // per-lane byte offsets by (p & 1) | ((p >> 2) & 1) << 1, K-row 0
   uint32_t sA, sB;        // bytes per K-row
 };
 
@@ -154,17 +157,19 @@ __device__ __forceinline__ void load_stage_tr(const uint16_t* A, int64_t lda, co
 #pragma unroll
   for (int p = 0; p < 8; ++p)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_ptr)(dst + p * 1024), 16,
-                                             lg.vA[p & 1] + (uint32_t)p * 2u * lg.sA, 0, 0, 0);
+                                             lg.vA[(p & 1) | ((p >> 1) & 2)] +
+                                                 (uint32_t)p * 2u * lg.sA, 0, 0, 0);
 #pragma unroll
   for (int p = 0; p < 8; ++p)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES + p * 1024), 16,
-                                             lg.vB[p & 1] + (uint32_t)p * 2u * lg.sB, 0, 0, 0);
+                                             lg.vB[(p & 1) | ((p >> 1) & 2)] +
+                                                 (uint32_t)p * 2u * lg.sB, 0, 0, 0);
 }
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16* lds_v4i16;
 
-// MFMA operand fragment (32 rows of M or N, 16 K) from a TR tile: two
+// MFMA operand fragment (16 rows of M or N, 8 K per lane) from a TR tile: two
 // transposing reads of 4 K each; off = the lane's byte offset for the first.
 __device__ __forceinline__ bf16x8 frag_tr(const char* tile, uint32_t off) {
   const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(tile + off));
@@ -245,10 +250,11 @@ __device__ __forceinline__ uint32_t f16_bits(float f) {
 template <int EPI, bool TR = false>
 __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   constexpr bool kStats = EPI == EPI_STATS || EPI == EPI_STATS_Y;
-  // MFMA shape: the plain fp32-store GEMM with K-contiguous operands uses
+  // MFMA shape: the fp32-store GEMMs (dH; dW in the TR operand mode) use
   // v_mfma_f32_16x16x32_bf16 (4 x 8 tiles of 16 x 16 per wave; measured 3-4%
   // faster than 32x32x16 on the same main loop), the others 32x32x16.
-  constexpr bool kM16 = EPI == EPI_STORE && !TR;
+  constexpr bool kM16 = EPI == EPI_STORE;
+  static_assert(!TR || kM16, "the TR operand mode is built for the 16x16x32 MFMA");
   __shared__ __attribute__((aligned(16))) char lds[LDS_TOTAL];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -293,8 +299,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   if (TR) {
     const int r = (wid % NLOAD) * 16 + (lane >> 5);
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int c = (lane & 31) ^ (4 * ((2 * q + (lane >> 5)) & 3));
+    for (int q = 0; q < 4; ++q) {
+      const int c = (lane & 31) ^ (4 * ((2 * (q & 1) + (lane >> 5)) & 3)) ^ (q & 2);
       lt.vA[q] = (uint32_t)(r * g.lda * 2 + (int64_t)mt * BM * 2 + c * 16);
       lt.vB[q] = (uint32_t)(r * g.ldb * 2 + (int64_t)nt * BN * 2 + c * 16);
     }
@@ -368,17 +374,21 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     }
 
     char* const ldsw = lds + (wid % NLOAD) * (TR ? 16 * 512 : (256 / NLOAD) * 128);
-    // TR fragment offsets: lane (group half gi, K-half kh, j = K-row in 4, a = M quad)
-    uint32_t oA[2], oB[4];
+    // TR fragment offsets (16x16x32): lane l of 16-lane group g = l >> 4 reads
+    // K-row g*8 + jr (jr = (l >> 2) & 3) and M-values 4 aq .. 4 aq + 3
+    // (aq = l & 3) of the fragment's 16; the transposed result gives lane l
+    // the 4 consecutive K of M-value l & 15.
+    uint32_t oA[4], oB[8];
     if (TR) {
-      const int gi = (lane >> 4) & 1, kh = lane >> 5, j = (lane >> 2) & 3, aq = lane & 3;
-      const uint32_t kb = (uint32_t)(kh * 8 + j) * 512u + (uint32_t)((aq & 1) * 8);
+      const int gq = lane >> 4, jr = (lane >> 2) & 3, aq = lane & 3;
+      const uint32_t kb = (uint32_t)(gq * 8 + jr) * 512u + (uint32_t)((aq & 1) * 8);
+      const int sw = 4 * jr + 2 * (gq & 1);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        oA[i] = kb + ((((wm * 64 + i * 32 + gi * 16 + 4 * aq) >> 3) ^ (4 * j)) << 4);
+      for (int i = 0; i < 4; ++i)
+        oA[i] = kb + (((((wm * 64 + i * 16) >> 3) + (aq >> 1)) ^ sw) << 4);
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
-        oB[jj] = kb + ((((wn * 128 + jj * 32 + gi * 16 + 4 * aq) >> 3) ^ (4 * j)) << 4);
+      for (int jj = 0; jj < 8; ++jj)
+        oB[jj] = kb + (((((wn * 128 + jj * 16) >> 3) + (aq >> 1)) ^ sw) << 4);
     }
     if (nk > 0 && loader) {
       if (TR) load_stage_tr(g.A, g.lda, g.B, g.ldb, 0, Kv, ldsw, lt);
@@ -400,15 +410,22 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           bf16x8 a[4], b[8];
+          if (TR) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int row = wm * 64 + i * 16 + r16;
-            a[i] = *(const bf16x8*)(As + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
-          }
+            for (int i = 0; i < 4; ++i) a[i] = frag_tr(As, oA[i] + ks * 32 * 512);
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int row = wn * 128 + j * 16 + r16;
-            b[j] = *(const bf16x8*)(Bs + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
+            for (int j = 0; j < 8; ++j) b[j] = frag_tr(Bs, oB[j] + ks * 32 * 512);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = wm * 64 + i * 16 + r16;
+              a[i] = *(const bf16x8*)(As + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              const int row = wn * 128 + j * 16 + r16;
+              b[j] = *(const bf16x8*)(Bs + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
+            }
           }
 #pragma unroll
           for (int i = 0; i < 4; ++i)
@@ -421,17 +438,10 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       for (int ks = 0; ks < 4; ++ks) {
         const int ch = ((ks * 2 + fh) ^ ((fr >> 1) & 7)) << 4;
         bf16x8 a[2], b[4];
-        if (TR) {
 #pragma unroll
-          for (int i = 0; i < 2; ++i) a[i] = frag_tr(As, oA[i] + ks * 16 * 512);
+        for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(As + (wm * 64 + i * 32 + fr) * 128 + ch);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) b[j] = frag_tr(Bs, oB[j] + ks * 16 * 512);
-        } else {
-#pragma unroll
-          for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(As + (wm * 64 + i * 32 + fr) * 128 + ch);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Bs + (wn * 128 + j * 32 + fr) * 128 + ch);
-        }
+        for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Bs + (wn * 128 + j * 32 + fr) * 128 + ch);
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
