@@ -250,10 +250,11 @@ __device__ __forceinline__ uint32_t f16_bits(float f) {
 template <int EPI, bool TR = false>
 __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   constexpr bool kStats = EPI == EPI_STATS || EPI == EPI_STATS_Y;
-  // MFMA shape: the fp32-store GEMMs (dH; dW in the TR operand mode) use
-  // v_mfma_f32_16x16x32_bf16 (4 x 8 tiles of 16 x 16 per wave; measured 3-4%
-  // faster than 32x32x16 on the same main loop), the others 32x32x16.
-  constexpr bool kM16 = EPI == EPI_STORE;
+  // MFMA shape: the forward and fp32-store GEMMs (forward statistics, dH; dW
+  // in the TR operand mode) use v_mfma_f32_16x16x32_bf16 (4 x 8 tiles of
+  // 16 x 16 per wave; measured 3-4% faster than 32x32x16 on the same main
+  // loop), the recomputing dZ GEMM 32x32x16.
+  constexpr bool kM16 = EPI == EPI_STORE || kStats;
   static_assert(!TR || kM16, "the TR operand mode is built for the 16x16x32 MFMA");
   __shared__ __attribute__((aligned(16))) char lds[LDS_TOTAL];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -460,145 +461,143 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     // accumulator element e of tile (i, j): row = wm*64 + i*32 + (e>>2)*8 + fh*4 + (e&3),
     //                                       col = wn*128 + j*32 + fr
     const int colb = n0 + wn * 128 + fr;
-    if (kStats) {
+    if constexpr (kStats) {
+      // 16x16 tiles: element q of tile (i, j) is row wm*64 + i*16 + (lane>>4)*4 + q,
+      // column wn*128 + j*16 + (lane & 15).  A lane holds 16 rows (e = 4 i + q)
+      // of its 16-lane group, 8 columns each; a row's 128 columns of this wave
+      // lie in the 16 lanes of one DPP row.
       float* xm = (float*)lds;           // cross-wave exchange [256 rows][3]
       float* mrow = (float*)(lds + 3072);  // row maximum over the tile [256]
-      bool cv[4];
+      const int r16 = lane & 15, q4 = lane >> 4;
+      const int colb16 = n0 + wn * 128 + r16;
+      bool cv[8];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) cv[j] = colb + j * 32 < N;
+      for (int j = 0; j < 8; ++j) cv[j] = colb16 + j * 16 < N;
       // tiles wholly inside N (all but at most the last column of tiles) skip
       // the column masks; the exponent is the hardware exp2 (arguments <= 0,
       // results below 2^-126 flush to 0)
       const bool full = n0 + BN <= N;
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        __builtin_amdgcn_sched_barrier(0);  // keep the accumulator reads of one tile row together
-        float mx[16], sm[16], um[16];
-        if (full) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            mx[e] = fmaxf(fmaxf(acc[i][0][e], acc[i][1][e]), fmaxf(acc[i][2][e], acc[i][3][e]));
-        } else {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            float v = -INFINITY;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) v = cv[j] ? fmaxf(v, acc[i][j][e]) : v;
-            mx[e] = v;
-          }
-        }
-        half_max_n(mx);
-        if (full) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            float s = 0.f, u = 0.f;
-            const float mk = mx[e] * kLog2e;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const float z = acc[i][j][e];
-              const float p = __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mk));
-              s += p;
-              u = fmaf(p, z, u);
-            }
-            sm[e] = s;
-            um[e] = u;
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            float s = 0.f, u = 0.f;
-            const float mk = mx[e] == -INFINITY ? 0.f : mx[e] * kLog2e;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const float z = acc[i][j][e];
-              const float p = cv[j] ? __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mk)) : 0.f;
-              s += p;
-              u = cv[j] ? fmaf(p, z, u) : u;
-            }
-            sm[e] = s;
-            um[e] = u;
-          }
-        }
-        half_sum_n(sm);
-        half_sum_n(um);
-        // logit of the sampled token
+      __builtin_amdgcn_sched_barrier(0);
+      float mx[16], sm[16], um[16];
+      if (full) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          int rl = wm * 64 + i * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
-          int y = rp_i[rl];
-          int yl = y - (n0 + wn * 128);
-          // the value is picked with selects outside the store's branch, so
-          // no register copies of the accumulator tiles are made there
-          const int jj = yl >> 5;
-          float z = acc[i][0][e];
-          z = jj == 1 ? acc[i][1][e] : z;
-          z = jj == 2 ? acc[i][2][e] : z;
-          z = jj == 3 ? acc[i][3][e] : z;
-          if (yl >= 0 && yl < 128 && (yl & 31) == fr) g.zy[g.rows_off + m0 + rl] = z;
+          const floatx4* t = acc4[e >> 2];
+          const int q = e & 3;
+          mx[e] = fmaxf(fmaxf(fmaxf(t[0][q], t[1][q]), fmaxf(t[2][q], t[3][q])),
+                        fmaxf(fmaxf(t[4][q], t[5][q]), fmaxf(t[6][q], t[7][q])));
         }
-        // lane (fr) < 16 owns row e = fr of its half
-        float om = mx[0], os = sm[0], ou = um[0];
+      } else {
 #pragma unroll
-        for (int e = 1; e < 16; ++e) {
-          bool sel = (fr & 15) == e;
-          om = sel ? mx[e] : om;
-          os = sel ? sm[e] : os;
-          ou = sel ? um[e] : ou;
+        for (int e = 0; e < 16; ++e) {
+          float v = -INFINITY;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v = cv[j] ? fmaxf(v, acc4[e >> 2][j][e & 3]) : v;
+          mx[e] = v;
         }
-        const int e_own = fr & 15;
-        const int rl = wm * 64 + i * 32 + (e_own >> 2) * 8 + fh * 4 + (e_own & 3);
-        if (wn == 1 && fr < 16) {
-          xm[rl * 3 + 0] = om;
-          xm[rl * 3 + 1] = os;
-          xm[rl * 3 + 2] = ou;
-        }
-        __syncthreads();
-        if (wn == 0 && fr < 16) {
-          int m = m0 + rl;
-          float mt = 0.f;
-          if (m < M) {
-            lse_merge(om, os, ou, xm[rl * 3 + 0], xm[rl * 3 + 1], xm[rl * 3 + 2]);
-            int64_t o = (int64_t)nt * g.ldp + g.p_off + m;
-            g.pm[o] = om;
-            g.ps[o] = os;
-            g.pu[o] = ou;
-            mt = om;
-          }
-          if (EPI == EPI_STATS_Y) mrow[rl] = mt;
-        }
-        __syncthreads();
       }
+      row16_max_n(mx);
+      if (full) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          float s0 = 0.f, u0 = 0.f;
+          const float mk = mx[e] * kLog2e;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float z = acc4[e >> 2][j][e & 3];
+            const float p = __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mk));
+            s0 += p;
+            u0 = fmaf(p, z, u0);
+          }
+          sm[e] = s0;
+          um[e] = u0;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          float s0 = 0.f, u0 = 0.f;
+          const float mk = mx[e] == -INFINITY ? 0.f : mx[e] * kLog2e;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float z = acc4[e >> 2][j][e & 3];
+            const float p = cv[j] ? __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mk)) : 0.f;
+            s0 += p;
+            u0 = cv[j] ? fmaf(p, z, u0) : u0;
+          }
+          sm[e] = s0;
+          um[e] = u0;
+        }
+      }
+      row16_sum_n(sm);
+      row16_sum_n(um);
+      // logit of the sampled token, picked with selects outside the store's
+      // branch (a dynamic index there makes the compiler copy the tiles)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int rl = wm * 64 + (e >> 2) * 16 + q4 * 4 + (e & 3);
+        const int yl = rp_i[rl] - (n0 + wn * 128);
+        const int jj = yl >> 4;
+        float z = acc4[e >> 2][0][e & 3];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) z = jj == j ? acc4[e >> 2][j][e & 3] : z;
+        if (yl >= 0 && yl < 128 && (yl & 15) == r16) g.zy[g.rows_off + m0 + rl] = z;
+      }
+      // lane r16 of group q4 owns row e = r16 of that group
+      float om = mx[0], os = sm[0], ou = um[0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) {
+        const bool sel = r16 == e;
+        om = sel ? mx[e] : om;
+        os = sel ? sm[e] : os;
+        ou = sel ? um[e] : ou;
+      }
+      const int rl = wm * 64 + (r16 >> 2) * 16 + q4 * 4 + (r16 & 3);
+      if (wn == 1) {
+        xm[rl * 3 + 0] = om;
+        xm[rl * 3 + 1] = os;
+        xm[rl * 3 + 2] = ou;
+      }
+      __syncthreads();
+      if (wn == 0) {
+        const int m = m0 + rl;
+        float mt = 0.f;
+        if (m < M) {
+          lse_merge(om, os, ou, xm[rl * 3 + 0], xm[rl * 3 + 1], xm[rl * 3 + 2]);
+          const int64_t o = (int64_t)nt * g.ldp + g.p_off + m;
+          g.pm[o] = om;
+          g.ps[o] = os;
+          g.pu[o] = ou;
+          mt = om;
+        }
+        if (EPI == EPI_STATS_Y) mrow[rl] = mt;
+      }
+      __syncthreads();
       if (EPI == EPI_STATS_Y) {
         // y = z - (row maximum over the tile) <= 0, rounded to fp16; rows past
         // M and columns past N hold values the backward never uses
-        uint2 hv[2][4][4];
+        uint2 hv[4][8];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 4; ++i) {
+          const int rl0 = wm * 64 + i * 16 + q4 * 4;
+          float mr[4];
 #pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4) {
-            const int rl0 = wm * 64 + i * 32 + e4 * 8 + fh * 4;
-            float mr[4];
+          for (int q = 0; q < 4; ++q) mr[q] = mrow[rl0 + q];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) mr[q] = mrow[rl0 + q];
+          for (int j = 0; j < 8; ++j) {
+            uint32_t hb[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              uint32_t hb[4];
-#pragma unroll
-              for (int q = 0; q < 4; ++q) hb[q] = f16_bits(acc[i][j][e4 * 4 + q] - mr[q]);
-              hv[i][j][e4].x = hb[0] | (hb[1] << 16);
-              hv[i][j][e4].y = hb[2] | (hb[3] << 16);
-            }
+            for (int q = 0; q < 4; ++q) hb[q] = f16_bits(acc4[i][j][q] - mr[q]);
+            hv[i][j].x = hb[0] | (hb[1] << 16);
+            hv[i][j].y = hb[2] | (hb[3] << 16);
           }
+        }
         __syncthreads();  // the staging tile overlaps xm and mrow
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int e4 = 0; e4 < 4; ++e4)
-              stage_col4(lds + (wm * 64 + i * 32 + e4 * 8 + fh * 4) * STG_PITCH +
-                             (wn * 128 + j * 32 + fr) * 2,
-                         hv[i][j][e4]);
+          for (int j = 0; j < 8; ++j)
+            stage_col4(lds + (wm * 64 + i * 16 + q4 * 4) * STG_PITCH + (wn * 128 + j * 16 + r16) * 2,
+                       hv[i][j]);
         __syncthreads();
         stage_copy_out(lds, g.y + (int64_t)m0 * g.ldy + n0, g.ldy, tid);
       }

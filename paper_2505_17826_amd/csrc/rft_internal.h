@@ -89,6 +89,31 @@ __device__ __forceinline__ void half_sum_n(float (&v)[N]) {
   for (int e = 0; e < N; ++e) v[e] += swz16_f(v[e]);
 }
 
+// Reductions over the 16 lanes of each DPP row (four butterfly steps), over N
+// independent values at a time; every lane of the row ends with the result.
+template <int N>
+__device__ __forceinline__ void row16_max_n(float (&v)[N]) {
+#pragma unroll
+  for (int e = 0; e < N; ++e) v[e] = fmaxf(v[e], dpp_f<0xB1>(v[e]));
+#pragma unroll
+  for (int e = 0; e < N; ++e) v[e] = fmaxf(v[e], dpp_f<0x4E>(v[e]));
+#pragma unroll
+  for (int e = 0; e < N; ++e) v[e] = fmaxf(v[e], dpp_f<0x141>(v[e]));
+#pragma unroll
+  for (int e = 0; e < N; ++e) v[e] = fmaxf(v[e], dpp_f<0x140>(v[e]));
+}
+template <int N>
+__device__ __forceinline__ void row16_sum_n(float (&v)[N]) {
+#pragma unroll
+  for (int e = 0; e < N; ++e) v[e] += dpp_f<0xB1>(v[e]);
+#pragma unroll
+  for (int e = 0; e < N; ++e) v[e] += dpp_f<0x4E>(v[e]);
+#pragma unroll
+  for (int e = 0; e < N; ++e) v[e] += dpp_f<0x141>(v[e]);
+#pragma unroll
+  for (int e = 0; e < N; ++e) v[e] += dpp_f<0x140>(v[e]);
+}
+
 // Whole-wave (64 lanes) reductions via cross-lane shuffles.
 __device__ __forceinline__ double wave_sum_d(double v) {
 #pragma unroll
