@@ -2,7 +2,7 @@
 //   C[m, n] = sum_k A[m, k] * B[n, k]   (both operands K-contiguous, bf16)
 // 256x256 workgroup tile, BK = 64, eight wavefronts (two per SIMD, so one
 // wave's LDS and barrier waits overlap the other's MFMAs), each owning 64x128
-// of C as 2x4 v_mfma_f32_32x32x16_bf16 tiles (fp32 accumulators).  Operands go
+// of C as 4x8 v_mfma_f32_16x16x32_bf16 tiles (fp32 accumulators).  Operands go
 // straight from HBM/L2 into LDS with buffer_load_dwordx4 ... lds (no staging
 // registers), issued by four of the eight waves; the buffer descriptor covers only the tile's valid rows, so rows
 // past the end and the K tail read as zeros without branches.  LDS holds
@@ -250,12 +250,6 @@ __device__ __forceinline__ uint32_t f16_bits(float f) {
 template <int EPI, bool TR = false>
 __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   constexpr bool kStats = EPI == EPI_STATS || EPI == EPI_STATS_Y;
-  // MFMA shape: the forward and fp32-store GEMMs (forward statistics, dH; dW
-  // in the TR operand mode) use v_mfma_f32_16x16x32_bf16 (4 x 8 tiles of
-  // 16 x 16 per wave; measured 3-4% faster than 32x32x16 on the same main
-  // loop), the recomputing dZ GEMM 32x32x16.
-  constexpr bool kM16 = EPI == EPI_STORE || kStats;
-  static_assert(!TR || kM16, "the TR operand mode is built for the 16x16x32 MFMA");
   __shared__ __attribute__((aligned(16))) char lds[LDS_TOTAL];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -308,8 +302,12 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     lt.sA = (uint32_t)(g.lda * 2);
     lt.sB = (uint32_t)(g.ldb * 2);
   }
-  // per-lane MFMA operand offsets (row = base + (lane&31), chunk = ks*2 + (lane>>5))
-  const int fr = lane & 31, fh = lane >> 5;
+  // MFMA tiles: v_mfma_f32_16x16x32_bf16, 4 x 8 tiles of 16 x 16 per wave
+  // (measured 3-4% faster than 4 x 2 tiles of 32x32x16 on the same main loop,
+  // and the forward's row reductions stay inside one 16-lane DPP row).
+  // Element q of tile (i, j) is row wm*64 + i*16 + q4*4 + q and column
+  // wn*128 + j*16 + r16 of the workgroup tile.
+  const int r16 = lane & 15, q4 = lane >> 4;
 
   int32_t* rp_i = (int32_t*)(lds + 2 * STAGE);
   float* rp_a = (float*)(lds + 2 * STAGE + BM * 4);
@@ -358,21 +356,11 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       }
     }
 
-    floatx16 acc[kM16 ? 1 : 2][4];
-    floatx4 acc4[kM16 ? 4 : 1][8];
-    if constexpr (kM16) {
+    floatx4 acc4[4][8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc4[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
-    } else {
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-    }
+      for (int j = 0; j < 8; ++j) acc4[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
 
     char* const ldsw = lds + (wid % NLOAD) * (TR ? 16 * 512 : (256 / NLOAD) * 128);
     // TR fragment offsets (16x16x32): lane l of 16-lane group g = l >> 4 reads
@@ -404,10 +392,9 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       }
       const char* As = lds + (kt & 1) * STAGE;
       const char* Bs = As + A_BYTES;
-      if constexpr (kM16) {
-        // 16x16x32: lane l holds row (l & 15) of a fragment, K-chunk
-        // ks * 4 + (l >> 4) of the stage's eight 16-byte chunks
-        const int r16 = lane & 15, q4 = lane >> 4;
+      {
+        // lane l holds row (l & 15) of a fragment and K-chunk ks * 4 + (l >> 4)
+        // of the stage's eight 16-byte chunks
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           bf16x8 a[4], b[8];
@@ -434,20 +421,6 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
             for (int j = 0; j < 8; ++j)
               acc4[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc4[i][j], 0, 0, 0);
         }
-      } else
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int ch = ((ks * 2 + fh) ^ ((fr >> 1) & 7)) << 4;
-        bf16x8 a[2], b[4];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(As + (wm * 64 + i * 32 + fr) * 128 + ch);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Bs + (wn * 128 + j * 32 + fr) * 128 + ch);
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
       }
       // Before the barrier: this wave's loads of the next stage have landed
       // and its fragment reads of this stage are complete, so after the
@@ -458,17 +431,11 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     }
 
     // ------------------------------------------------------------ epilogue
-    // accumulator element e of tile (i, j): row = wm*64 + i*32 + (e>>2)*8 + fh*4 + (e&3),
-    //                                       col = wn*128 + j*32 + fr
-    const int colb = n0 + wn * 128 + fr;
     if constexpr (kStats) {
-      // 16x16 tiles: element q of tile (i, j) is row wm*64 + i*16 + (lane>>4)*4 + q,
-      // column wn*128 + j*16 + (lane & 15).  A lane holds 16 rows (e = 4 i + q)
-      // of its 16-lane group, 8 columns each; a row's 128 columns of this wave
-      // lie in the 16 lanes of one DPP row.
+      // A lane holds 16 rows (e = 4 i + q) of its 16-lane group, 8 columns
+      // each; a row's 128 columns of this wave lie in the 16 lanes of one DPP row.
       float* xm = (float*)lds;           // cross-wave exchange [256 rows][3]
       float* mrow = (float*)(lds + 3072);  // row maximum over the tile [256]
-      const int r16 = lane & 15, q4 = lane >> 4;
       const int colb16 = n0 + wn * 128 + r16;
       bool cv[8];
 #pragma unroll
@@ -604,38 +571,35 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     } else if (EPI == EPI_DZ) {
       // d = c (onehot - p) + e p (z - mu) in bf16, packed per lane as four
       // consecutive rows of one column
-      uint2 hv[2][4][4];
+      uint2 hv[4][8];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_barrier(0);
+        const int rl0 = wm * 64 + i * 16 + q4 * 4;
+        float Lr[4], cr[4], er[4], ur[4];
+        int yr[4];
 #pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          __builtin_amdgcn_sched_barrier(0);
-          const int rl0 = wm * 64 + i * 32 + e4 * 8 + fh * 4;
-          float Lr[4], cr[4], er[4], ur[4];
-          int yr[4];
+        for (int q = 0; q < 4; ++q) {
+          yr[q] = rp_i[rl0 + q];
+          Lr[q] = rp_a[rl0 + q] * kLog2e;
+          cr[q] = rp_b[rl0 + q];
+          er[q] = rp_e[rl0 + q];
+          ur[q] = rp_u[rl0 + q];
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int col = n0 + wn * 128 + j * 16 + r16;
+          const bool cvalid = col < g.Vvalid;
+          uint32_t hb[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            yr[q] = rp_i[rl0 + q];
-            Lr[q] = rp_a[rl0 + q] * kLog2e;
-            cr[q] = rp_b[rl0 + q];
-            er[q] = rp_e[rl0 + q];
-            ur[q] = rp_u[rl0 + q];
+            const float z = acc4[i][j][q];
+            const float p = __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -Lr[q]));
+            const float d = dlogit(cr[q], er[q], ur[q], p, z, col == yr[q]);
+            hb[q] = f32_to_bf16(cvalid ? d : 0.f);
           }
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int col = colb + j * 32;
-            const bool cvalid = col < g.Vvalid;
-            uint32_t hb[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              float z = acc[i][j][e4 * 4 + q];
-              float p = exp2f(z * kLog2e - Lr[q]);
-              float d = dlogit(cr[q], er[q], ur[q], p, z, col == yr[q]);
-              hb[q] = f32_to_bf16(cvalid ? d : 0.f);
-            }
-            hv[i][j][e4].x = hb[0] | (hb[1] << 16);
-            hv[i][j][e4].y = hb[2] | (hb[3] << 16);
-          }
+          hv[i][j].x = hb[0] | (hb[1] << 16);
+          hv[i][j].y = hb[2] | (hb[3] << 16);
         }
       }
       // Stage the tile through LDS and write it with 16-byte stores that
@@ -644,20 +608,14 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       __syncthreads();  // every wave is done with the stages and the row parameters
       // dZ [rows, Vpad]: element (row, col) at byte row * pitch + col * 2
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4)
-            stage_col4(st + (wm * 64 + i * 32 + e4 * 8 + fh * 4) * STG_PITCH +
-                           (wn * 128 + j * 32 + fr) * 2,
-                       hv[i][j][e4]);
+        for (int j = 0; j < 8; ++j)
+          stage_col4(st + (wm * 64 + i * 16 + q4 * 4) * STG_PITCH + (wn * 128 + j * 16 + r16) * 2,
+                     hv[i][j]);
       __syncthreads();
       stage_copy_out(st, g.dz + (int64_t)m0 * g.ldz + n0, g.ldz, tid);
-    } else if constexpr (kM16) {  // EPI_STORE, 16x16 tiles
-      // element q of tile (i, j): row wm*64 + i*16 + (lane>>4)*4 + q,
-      // column wn*128 + j*16 + (lane & 15)
-      const int r16 = lane & 15, q4 = lane >> 4;
+    } else {  // EPI_STORE
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         __builtin_amdgcn_sched_barrier(0);
@@ -672,27 +630,6 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
             const int col = n0 + wn * 128 + j * 16 + r16;
             if (col < N) {
               float v = acc4[i][j][q];
-              if (g.accumulate) v += g.C[dst + col];
-              g.C[dst + col] = v;
-            }
-          }
-        }
-      }
-    } else {  // EPI_STORE
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int rl = wm * 64 + i * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
-          const int m = m0 + rl;
-          if (m >= M) continue;
-          const int64_t dst = (int64_t)rp_i[rl] * g.ldc;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int col = colb + j * 32;
-            if (col < N) {
-              float v = acc[i][j][e];
               if (g.accumulate) v += g.C[dst + col];
               g.C[dst + col] = v;
             }

@@ -30,63 +30,13 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 }
 
 // ------------------------------------------------------- wave reductions --
-// Butterfly reductions over the 32 lanes of each half-wave (lanes 0-31 and
-// 32-63 reduce separately) with DPP moves and one swizzle; every lane of the
-// half ends with the result. The DPP patterns used are permutations within a
-// row (every lane has a source), so bound_ctrl changes no value; setting it
-// lets the compiler fold the move into the add or max that uses it.
+// DPP move within a row of 16 lanes.  The patterns used here are
+// permutations within the row (every lane has a source), so bound_ctrl
+// changes no value; setting it lets the compiler fold the move into the add
+// or max that uses it.
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
-}
-__device__ __forceinline__ float swz16_f(float v) {  // lane ^ 16 within 32
-  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F));
-}
-__device__ __forceinline__ float half_max(float v) {
-  v = fmaxf(v, dpp_f<0xB1>(v));   // quad_perm [1,0,3,2]
-  v = fmaxf(v, dpp_f<0x4E>(v));   // quad_perm [2,3,0,1]
-  v = fmaxf(v, dpp_f<0x141>(v));  // row_half_mirror
-  v = fmaxf(v, dpp_f<0x140>(v));  // row_mirror
-  v = fmaxf(v, swz16_f(v));
-  return v;
-}
-__device__ __forceinline__ float half_sum(float v) {
-  v += dpp_f<0xB1>(v);
-  v += dpp_f<0x4E>(v);
-  v += dpp_f<0x141>(v);
-  v += dpp_f<0x140>(v);
-  v += swz16_f(v);
-  return v;
-}
-
-// The same reductions over N independent values, one butterfly step at a time
-// across all of them, so consecutive DPP operations never depend on each
-// other (no wait states between a result and its DPP read).
-template <int N>
-__device__ __forceinline__ void half_max_n(float (&v)[N]) {
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] = fmaxf(v[e], dpp_f<0xB1>(v[e]));
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] = fmaxf(v[e], dpp_f<0x4E>(v[e]));
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] = fmaxf(v[e], dpp_f<0x141>(v[e]));
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] = fmaxf(v[e], dpp_f<0x140>(v[e]));
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] = fmaxf(v[e], swz16_f(v[e]));
-}
-template <int N>
-__device__ __forceinline__ void half_sum_n(float (&v)[N]) {
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] += dpp_f<0xB1>(v[e]);
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] += dpp_f<0x4E>(v[e]);
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] += dpp_f<0x141>(v[e]);
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] += dpp_f<0x140>(v[e]);
-#pragma unroll
-  for (int e = 0; e < N; ++e) v[e] += swz16_f(v[e]);
 }
 
 // Reductions over the 16 lanes of each DPP row (four butterfly steps), over N
