@@ -69,8 +69,8 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--ws-gb", type=float, default=0.0,
                     help="workspace of the fused step in GB (default 0: the library's "
-                         "recommended size, chunks of up to 131072 rows); a larger workspace "
-                         "means fewer, larger row chunks")
+                         "recommended size); the step takes the largest row chunk that fits, "
+                         "so a smaller workspace means more, smaller chunks")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GB",
                     help="only run a plain device copy of GB gigabytes (the known-size kernel "
                          "that scales the HBM byte counters) and exit")
@@ -224,7 +224,7 @@ def main():
                              dtype=torch.uint8, device=dev)
         ws_step_bytes = R.workspace_bytes(R.RFT_OP_PPO_STEP, tok, d, V, dt)
         if args.ws_gb > 0:
-            ws_step_bytes = max(ws_step_bytes, int(args.ws_gb * 1e9))
+            ws_step_bytes = int(args.ws_gb * 1e9)
         ws_step = torch.empty(ws_step_bytes, dtype=torch.uint8, device=dev)
         # rollout-side log-probs for the old / reference policies (setup, untimed)
         R.rft_token_logprobs(tok, b.H, b.W, logp=logp, entropy=ent, lse=lse, ws=ws_fwd)

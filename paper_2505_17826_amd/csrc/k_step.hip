@@ -9,7 +9,10 @@
 //   k_dz_from_y   dZ = c_t (onehot(y_t) - p) + e_t p (z - mu_t) from the fp16
 //                 y = z - (row maximum over the 256-column tile) that the
 //                 forward GEMM stored, written in place as bf16 [Tc, Vpad]
-//                 (both backward GEMMs read this one layout).
+//                 (the dH GEMM's operand) and transposed, [Vpad, Tc] (the dW
+//                 GEMM's, K-contiguous);
+//   k_transpose_hc  the chunk's compacted hidden rows transposed, [d, Tc]
+//                 (the dW GEMM's other operand).
 // The arithmetic of k_step_rows is that of k_merge_rows and k_loss_fwd (same
 // merge order, same per-token formula), so the step and the separate calls
 // give the same log-probs and gradients bit for bit.
@@ -61,9 +64,14 @@ __global__ void __launch_bounds__(256) k_step_rows(
 // One 512-thread workgroup per 256 x 256 tile of the chunk.  Thread tid owns
 // the 8 x 8 blocks (row block rb, column block cb) with cb = tid % 32 and
 // rb = tid / 32 and tid / 32 + 16: it reads eight 16-byte row pieces (a wave
-// reads two 512-byte rows per instruction) and writes dZ back in place.
-// Tiles wholly past the chunk's count are skipped (the backward GEMMs read
-// rows only up to the count).
+// reads two 512-byte rows per instruction) and writes dZ back in place.  The
+// transposed copy is staged in LDS (column c of the tile as a 512-byte row,
+// its 16-byte chunk j at chunk j ^ ((c >> 3) & 15): the 32 lanes writing one
+// column position of 32 blocks hit 16 distinct bank groups) and leaves as
+// 16-byte stores, a wave writing two 512-byte rows of dZ^T per instruction.
+// Rows of the last tile past the count are written as 0 in both layouts (the
+// dW GEMM reads K up to the next multiple of 64).  Tiles wholly past the
+// chunk's count are skipped (the backward GEMMs read rows only up to the count).
 constexpr int kDzT = 512;
 
 __device__ __forceinline__ uint32_t bf16_bits(float f) { return (uint32_t)f32_to_bf16(f); }
@@ -73,9 +81,10 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
     const int32_t* __restrict__ rows, const int32_t* __restrict__ ids,
     const int32_t* __restrict__ meta, int64_t c0, const float* __restrict__ pm,
     const float* __restrict__ lse, const float* __restrict__ grad, const float* __restrict__ ce,
-    const float* __restrict__ cmu, int ntc) {
+    const float* __restrict__ cmu, int ntc, uint16_t* __restrict__ dzt, int64_t ldt) {
   __shared__ float rL[256], rC[256], rM[256], rE[256], rD[256];
   __shared__ int rY[256];
+  __shared__ __attribute__((aligned(16))) uint16_t stT[256 * 256];  // [tile column][tile row]
   const int tid = threadIdx.x;
   const int nt = (int)(blockIdx.x % ntc), mt = (int)(blockIdx.x / ntc);
   int64_t count = (int64_t)meta[0] - c0;
@@ -112,6 +121,7 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
     const int rb = (tid >> 5) + 16 * h;
     uint16_t* src = yz + (r0 + rb * 8) * Vpad + n0 + cb * 8;
     uint4 in[8];
+    uint32_t tcol[8][4];  // column q of the block: its 8 rows as bf16 pairs
 #pragma unroll
     for (int r = 0; r < 8; ++r) in[r] = *(const uint4*)(src + r * Vpad);
 #pragma unroll
@@ -134,12 +144,53 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
           const float p = exp2f(fmaf(yv, kLog2e, Mk - Lk));
           float d = dlogit(Ck, Ek, -Dk, p, yv, col == (int64_t)Yk);
           d = (rv && col < V) ? d : 0.f;
-          pair |= bf16_bits(d) << (hh * 16);
+          const uint32_t b = bf16_bits(d);
+          pair |= b << (hh * 16);
+          if (r & 1) tcol[q][r >> 1] |= b << 16;
+          else tcol[q][r >> 1] = b;
         }
         o[q2] = pair;
       }
       *(uint4*)(src + r * Vpad) = make_uint4(o[0], o[1], o[2], o[3]);
     }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int c = cb * 8 + q;
+      *(uint4*)(stT + c * 256 + ((rb ^ (cb & 15)) << 3)) =
+          make_uint4(tcol[q][0], tcol[q][1], tcol[q][2], tcol[q][3]);
+    }
+  }
+  __syncthreads();
+  // dZ^T rows n0 .. n0 + 255, columns r0 .. r0 + 255
+#pragma unroll 4
+  for (int it = 0; it < 16; ++it) {
+    const int i = it * kDzT + tid, c = i >> 5, j = i & 31;
+    const uint4 v = *(const uint4*)(stT + c * 256 + ((j ^ ((c >> 3) & 15)) << 3));
+    *(uint4*)(dzt + (n0 + c) * ldt + r0 + j * 8) = v;
+  }
+}
+
+// Hc^T [d, ldt] of the chunk's compacted hidden rows [c0, c0 + count): 64 x 64
+// tiles through LDS; columns count .. (next multiple of 256) are written as 0.
+__global__ void __launch_bounds__(256) k_transpose_hc(const uint16_t* __restrict__ hc, int64_t d,
+                                                      const int32_t* __restrict__ meta, int64_t c0,
+                                                      int64_t Tc, uint16_t* __restrict__ hct,
+                                                      int64_t ldt) {
+  __shared__ uint16_t t[64][66];
+  int64_t count = (int64_t)meta[0] - c0;
+  count = count < 0 ? 0 : (count > Tc ? Tc : count);
+  const int64_t kend = (count + 255) / 256 * 256;
+  const int64_t k0 = (int64_t)blockIdx.x * 64, j0 = (int64_t)blockIdx.y * 64;
+  if (k0 >= kend) return;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int r = ty; r < 64; r += 4) {
+    const int64_t k = k0 + r, j = j0 + tx;
+    t[r][tx] = (k < count && j < d) ? hc[(c0 + k) * d + j] : (uint16_t)0;
+  }
+  __syncthreads();
+  for (int r = ty; r < 64; r += 4) {
+    const int64_t j = j0 + r, k = k0 + tx;
+    if (j < d) hct[j * ldt + k] = t[tx][r];
   }
 }
 
@@ -157,11 +208,19 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
 hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
                             const int32_t* rows, const int32_t* ids, const int32_t* meta,
                             int64_t c0, const float* pm, const float* lse, const float* grad,
-                            const float* ce, const float* cmu, hipStream_t s) {
+                            const float* ce, const float* cmu, uint16_t* dzt, int64_t ldt,
+                            hipStream_t s) {
   const int ntc = (int)(Vpad / 256);
   const int64_t nb = (Tc / 256) * ntc;
   k_dz_from_y<<<(unsigned)nb, kDzT, 0, s>>>(yz, Vpad, Tc, V, rows, ids, meta, c0, pm, lse, grad,
-                                            ce, cmu, ntc);
+                                            ce, cmu, ntc, dzt, ldt);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_hc(const uint16_t* hc, int64_t d, const int32_t* meta, int64_t c0,
+                               int64_t Tc, uint16_t* hct, int64_t ldt, hipStream_t s) {
+  const dim3 grid((unsigned)(Tc / 64), (unsigned)((d + 63) / 64));
+  k_transpose_hc<<<grid, 256, 0, s>>>(hc, d, meta, c0, Tc, hct, ldt);
   return hipGetLastError();
 }
 

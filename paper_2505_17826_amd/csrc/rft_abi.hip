@@ -237,18 +237,23 @@ int64_t bwd_tc_for(const rft_tokens& tok, int64_t d, int64_t V, int dtype, size_
 }
 
 // Fused step (bf16): compacted hidden rows, transposed weight, per-chunk
-// log-sum-exp partials, the sampled logits, the loss partials and the chunk
-// buffer (fp16 y, then bf16 dZ, in dz).
+// log-sum-exp partials, the sampled logits, the loss partials, the chunk
+// buffer (fp16 y, then bf16 dZ, in dz) and the chunk's dZ^T [Vpad, Tc] and
+// hidden rows transposed [d, Tc] (the weight gradient's K-contiguous operands).
 struct StepWs {
   TokMeta m;
-  uint16_t *hc, *wt, *dz;
+  uint16_t *hc, *wt, *dz, *dzt, *hct;
   float *pm, *ps, *pu, *zy;
   float *ce, *cmu;  // per chunk row: entropy-bonus coefficient and softmax mean
   LossPartial* parts;
   int ntiles;
-  int64_t Tc, Vpad;
+  int64_t Tc, Vpad, ldt;
   size_t bytes;
 };
+// Row pitch of the transposed chunk buffers: Tc plus 128 elements, so that
+// rows are not a power of two apart (Tc is a multiple of 256; power-of-two
+// strides put every row of a tile in the same memory channel).
+constexpr int64_t kLdtPad = 128;
 StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
   Carver c(base);
   StepWs w = {};
@@ -267,6 +272,9 @@ StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64
   w.cmu = c.take<float>((size_t)Tc);
   w.parts = c.take<LossPartial>((size_t)((T1 + 255) / 256));
   w.dz = c.take<uint16_t>((size_t)Tc * w.Vpad);
+  w.ldt = Tc + kLdtPad;
+  w.dzt = c.take<uint16_t>((size_t)w.Vpad * w.ldt);
+  w.hct = c.take<uint16_t>((size_t)d * w.ldt);
   w.bytes = c.bytes();
   return w;
 }
@@ -664,13 +672,15 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
                              bonus ? w.ce : nullptr, w.cmu, s),
             fn);
     RFT_HIP(launch_dz_from_y(w.dz, w.Vpad, Tc, V, w.m.rows, tok->token_ids, cnt, c0, w.pm, lse,
-                             grad_logp, bonus ? w.ce : nullptr, w.cmu, s),
+                             grad_logp, bonus ? w.ce : nullptr, w.cmu, w.dzt, w.ldt, s),
             fn);
+    RFT_HIP(launch_transpose_hc(w.hc, d, cnt, c0, Tc, w.hct, w.ldt, s), fn);
     RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
                             d_hidden, d, w.m.rows, c0, 0, s),
             fn);
-    RFT_HIP(mfma_gemm_store_tr(w.dz, w.Vpad, w.hc + c0 * d, d, V, d, Tc, cnt, c0, Tc, d_weight, d,
-                               (ci > 0 || accumulate_dw) ? 1 : 0, s),
+    // dW = dZ^T . Hc with both operands K-contiguous (K = the chunk's rows)
+    RFT_HIP(mfma_gemm_store(w.dzt, w.ldt, w.hct, w.ldt, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight, d,
+                            nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s),
             fn);
   }
   if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);

@@ -288,7 +288,10 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
 hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
                             const int32_t* rows, const int32_t* ids, const int32_t* meta,
                             int64_t c0, const float* pm, const float* lse, const float* grad,
-                            const float* ce, const float* cmu, hipStream_t s);
+                            const float* ce, const float* cmu, uint16_t* dzt, int64_t ldt,
+                            hipStream_t s);
+hipError_t launch_transpose_hc(const uint16_t* hc, int64_t d, const int32_t* meta, int64_t c0,
+                               int64_t Tc, uint16_t* hct, int64_t ldt, hipStream_t s);
 hipError_t mfma_dz(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
                    const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
