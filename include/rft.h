@@ -304,7 +304,11 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
  * the chunk's forward GEMM keeps, next to the log-sum-exp partials, each
  * logit minus its row's maximum over a 256-column tile in fp16 in the
  * workspace, and the backward forms dZ from it instead of recomputing the
- * logits (6 N d V flops instead of 8 N d V); logp, entropy, lse, grad_logp
+ * logits (6 N d V flops instead of 8 N d V); dZ is kept in both layouts
+ * (rows x vocabulary for d_hidden, transposed for d_weight), so the
+ * workspace per chunk row is about 4 Vpad + 2 d bytes (the recommended size
+ * holds chunks of up to 131072 rows: ~85 GB at V = 152064, d = 3584; a
+ * smaller workspace gives smaller chunks); logp, entropy, lse, grad_logp
  * and the stats equal those of the separate calls bit for bit, d_hidden and
  * d_weight agree to the rounding of dZ.  For fp32 inputs the call runs the
  * three separate calls in order.  logits are never stored beyond one chunk.
