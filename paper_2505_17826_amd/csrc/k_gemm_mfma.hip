@@ -36,9 +36,13 @@ constexpr int B_BYTES = BN * BK * 2;
 constexpr int STAGE = A_BYTES + B_BYTES;  // 64 KiB
 constexpr int ROWP = BM * 20;             // per-row epilogue parameters (five words)
 // dZ epilogue: one 256x256 bf16 tile staged in LDS, rows padded to 528 bytes
-// (conflict-free 2- and 8-byte writes, contiguous 16-byte reads)
+// (conflict-free 2- and 8-byte writes, contiguous 16-byte reads); the
+// transposed tile uses rows of 544 bytes (a lane's 8-byte write of four
+// consecutive K: the 16 columns of a lane group 8 banks apart, the 4 K groups
+// 2 banks apart, so a wave's 64 writes cover every bank twice)
 constexpr int STG_PITCH = 528;
-constexpr int STG_BYTES = 256 * STG_PITCH;
+constexpr int STG_PITCH_T = 544;
+constexpr int STG_BYTES = 256 * STG_PITCH_T;
 constexpr int LDS_TOTAL = 2 * STAGE + ROWP > STG_BYTES ? 2 * STAGE + ROWP : STG_BYTES;
 
 enum { EPI_STATS = 0, EPI_DZ = 1, EPI_STORE = 2, EPI_STATS_Y = 3 };
@@ -73,6 +77,7 @@ struct Args {
   int64_t p_off;                                            //   zy at rows_off + m
   uint16_t* y; int64_t ldy;                                 // EPI_STATS_Y: fp16 z - tile max
   uint16_t* dz; int64_t ldz; int64_t Vvalid;                  // EPI_DZ
+  uint16_t* dzt; int64_t ldzt;                                //   and dZ^T [Vpad, ldzt] (nullptr = none)
   float* C; int64_t ldc; int accumulate; int c_scatter;  // EPI_STORE
 };
 
@@ -615,6 +620,23 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
                      hv[i][j]);
       __syncthreads();
       stage_copy_out(st, g.dz + (int64_t)m0 * g.ldz + n0, g.ldz, tid);
+      if (g.dzt) {
+        // dZ^T: tile column c (vocabulary) as a 512-byte row of the 256 chunk rows
+        __syncthreads();  // the row-major copy has left the staging tile
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            *(uint2*)(st + (wn * 128 + j * 16 + r16) * STG_PITCH_T +
+                      (wm * 64 + i * 16 + q4 * 4) * 2) = hv[i][j];
+        __syncthreads();
+#pragma unroll 4
+        for (int it = 0; it < 16; ++it) {
+          const int c = it * NT + tid, row = c >> 5, ch = c & 31;
+          const uint4 v = *(const uint4*)(st + row * STG_PITCH_T + ch * 16);
+          *(uint4*)(g.dzt + (int64_t)(n0 + row) * g.ldzt + m0 + ch * 8) = v;
+        }
+      }
     } else {  // EPI_STORE
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -688,7 +710,7 @@ hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, in
 hipError_t mfma_dz(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
                    const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
-                   int64_t Tc, uint16_t* dz, hipStream_t s) {
+                   int64_t Tc, uint16_t* dz, uint16_t* dzt, int64_t ldzt, hipStream_t s) {
   mf::Args a = {};
   a.A = Hc + c0 * d; a.lda = d;
   a.B = W; a.ldb = d;
@@ -697,6 +719,7 @@ hipError_t mfma_dz(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V, 
   a.rows = rows; a.rows_off = c0; a.ids = ids; a.lse = lse; a.cgrad = cgrad;
   a.egrad = egrad; a.ent = ent;
   a.dz = dz; a.ldz = Vpad; a.Vvalid = V;
+  a.dzt = dzt; a.ldzt = ldzt;
   a.NB = (int)V;  // W has V rows; columns V..Vpad-1 of dZ are written as 0
   // dz rows are indexed by the chunk-local m (m0 + row)
   mf::k_gemm<mf::EPI_DZ><<<grid_for(Tc, Vpad), mf::NT, 0, s>>>(a);

@@ -188,11 +188,15 @@ DpoCarve carve_dpo(void* base, const rft_tokens& tok) {
 
 struct BwdWs {
   TokMeta m;
-  uint16_t *hc, *wt, *dz;  // bf16 path
-  float* dz32;                   // fp32 path
-  int64_t Tc, Vpad;
+  uint16_t *hc, *wt, *dz, *dzt, *hct;  // bf16 path (dZ^T, Hc^T: [*, Tc + 128])
+  float* dz32;                         // fp32 path
+  int64_t Tc, Vpad, ldt;
   size_t bytes;
 };
+// Row pitch of the transposed chunk buffers: Tc plus 128 elements, so that
+// rows are not a power of two apart (Tc is a multiple of 256; power-of-two
+// strides put every row of a tile in the same memory channel).
+constexpr int64_t kLdtPad = 128;
 constexpr int64_t kBf16Align = 256;   // row chunk / vocabulary padding of the bf16 path
 constexpr int64_t kF32Align = 64;
 constexpr int64_t kRecommendTc = 131072;
@@ -207,6 +211,9 @@ BwdWs carve_bwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dty
     w.hc = c.take<uint16_t>((size_t)(tok.T > 0 ? tok.T : 1) * d);
     w.wt = c.take<uint16_t>((size_t)d * w.Vpad);
     w.dz = c.take<uint16_t>((size_t)Tc * w.Vpad);
+    w.ldt = Tc + kLdtPad;
+    w.dzt = c.take<uint16_t>((size_t)w.Vpad * w.ldt);
+    w.hct = c.take<uint16_t>((size_t)d * w.ldt);
   } else {
     w.Vpad = round_up(V, kF32Align);
     w.dz32 = c.take<float>((size_t)Tc * w.Vpad);
@@ -250,10 +257,6 @@ struct StepWs {
   int64_t Tc, Vpad, ldt;
   size_t bytes;
 };
-// Row pitch of the transposed chunk buffers: Tc plus 128 elements, so that
-// rows are not a power of two apart (Tc is a multiple of 256; power-of-two
-// strides put every row of a tile in the same memory channel).
-constexpr int64_t kLdtPad = 128;
 StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
   Carver c(base);
   StepWs w = {};
@@ -518,15 +521,16 @@ rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, cons
     for (int64_t ci = 0; ci < nchunks; ++ci) {
       int64_t c0 = ci * Tc;
       RFT_HIP(mfma_dz(w.hc, d, W, V, w.Vpad, w.m.rows, tok->token_ids, lse, grad_logp,
-                      grad_entropy, entropy, cnt, c0, Tc, w.dz, s),
+                      grad_entropy, entropy, cnt, c0, Tc, w.dz, w.dzt, w.ldt, s),
               fn);
+      RFT_HIP(launch_transpose_hc(w.hc, d, cnt, c0, Tc, w.hct, w.ldt, s), fn);
       // dH rows of this chunk: dZ [count, Vpad] . Wt[d, Vpad]^T, scattered to token rows
       RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
                               d_hidden, d, w.m.rows, c0, 0, s),
               fn);
-      // dW += dZ^T . Hc over the chunk's rows (both read as stored: K = rows)
-      RFT_HIP(mfma_gemm_store_tr(w.dz, w.Vpad, w.hc + c0 * d, d, V, d, Tc, cnt, c0, Tc, d_weight,
-                                 d, (ci > 0 || accumulate_dw) ? 1 : 0, s),
+      // dW += dZ^T . Hc over the chunk's rows, both operands K-contiguous (K = rows)
+      RFT_HIP(mfma_gemm_store(w.dzt, w.ldt, w.hct, w.ldt, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight,
+                              d, nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s),
               fn);
     }
     if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);
