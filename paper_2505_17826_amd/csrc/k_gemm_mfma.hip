@@ -21,8 +21,8 @@
 //              tile, rounded to fp16, row-major [rows, Vpad] (the backward
 //              then forms dZ from it instead of recomputing z).
 //   EPI_DZ     backward recompute: dZ = c (onehot(y) - p) + e p (z - mu) in bf16,
-//              written row-major [rows, Vpad] (the weight-gradient GEMM reads
-//              it as its K-by-M operand, see the TR operand layout).
+//              written row-major [rows, Vpad] (the dH operand) and transposed
+//              [Vpad, ldzt] (the dW operand, K-contiguous).
 //   EPI_STORE  fp32 result, optionally scattered to rows through a map and
 //              optionally added to the existing values.
 #include "rft_internal.h"
@@ -132,58 +132,6 @@ __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_b
   }
 }
 
-// Operands stored with M (N) contiguous and K across rows ("TR": the weight
-// gradient reads dZ [rows, Vpad] and the compacted hidden rows [rows, d]
-// as they are, with no transposed copies).  A stage holds BK = 64 K-rows of
-// 256 M-values (512 B per row) for A, then the same for B; 16-byte chunk c of
-// K-row k sits at chunk c ^ 4 (k & 3) ^ 2 ((k >> 3) & 1).  The fragments of
-// the 16x16x32 MFMA come from transposing reads (ds_read_b64_tr_b16: a
-// 16-lane group reads 4 K-rows x 16 M-values and each lane receives 4
-// consecutive K of one M); the two groups of a half wave read K-rows 8
-// apart, and with this swizzle the two touch disjoint halves of the 16
-// bank groups, so the reads are conflict-free.  Loader wave w fills K-rows
-// [16w, 16w + 16) of A and B with 8 + 8 instructions of two rows each; lane l
-// writes LDS chunk l of its instruction (row l >> 5 of the pair, physical
-// chunk l & 31), so it loads logical chunk
-// (l & 31) ^ 4 ((2 (p & 1) + (l >> 5)) & 3) ^ 2 ((p >> 2) & 1) of instruction
-// p.  The buffer descriptors are rebased on every K step (32-bit offsets) and
-// cover only the valid K-rows: rows past the count read as 0.
-struct LoadGeomTr {
-  uint32_t vA[4], vB[4];  // per-lane byte offsets by (p & 1) | ((p >> 2) & 1) << 1, K-row 0
-  uint32_t sA, sB;        // bytes per K-row
-};
-
-__device__ __forceinline__ void load_stage_tr(const uint16_t* A, int64_t lda, const uint16_t* B,
-                                              int64_t ldb, int k0, int Kv, char* dst,
-                                              const LoadGeomTr& lg) {
-  const int rows = Kv - k0 < BK ? (Kv - k0 > 0 ? Kv - k0 : 0) : BK;
-  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A + (int64_t)k0 * lda, (int64_t)rows * lda * 2);
-  const __amdgpu_buffer_rsrc_t rB = make_rsrc(B + (int64_t)k0 * ldb, (int64_t)rows * ldb * 2);
-#pragma unroll
-  for (int p = 0; p < 8; ++p)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_ptr)(dst + p * 1024), 16,
-                                             lg.vA[(p & 1) | ((p >> 1) & 2)] +
-                                                 (uint32_t)p * 2u * lg.sA, 0, 0, 0);
-#pragma unroll
-  for (int p = 0; p < 8; ++p)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES + p * 1024), 16,
-                                             lg.vB[(p & 1) | ((p >> 1) & 2)] +
-                                                 (uint32_t)p * 2u * lg.sB, 0, 0, 0);
-}
-
-typedef short v4i16 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4i16* lds_v4i16;
-
-// MFMA operand fragment (16 rows of M or N, 8 K per lane) from a TR tile: two
-// transposing reads of 4 K each; off = the lane's byte offset for the first.
-__device__ __forceinline__ bf16x8 frag_tr(const char* tile, uint32_t off) {
-  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(tile + off));
-  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16)(tile + off + 4 * 512));
-  const short __attribute__((ext_vector_type(8))) v = {lo[0], lo[1], lo[2], lo[3],
-                                                       hi[0], hi[1], hi[2], hi[3]};
-  return __builtin_bit_cast(bf16x8, v);
-}
-
 // Tile order.  Workgroup b runs on XCD x = b % 8 as the j = b / 8-th
 // workgroup dispatched there.  M-tiles are taken in super-groups of 64: XCD x
 // owns M-tiles [64 s + 8 x, 64 s + 8 x + 8) of super-group s and walks them
@@ -252,7 +200,7 @@ __device__ __forceinline__ uint32_t f16_bits(float f) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
-template <int EPI, bool TR = false>
+template <int EPI>
 __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   constexpr bool kStats = EPI == EPI_STATS || EPI == EPI_STATS_Y;
   __shared__ __attribute__((aligned(16))) char lds[LDS_TOTAL];
@@ -260,15 +208,12 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid >> 1, wn = wid & 1;  // 4 x 2 waves, wave tile 64 x 128
 
-  int M = g.M, K = g.K, Kv = g.K;  // Kv: valid K (rows of the TR operands)
+  int M = g.M, K = g.K;
   if (g.cnt) {
     int64_t c = (int64_t)g.cnt[0] - g.cnt_off;
     c = c < 0 ? 0 : (c > g.cnt_cap ? g.cnt_cap : c);
     if (g.m_from_cnt) M = (int)c;
-    if (g.k_from_cnt) {
-      K = (int)((c + BK - 1) / BK * BK);
-      Kv = (int)c;
-    }
+    if (g.k_from_cnt) K = (int)((c + BK - 1) / BK * BK);
   }
   const int N = g.N;
   const int NB = g.NB > 0 ? g.NB : N;
@@ -294,18 +239,6 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     }
     lg.sA = (uint32_t)(8 * g.lda * 2);
     lg.sB = (uint32_t)(8 * g.ldb * 2);
-  }
-  LoadGeomTr lt;
-  if (TR) {
-    const int r = (wid % NLOAD) * 16 + (lane >> 5);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int c = (lane & 31) ^ (4 * ((2 * (q & 1) + (lane >> 5)) & 3)) ^ (q & 2);
-      lt.vA[q] = (uint32_t)(r * g.lda * 2 + (int64_t)mt * BM * 2 + c * 16);
-      lt.vB[q] = (uint32_t)(r * g.ldb * 2 + (int64_t)nt * BN * 2 + c * 16);
-    }
-    lt.sA = (uint32_t)(g.lda * 2);
-    lt.sB = (uint32_t)(g.ldb * 2);
   }
   // MFMA tiles: v_mfma_f32_16x16x32_bf16, 4 x 8 tiles of 16 x 16 per wave
   // (measured 3-4% faster than 4 x 2 tiles of 32x32x16 on the same main loop,
@@ -367,34 +300,12 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc4[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
 
-    char* const ldsw = lds + (wid % NLOAD) * (TR ? 16 * 512 : (256 / NLOAD) * 128);
-    // TR fragment offsets (16x16x32): lane l of 16-lane group g = l >> 4 reads
-    // K-row g*8 + jr (jr = (l >> 2) & 3) and M-values 4 aq .. 4 aq + 3
-    // (aq = l & 3) of the fragment's 16; the transposed result gives lane l
-    // the 4 consecutive K of M-value l & 15.
-    uint32_t oA[4], oB[8];
-    if (TR) {
-      const int gq = lane >> 4, jr = (lane >> 2) & 3, aq = lane & 3;
-      const uint32_t kb = (uint32_t)(gq * 8 + jr) * 512u + (uint32_t)((aq & 1) * 8);
-      const int sw = 4 * jr + 2 * (gq & 1);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        oA[i] = kb + (((((wm * 64 + i * 16) >> 3) + (aq >> 1)) ^ sw) << 4);
-#pragma unroll
-      for (int jj = 0; jj < 8; ++jj)
-        oB[jj] = kb + (((((wn * 128 + jj * 16) >> 3) + (aq >> 1)) ^ sw) << 4);
-    }
-    if (nk > 0 && loader) {
-      if (TR) load_stage_tr(g.A, g.lda, g.B, g.ldb, 0, Kv, ldsw, lt);
-      else load_stage(rA, rB, ldsw, 0, K, lg);
-    }
+    char* const ldsw = lds + (wid % NLOAD) * ((256 / NLOAD) * 128);
+    if (nk > 0 && loader) load_stage(rA, rB, ldsw, 0, K, lg);
     __syncthreads();  // first stage and the per-row parameters are visible to every wave
     for (int kt = 0; kt < nk; ++kt) {
-      if (kt + 1 < nk && loader) {
-        if (TR) load_stage_tr(g.A, g.lda, g.B, g.ldb, (kt + 1) * BK, Kv,
-                              ldsw + ((kt + 1) & 1) * STAGE, lt);
-        else load_stage(rA, rB, ldsw + ((kt + 1) & 1) * STAGE, (kt + 1) * BK, K, lg);
-      }
+      if (kt + 1 < nk && loader)
+        load_stage(rA, rB, ldsw + ((kt + 1) & 1) * STAGE, (kt + 1) * BK, K, lg);
       const char* As = lds + (kt & 1) * STAGE;
       const char* Bs = As + A_BYTES;
       {
@@ -403,22 +314,15 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           bf16x8 a[4], b[8];
-          if (TR) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) a[i] = frag_tr(As, oA[i] + ks * 32 * 512);
+          for (int i = 0; i < 4; ++i) {
+            const int row = wm * 64 + i * 16 + r16;
+            a[i] = *(const bf16x8*)(As + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
+          }
 #pragma unroll
-            for (int j = 0; j < 8; ++j) b[j] = frag_tr(Bs, oB[j] + ks * 32 * 512);
-          } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int row = wm * 64 + i * 16 + r16;
-              a[i] = *(const bf16x8*)(As + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
-            }
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-              const int row = wn * 128 + j * 16 + r16;
-              b[j] = *(const bf16x8*)(Bs + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
-            }
+          for (int j = 0; j < 8; ++j) {
+            const int row = wn * 128 + j * 16 + r16;
+            b[j] = *(const bf16x8*)(Bs + row * 128 + (((ks * 4 + q4) ^ ((row >> 1) & 7)) << 4));
           }
 #pragma unroll
           for (int i = 0; i < 4; ++i)
@@ -723,24 +627,6 @@ hipError_t mfma_dz(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V, 
   a.NB = (int)V;  // W has V rows; columns V..Vpad-1 of dZ are written as 0
   // dz rows are indexed by the chunk-local m (m0 + row)
   mf::k_gemm<mf::EPI_DZ><<<grid_for(Tc, Vpad), mf::NT, 0, s>>>(a);
-  return hipGetLastError();
-}
-
-// C[M, N] (+)= A^T . B with A [K, lda] (M contiguous) and B [K, ldb] (N
-// contiguous), fp32 output; K (the valid rows of A and B) from the device
-// counter.  Rows of A and B past the count read as 0.
-hipError_t mfma_gemm_store_tr(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
-                              int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
-                              int64_t cnt_cap, float* C, int64_t ldc, int accumulate,
-                              hipStream_t s) {
-  mf::Args a = {};
-  a.A = A; a.lda = lda; a.B = B; a.ldb = ldb;
-  a.M = (int)M; a.N = (int)N; a.K = (int)K;
-  a.cnt = cnt; a.cnt_off = cnt_off; a.cnt_cap = cnt_cap; a.m_from_cnt = 0;
-  a.k_from_cnt = cnt != nullptr ? 1 : 0;
-  a.C = C; a.ldc = ldc; a.rows = nullptr; a.rows_off = 0; a.c_scatter = 0;
-  a.accumulate = accumulate;
-  mf::k_gemm<mf::EPI_STORE, true><<<grid_for(M, N), mf::NT, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -296,10 +296,6 @@ hipError_t mfma_dz(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V, i
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
                    const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
                    int64_t Tc, uint16_t* dz, uint16_t* dzt, int64_t ldzt, hipStream_t s);
-hipError_t mfma_gemm_store_tr(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
-                              int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
-                              int64_t cnt_cap, float* C, int64_t ldc, int accumulate,
-                              hipStream_t s);
 hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
                            int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
                            int64_t cnt_cap, int m_from_cnt, int k_from_cnt, float* C, int64_t ldc,
