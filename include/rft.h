@@ -219,7 +219,11 @@ rft_status rft_token_logprobs(const rft_tokens* tok, const void* hidden, const v
                               float* lse, void* ws, size_t ws_bytes, void* stream);
 
 /* The same statistics from given fp32 logits [T, V].  gathered (may be NULL)
- * receives logits[t, id_t] (bit-exact copy; NaN for an out-of-range id). */
+ * receives logits[t, id_t] (bit-exact copy; NaN for an out-of-range id).
+ * Logits of -inf mark vocabulary entries the caller excludes: they get p = 0
+ * and add 0 to the entropy, so the results are those of the vocabulary without
+ * them (a row needs one finite logit).  The same holds in the loss-only and
+ * d_logits calls, whose d_logits are exactly 0 in those columns. */
 rft_status rft_token_logprobs_from_logits(const rft_tokens* tok, const float* logits, int64_t V,
                                           float* logp, float* entropy, float* lse,
                                           float* gathered, void* ws, size_t ws_bytes,
@@ -261,7 +265,11 @@ rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* 
  *   d_weight = dZ^T . hidden ([V, d] f32, overwritten, or added to when
  *              accumulate_dw != 0).
  * z is recomputed from hidden and weight (it is never stored by the forward);
- * dZ is formed in chunks of rows in the workspace (bf16 for bf16 inputs).
+ * dZ is formed in chunks of rows in the workspace (bf16 for bf16 inputs, kept
+ * in both layouts with the chunk's hidden rows transposed, so that both GEMMs
+ * read K-contiguous operands: about 4 Vpad + 2 d bytes per chunk row).
+ * The masked-vocabulary convention of rft_token_logprobs_from_logits (z = -inf
+ * gives p = 0 and a 0 entropy term) holds in the d_logits calls as well.
  * lse and grad_logp [T] are normally the outputs of rft_token_logprobs and
  * rft_ppo_clip_loss_fwd.
  * Errors: as rft_token_logprobs. */
