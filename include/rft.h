@@ -268,8 +268,6 @@ rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* 
  * dZ is formed in chunks of rows in the workspace (bf16 for bf16 inputs, kept
  * in both layouts with the chunk's hidden rows transposed, so that both GEMMs
  * read K-contiguous operands: about 4 Vpad + 2 d bytes per chunk row).
- * The masked-vocabulary convention of rft_token_logprobs_from_logits (z = -inf
- * gives p = 0 and a 0 entropy term) holds in the d_logits calls as well.
  * lse and grad_logp [T] are normally the outputs of rft_token_logprobs and
  * rft_ppo_clip_loss_fwd.
  * Errors: as rft_token_logprobs. */
