@@ -43,7 +43,11 @@ constexpr int ROWP = BM * 20;             // per-row epilogue parameters (five w
 constexpr int STG_PITCH = 528;
 constexpr int STG_PITCH_T = 544;
 constexpr int STG_BYTES = 256 * STG_PITCH_T;
-constexpr int LDS_TOTAL = 2 * STAGE + ROWP > STG_BYTES ? 2 * STAGE + ROWP : STG_BYTES;
+constexpr int LDS_MAIN = 2 * STAGE + ROWP > STG_BYTES ? 2 * STAGE + ROWP : STG_BYTES;
+// statistics epilogue: exchange between the two column halves of a tile,
+// outside the staging tile (partials [256][3], half maxima [2][256])
+constexpr int XCH_BYTES = 256 * 3 * 4 + 2 * 256 * 4;
+constexpr int LDS_TOTAL = LDS_MAIN + XCH_BYTES;
 
 enum { EPI_STATS = 0, EPI_DZ = 1, EPI_STORE = 2, EPI_STATS_Y = 3 };
 
@@ -348,8 +352,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     if constexpr (kStats) {
       // A lane holds 16 rows (e = 4 i + q) of its 16-lane group, 8 columns
       // each; a row's 128 columns of this wave lie in the 16 lanes of one DPP row.
-      float* xm = (float*)lds;           // cross-wave exchange [256 rows][3]
-      float* mrow = (float*)(lds + 3072);  // row maximum over the tile [256]
+      float* xm = (float*)(lds + LDS_MAIN);            // partials of the wn = 1 half [256][3]
+      float* xmax = (float*)(lds + LDS_MAIN + 3072);   // half maxima [2][256] (STATS_Y)
       const int colb16 = n0 + wn * 128 + r16;
       bool cv[8];
 #pragma unroll
@@ -378,6 +382,56 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
         }
       }
       row16_max_n(mx);
+      // logit of the sampled token, picked with selects outside the store's
+      // branch (a dynamic index there makes the compiler copy the tiles)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int rl = wm * 64 + (e >> 2) * 16 + q4 * 4 + (e & 3);
+        const int yl = rp_i[rl] - (n0 + wn * 128);
+        const int jj = yl >> 4;
+        float z = acc4[e >> 2][0][e & 3];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) z = jj == j ? acc4[e >> 2][j][e & 3] : z;
+        if (yl >= 0 && yl < 128 && (yl & 15) == r16) g.zy[g.rows_off + m0 + rl] = z;
+      }
+      // lane r16 of group q4 owns row e = r16 of that group
+      const int rl = wm * 64 + (r16 >> 2) * 16 + q4 * 4 + (r16 & 3);
+      if (EPI == EPI_STATS_Y) {
+        // y = z - (row maximum over the tile) <= 0, rounded to fp16, stored
+        // before the exponent sums so that the stores drain while those run
+        // (the sums and the merge below are the statistics-only forward's
+        // arithmetic); rows past M and columns past N hold values the
+        // backward never uses
+        float hm = mx[0];
+#pragma unroll
+        for (int e = 1; e < 16; ++e) hm = r16 == e ? mx[e] : hm;
+        xmax[wn * 256 + rl] = hm;
+        __syncthreads();  // also: every row parameter read before the staging tile covers them
+        uint2 hv[4][8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int rl0 = wm * 64 + i * 16 + q4 * 4;
+          float mr[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) mr[q] = fmaxf(mx[i * 4 + q], xmax[(1 - wn) * 256 + rl0 + q]);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            uint32_t hb[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) hb[q] = f16_bits(acc4[i][j][q] - mr[q]);
+            hv[i][j].x = hb[0] | (hb[1] << 16);
+            hv[i][j].y = hb[2] | (hb[3] << 16);
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            stage_col4(lds + (wm * 64 + i * 16 + q4 * 4) * STG_PITCH + (wn * 128 + j * 16 + r16) * 2,
+                       hv[i][j]);
+        __syncthreads();
+        stage_copy_out(lds, g.y + (int64_t)m0 * g.ldy + n0, g.ldy, tid);
+      }
       if (full) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
@@ -411,19 +465,6 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       }
       row16_sum_n(sm);
       row16_sum_n(um);
-      // logit of the sampled token, picked with selects outside the store's
-      // branch (a dynamic index there makes the compiler copy the tiles)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int rl = wm * 64 + (e >> 2) * 16 + q4 * 4 + (e & 3);
-        const int yl = rp_i[rl] - (n0 + wn * 128);
-        const int jj = yl >> 4;
-        float z = acc4[e >> 2][0][e & 3];
-#pragma unroll
-        for (int j = 1; j < 8; ++j) z = jj == j ? acc4[e >> 2][j][e & 3] : z;
-        if (yl >= 0 && yl < 128 && (yl & 15) == r16) g.zy[g.rows_off + m0 + rl] = z;
-      }
-      // lane r16 of group q4 owns row e = r16 of that group
       float om = mx[0], os = sm[0], ou = um[0];
 #pragma unroll
       for (int e = 1; e < 16; ++e) {
@@ -432,7 +473,6 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
         os = sel ? sm[e] : os;
         ou = sel ? um[e] : ou;
       }
-      const int rl = wm * 64 + (r16 >> 2) * 16 + q4 * 4 + (r16 & 3);
       if (wn == 1) {
         xm[rl * 3 + 0] = om;
         xm[rl * 3 + 1] = os;
@@ -441,46 +481,13 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       __syncthreads();
       if (wn == 0) {
         const int m = m0 + rl;
-        float mt = 0.f;
         if (m < M) {
           lse_merge(om, os, ou, xm[rl * 3 + 0], xm[rl * 3 + 1], xm[rl * 3 + 2]);
           const int64_t o = (int64_t)nt * g.ldp + g.p_off + m;
           g.pm[o] = om;
           g.ps[o] = os;
           g.pu[o] = ou;
-          mt = om;
         }
-        if (EPI == EPI_STATS_Y) mrow[rl] = mt;
-      }
-      __syncthreads();
-      if (EPI == EPI_STATS_Y) {
-        // y = z - (row maximum over the tile) <= 0, rounded to fp16; rows past
-        // M and columns past N hold values the backward never uses
-        uint2 hv[4][8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int rl0 = wm * 64 + i * 16 + q4 * 4;
-          float mr[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) mr[q] = mrow[rl0 + q];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            uint32_t hb[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) hb[q] = f16_bits(acc4[i][j][q] - mr[q]);
-            hv[i][j].x = hb[0] | (hb[1] << 16);
-            hv[i][j].y = hb[2] | (hb[3] << 16);
-          }
-        }
-        __syncthreads();  // the staging tile overlaps xm and mrow
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            stage_col4(lds + (wm * 64 + i * 16 + q4 * 4) * STG_PITCH + (wn * 128 + j * 16 + r16) * 2,
-                       hv[i][j]);
-        __syncthreads();
-        stage_copy_out(lds, g.y + (int64_t)m0 * g.ldy + n0, g.ldy, tid);
       }
     } else if (EPI == EPI_DZ) {
       // d = c (onehot - p) + e p (z - mu) in bf16, packed per lane as four
