@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define RFT_ABI_VERSION 6
+#define RFT_ABI_VERSION 7
 
 typedef enum {
   RFT_OK = 0,
@@ -174,6 +174,14 @@ const char* rft_last_error(void);
 size_t rft_workspace_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
 size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
 
+/* Rows per chunk that RFT_OP_PPO_BWD or RFT_OP_PPO_STEP processes with a
+ * workspace of ws_bytes for this layout and sizes (the calls loop over
+ * ceil(T / chunk) chunks); 0 if the workspace is too small, the operation has
+ * no row chunks or an argument is invalid.  A chunk never exceeds 2^21 rows
+ * (its transposed tiles stay within one 2 GiB buffer descriptor). */
+int64_t rft_chunk_rows(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype,
+                       size_t ws_bytes);
+
 /* GRPO group-relative advantages (Sec. 3.2, Listing 4: advantage_fn "grpo",
  * repeat_times 8; Sec. 3.3.1: 8 rollouts per task).
  * rewards[n_groups * group_size] (f32); rollouts g*G .. g*G+G-1 form group g.
@@ -218,7 +226,10 @@ rft_status rft_token_logprobs(const rft_tokens* tok, const void* hidden, const v
                               int dtype, int64_t d, int64_t V, float* logp, float* entropy,
                               float* lse, void* ws, size_t ws_bytes, void* stream);
 
-/* The same statistics from given fp32 logits [T, V].  gathered (may be NULL)
+/* The same statistics from given fp32 logits [T, V] (Sec. 3.1.1: log-probs of
+ * the response tokens under the policy, which PPO and GRPO need; Sec. 3.4.2:
+ * the actor's entropy).  This is the statistics half of the loss-only path,
+ * for callers whose logits already exist.  gathered (may be NULL)
  * receives logits[t, id_t] (bit-exact copy; NaN for an out-of-range id).
  * Logits of -inf mark vocabulary entries the caller excludes: they get p = 0
  * and add 0 to the entropy, so the results are those of the vocabulary without
@@ -239,8 +250,10 @@ rft_status rft_token_logprobs_from_logits(const rft_tokens* tok, const float* lo
  *   kl = exp(ref - logp) - (ref - logp) - 1,
  *   loss = sum_t w_t (pg + beta kl)  with w_t from params.agg,
  *   grad_logp[t] = w_t (-A rho [not clipped] + beta (1 - exp(ref - logp))).
- * "Clipped" means A > 0 and rho > 1+eps_high, or A < 0 and rho < 1-eps_low,
- * decided in fp32 on logp - old against fp32(log(1 +/- eps)).
+ * "Clipped" means A > 0 and rho > 1+eps_high, or A < 0 and rho < 1-eps_low
+ * (strict: on a bound the gradient is -A rho).  The test is taken in fp32 on
+ * logp - old against fp32(log(1 +/- eps)); it agrees with the exact test
+ * except for a token within fp32 rounding (about 1e-7 relative) of a bound.
  * Inputs f32 [T] (adv is [n_seq]); ref_logp may be NULL iff kl_coef == 0;
  * entropy may be NULL (entropy_mean 0) unless entropy_coef > 0.  Outputs:
  * grad_logp [T] (0 on masked rows), *stats (device), and, if not NULL,
@@ -256,7 +269,13 @@ rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* 
                                  float* grad_logp, float* grad_entropy, rft_ppo_stats* stats,
                                  void* ws, size_t ws_bytes, void* stream);
 
-/* Backward of the loss through the policy head: with c_t = grad_logp[t],
+/* Backward of the PPO-clip/KL loss of Sec. 3.3.2 (whose call shape is that of
+ * Sec. 3.2, Listing 4: log-probs, old log-probs, action mask, advantages in;
+ * loss out) through the policy head z_t = weight . hidden_t, i.e. the
+ * trainer's gradient of that loss with respect to the hidden states and the
+ * lm_head weight.  The same call back-propagates any loss whose gradient with
+ * respect to the log-probs is given (the SFT and DPO losses below).
+ * With c_t = grad_logp[t],
  *   dZ_tj = c_t ([j == id_t] - p_tj) + e_t p_tj (z_tj - (lse_t - H_t)),
  *   p_tj = exp(z_tj - lse_t), c_t = grad_logp[t], e_t = grad_entropy[t]
  *   (the entropy bonus term; grad_entropy and entropy may both be NULL,
@@ -277,7 +296,9 @@ rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, cons
                                  const float* entropy, float* d_hidden, float* d_weight,
                                  int32_t accumulate_dw, void* ws, size_t ws_bytes, void* stream);
 
-/* d_logits[t, j] = c_t ([j == id_t] - p_tj) + e_t p_tj (z_tj - (lse_t - H_t))
+/* Backward of the same loss (Sec. 3.3.2; Sec. 3.2, Listing 4) to given fp32
+ * logits, the loss-only path's gradient:
+ * d_logits[t, j] = c_t ([j == id_t] - p_tj) + e_t p_tj (z_tj - (lse_t - H_t))
  * with z = logits, as rft_ppo_clip_loss_bwd (grad_entropy and entropy may both
  * be NULL); 0 on masked rows (every row of d_logits [T, V] f32 is written). */
 rft_status rft_ppo_clip_loss_bwd_logits(const rft_tokens* tok, const float* logits, int64_t V,
@@ -285,7 +306,10 @@ rft_status rft_ppo_clip_loss_bwd_logits(const rft_tokens* tok, const float* logi
                                         const float* grad_entropy, const float* entropy,
                                         float* d_logits, void* ws, size_t ws_bytes, void* stream);
 
-/* The loss-only path in one pass per row: log-softmax statistics of the given
+/* The loss-only path in one pass per row (Sec. 3.1.1 log-probs and Sec. 3.4.2
+ * entropy of the response tokens, the PPO-clip/KL loss of Sec. 3.3.2 with the
+ * metrics Sec. 3.2, Listing 4 returns, and its gradient to the logits):
+ * log-softmax statistics of the given
  * logits, the PPO-clip/KL loss and metrics, and d_logits, reading each valid
  * logits row once from HBM (the row stays on chip between the statistics and
  * the gradient) and writing d_logits once.  Outputs as rft_token_logprobs_from_logits,

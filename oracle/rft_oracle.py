@@ -37,9 +37,11 @@ Readings where the paper is silent (it prints no formula):
   R3 Group std: sample std (divisor G-1) by default, the population std
      (divisor G) on request; eps = 1e-6 added to the std; a group whose rewards
      are all equal (or G = 1) gets advantage exactly 0.
-  R4 Clip decision: strict inequalities, taken in fp32 on ``logp - old``
-     against ``fp32(log(1 +/- eps))`` so that a GPU fed the same fp32 inputs
-     takes the same decision; values are fp64.
+  R4 Clip decision: by the definition, in fp64: a token is clipped when
+     A > 0 and rho > 1 + eps_high, or A < 0 and rho < 1 - eps_low, with
+     strict inequalities (at a bound both branches have the same value and the
+     gradient is the interior one, -A rho), rho = exp(logp - old) in fp64.
+     The value and the gradient take the same decision.
   R5 Masked rows give 0 in every per-row output; out-of-range token ids in a
      valid row give NaN log-prob, are counted in ``n_bad_ids`` and contribute
      nothing to the loss, its metrics or its gradient (they still count in N
@@ -266,14 +268,6 @@ def token_logprobs_from_logits(logits, ids, mask, rows=None, block=256):
 
 
 # ------------------------------------------------------------------ loss ----
-def clip_thresholds(eps_low, eps_high):
-    """fp32 thresholds on ``logp - old`` equivalent to ``rho < 1-eps_low`` and
-    ``rho > 1+eps_high`` (reading R4)."""
-    lo = np.float32(math.log(1.0 - eps_low)) if eps_low < 1.0 else np.float32(-np.inf)
-    hi = np.float32(math.log1p(eps_high)) if math.isfinite(eps_high) else np.float32(np.inf)
-    return lo, hi
-
-
 def ppo_clip_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids=None, V=None,
                       eps_low=0.2, eps_high=0.2, beta=0.0, agg=AGG_SEQ_MEAN_TOKEN_MEAN,
                       denom_override=0.0, entropy=None, is_expert=None, mix_mu=0.0,
@@ -371,13 +365,12 @@ def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, e
     else:
         raise ValueError(agg)
 
-    delta = lp - old
-    rho = np.exp(delta)
-    rho_bar = np.clip(rho, 1.0 - eps_low, 1.0 + eps_high)
+    # ratio, clipped surrogate and the clip decision by the definition (R4)
+    rho = np.exp(lp - old)
+    lo, hi = 1.0 - eps_low, 1.0 + eps_high
+    rho_bar = np.clip(rho, lo, hi)
     pg = np.maximum(-A * rho, -A * rho_bar)
-    lo32, hi32 = clip_thresholds(eps_low, eps_high)
-    d32 = (lp.astype(np.float32) - old.astype(np.float32)).astype(np.float32)
-    clipped = ((A > 0) & (d32 > hi32)) | ((A < 0) & (d32 < lo32))
+    clipped = ((A > 0) & (rho > hi)) | ((A < 0) & (rho < lo))
     dk = ref - lp
     kl = np.exp(dk) - dk - 1.0
     ell = pg + beta * kl
@@ -411,8 +404,10 @@ def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, e
         "sft_loss": 0.0, "n_expert": 0,
         "grad_logp": grad, "weights_rows": rows, "weights": w,
         "clipped_rows": rows[clipped],
-        "margin": np.minimum(np.abs(d32.astype(np.float64) - float(hi32)),
-                             np.abs(d32.astype(np.float64) - float(lo32))),
+        # relative distance of rho from the nearer clip bound (an infinite
+        # bound, or a lower bound of 0, is never near)
+        "margin": np.minimum(np.abs(rho / hi - 1.0) if math.isfinite(hi) else np.inf,
+                             np.abs(rho / lo - 1.0) if lo > 0 else np.inf),
     }
     if entropy is not None:
         ent = np.where(good, _f64(entropy)[rows], 0.0)

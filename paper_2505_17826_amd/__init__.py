@@ -71,6 +71,8 @@ _SIGS = {
                                               ctypes.c_int]),
     "rft_workspace_min_bytes": (ctypes.c_size_t, [ctypes.c_int, ctypes.POINTER(rft_tokens), _i64,
                                                   _i64, ctypes.c_int]),
+    "rft_chunk_rows": (_i64, [ctypes.c_int, ctypes.POINTER(rft_tokens), _i64, _i64, ctypes.c_int,
+                              ctypes.c_size_t]),
     "rft_group_advantages": (ctypes.c_int, [_p, _i64, ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
                                             _p, _p]),
     "rft_group_advantages_ids": (ctypes.c_int, [_p, _p, _i64, _i64, ctypes.c_int32, ctypes.c_float,
@@ -204,6 +206,11 @@ def workspace_bytes(op, tokens: Tokens, d=0, V=1, dtype=RFT_F32, minimum=False) 
     tk = tokens.c()
     f = L.rft_workspace_min_bytes if minimum else L.rft_workspace_bytes
     return int(f(op, ctypes.byref(tk), d, V, dtype))
+
+
+def chunk_rows(op, tokens: Tokens, d, V, dtype, ws_bytes) -> int:
+    tk = tokens.c()
+    return int(lib().rft_chunk_rows(op, ctypes.byref(tk), d, V, dtype, ws_bytes))
 
 
 def _workspace(nbytes, device, ws=None):

@@ -224,10 +224,17 @@ BwdWs carve_bwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dty
 
 int64_t bwd_align(int dtype) { return dtype == RFT_BF16 ? kBf16Align : kF32Align; }
 
+// Upper bound of a row chunk: the dW GEMM reads 256-row tiles of the
+// transposed chunk buffers (row pitch Tc + kLdtPad, bf16) through one buffer
+// descriptor with 32-bit offsets, so 256 (Tc + kLdtPad) 2 bytes must stay
+// below 2^31.  2^21 rows is below that bound for both dtypes.
+constexpr int64_t kMaxTc = (int64_t)1 << 21;
+static_assert(256 * (kMaxTc + kLdtPad) * 2 < ((int64_t)1 << 31), "chunk tile must fit a descriptor");
+
 int64_t bwd_tc_max(const rft_tokens& tok, int dtype) {
   int64_t a = bwd_align(dtype);
   int64_t t = round_up(tok.T > 0 ? tok.T : 1, a);
-  return t;
+  return t < kMaxTc ? t : kMaxTc;
 }
 
 // largest row chunk (a multiple of the alignment) whose workspace fits, 0 if none
@@ -374,6 +381,23 @@ size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t
     return carve_bwd(nullptr, *tok, d, V, dtype, bwd_align(dtype)).bytes;
   }
   return rft_workspace_bytes(op, tok, d, V, dtype);
+}
+
+int64_t rft_chunk_rows(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype,
+                       size_t ws_bytes) {
+  if (!tok || tok->T < 0 || tok->n_seq < 0 || V < 1 || d < 1) return 0;
+  if (dtype != RFT_F32 && dtype != RFT_BF16) return 0;
+  if (op == RFT_OP_PPO_BWD) return bwd_tc_for(*tok, d, V, dtype, ws_bytes);
+  if (op == RFT_OP_PPO_STEP) {
+    if (dtype == RFT_BF16) return step_tc_for(*tok, d, V, ws_bytes);
+    // fp32: the separate backward runs in the front of the workspace
+    const int64_t tail = round_up((tok->T > 0 ? tok->T : 1) * 4, 256);
+    if ((int64_t)ws_bytes < tail + 256) return 0;
+    const size_t front = (size_t)(((int64_t)ws_bytes - tail) / 256 * 256);
+    if (front < step_f32_front(*tok, d, V, bwd_align(dtype))) return 0;
+    return bwd_tc_for(*tok, d, V, dtype, front);
+  }
+  return 0;
 }
 
 rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t group_size,

@@ -52,6 +52,16 @@ def oracle_eps(cfg):
     return f32(cfg.eps_low), f32(cfg.eps_high), f32(cfg.beta)
 
 
+def near_bound(logp, old, eps_low, eps_high):
+    """Relative distance of rho = exp(logp - old) (fp64) from the nearer clip
+    bound 1 - eps_low or 1 + eps_high (inf where a bound cannot be reached)."""
+    rho = np.exp(np.asarray(logp, np.float64) - np.asarray(old, np.float64))
+    hi, lo = 1.0 + eps_high, 1.0 - eps_low
+    d_hi = np.abs(rho / hi - 1.0) if np.isfinite(hi) else np.full(rho.shape, np.inf)
+    d_lo = np.abs(rho / lo - 1.0) if lo > 0 else np.full(rho.shape, np.inf)
+    return np.minimum(d_hi, d_lo)
+
+
 def perturbed_logprobs(logp_fp64, batch: synth.Batch):
     """Old / reference log-probs = given log-probs + the batch's noise, as fp32."""
     m = batch.mask.cpu().numpy() != 0
@@ -118,12 +128,36 @@ def oracle_step(b: synth.Batch, old32, ref32, denom=0.0, is_expert=None, mu=0.0,
                           denom, is_expert=is_expert, mix_mu=f32(mu), entropy_coef=f32(ent_coef))
 
 
+def compare_stats(st, of, n_near=0):
+    """Every loss statistic of the library against the oracle's.  The
+    per-token log-probs may differ by TOL_LOGP, so the means over tokens of
+    kl, ratio and entropy are held to that (absolute; relative for the
+    ratio); the weighted sums like the loss; the clip fraction may differ by
+    the tokens near a bound (n_near)."""
+    assert st["n_bad_ids"] == of["n_bad_ids"], (st["n_bad_ids"], of["n_bad_ids"])
+    assert st["n_valid"] == of["n_valid"] and st["n_seq_valid"] == of["n_seq_valid"]
+    for k in ("loss", "pg_loss", "kl_loss", "entropy_loss", "sft_loss"):
+        assert abs(st[k] - of[k]) <= TOL_LOSS_REL * abs(of[k]) + TOL_LOSS_ABS, (k, st[k], of[k])
+    for k in ("kl_mean", "entropy_mean"):
+        assert abs(st[k] - of[k]) <= TOL_LOGP, (k, st[k], of[k])
+    assert abs(st["ratio_mean"] - of["ratio_mean"]) <= TOL_LOGP * max(abs(of["ratio_mean"]), 1e-30) \
+        + 1e-12, (st["ratio_mean"], of["ratio_mean"])
+    assert abs(st["n_clipped"] - of["n_clipped"]) <= n_near, (st["n_clipped"], of["n_clipped"])
+    n_pol = of["n_valid"] - of.get("n_expert", 0)
+    if n_pol > 0:
+        assert abs(st["clipfrac"] - of["clipfrac"]) <= n_near / n_pol + 1e-12, \
+            (st["clipfrac"], of["clipfrac"])
+
+
 def compare_step(g, o, b: synth.Batch, check_bwd=True):
     m = b.mask.cpu().numpy() != 0
     np.testing.assert_allclose(g["adv"], o["adv"], atol=TOL_ADV, rtol=0)
     for k in ("logp", "entropy", "lse"):
         assert np.all(g[k][~m] == 0.0), f"{k}: masked rows must be exactly 0"
-        err = np.abs(g[k][m] - o[k][m]).max() if m.any() else 0.0
+        # a valid row with an out-of-range id has a NaN log-prob on both sides
+        gn, on = np.isnan(g[k][m]), np.isnan(o[k][m])
+        assert np.array_equal(gn, on), f"{k}: NaN rows differ"
+        err = np.abs(g[k][m][~on] - o[k][m][~on]).max() if (~on).any() else 0.0
         assert err <= TOL_LOGP, f"{k}: max abs err {err}"
     st, of = g["stats"], o["fwd"]
     assert st["n_valid"] == of["n_valid"] and st["n_seq_valid"] == of["n_seq_valid"]
@@ -139,6 +173,7 @@ def compare_step(g, o, b: synth.Batch, check_bwd=True):
     bad = np.abs(gr - orr) > 1e-3 * np.abs(orr) + 1e-7 * scale
     assert not bad.any(), f"grad_logp: {bad.sum()} tokens off"
     assert abs(st["n_clipped"] - of["n_clipped"]) <= int((~keep).sum())
+    compare_stats(st, of, n_near=int((~keep).sum()))
     assert st["n_expert"] == of["n_expert"]
     assert abs(st["sft_loss"] - of["sft_loss"]) <= TOL_LOSS_REL * abs(of["sft_loss"]) + TOL_LOSS_ABS
     ent_l = of.get("entropy_loss", 0.0)

@@ -216,3 +216,34 @@ def test_header_documents_every_entry_point():
         # every prototype is preceded by a comment block
         i = src.rindex(n + "(")
         assert "*/" in src[max(0, i - 2000):i], n
+
+
+def test_chunk_rows_are_bounded_for_huge_row_counts():
+    """A huge T with a tiny vocabulary and a workspace big enough for one
+    chunk of every row: the chunk stays at or below 2^21 rows, so the
+    transposed chunk tiles of the weight-gradient GEMM (256 rows of pitch
+    chunk + 128, bf16) fit one 2 GiB buffer descriptor."""
+    L = R.lib()
+    T = (1 << 30) - 256
+    tk = _tok(T=T, n_seq=1 << 20)
+    for op in (R.RFT_OP_PPO_BWD, R.RFT_OP_PPO_STEP):
+        for dt in (R.RFT_BF16, R.RFT_F32):
+            ws = 1 << 50   # far more than any chunk needs
+            c = L.rft_chunk_rows(op, ctypes.byref(tk), 8, 256, dt, ws)
+            assert 0 < c <= (1 << 21), (op, dt, c)
+            assert 256 * (c + 128) * 2 < (1 << 31)
+            assert c % (256 if dt == R.RFT_BF16 else 64) == 0
+            # too small a workspace gives 0, the minimum one the smallest chunk
+            mn = L.rft_workspace_min_bytes(op, ctypes.byref(tk), 8, 256, dt)
+            assert L.rft_chunk_rows(op, ctypes.byref(tk), 8, 256, dt, mn - 256) == 0
+            # (the fp32 step's minimum is set by its forward's partials, which
+            # leave room for a larger backward chunk)
+            c = L.rft_chunk_rows(op, ctypes.byref(tk), 8, 256, dt, mn)
+            assert (256 if dt == R.RFT_BF16 else 64) <= c <= (1 << 21)
+            if op == R.RFT_OP_PPO_BWD or dt == R.RFT_BF16:
+                assert c == (256 if dt == R.RFT_BF16 else 64)
+    # the recommended workspace of an ordinary batch holds its whole chunk
+    tk = _tok(T=4096, n_seq=8)
+    ws = L.rft_workspace_bytes(R.RFT_OP_PPO_STEP, ctypes.byref(tk), 256, 5000, R.RFT_BF16)
+    assert L.rft_chunk_rows(R.RFT_OP_PPO_STEP, ctypes.byref(tk), 256, 5000, R.RFT_BF16, ws) == 4096
+    assert L.rft_chunk_rows(R.RFT_OP_PPO_FWD, ctypes.byref(tk), 256, 5000, R.RFT_BF16, ws) == 0

@@ -261,9 +261,7 @@ def test_fullsize_step_mix_entropy():
                              entropy_coef=f32(coef))
     # tokens near a clip bound are left out (either branch is valid there)
     g_o = of["grad_logp"][rows]
-    lo, hi = O.clip_thresholds(el, eh)
-    dl = (np.float32(cpu(logp)[rows]) - np.float32(cpu(old)[rows])).astype(np.float64)
-    near = np.minimum(np.abs(dl - float(hi)), np.abs(dl - float(lo))) < 1e-4
+    near = near_bound(olp[rows], cpu(old)[rows], el, eh) < 1e-4
     gg = cpu(grad)[rows]
     np.testing.assert_allclose(gg[~near], g_o[~near], rtol=1e-3, atol=1e-7 * np.abs(g_o).max())
     hrows = rows[~near][:12]

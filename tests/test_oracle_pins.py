@@ -376,6 +376,89 @@ def test_bad_ids_in_loss():
     assert out["n_valid"] == v.size
 
 
+def test_golden_bad_id_every_metric():
+    """Hand-derived fixture: a valid row with an out-of-range id (holding
+    finite values that would clip, add KL and entropy if counted) changes no
+    returned metric, gradient or entropy-bonus coefficient, and still counts
+    in N and n_i (reading R5)."""
+    g = GOLD["ppo_bad_id_all_metrics"]
+    ss = np.array([0, 3], np.int32)
+    mask = np.ones(3, np.uint8)
+    out = O.ppo_clip_loss_fwd(np.array(g["logp"]), np.array(g["old_logp"]), np.array(g["ref_logp"]),
+                              np.array([g["adv"]]), mask, ss, np.array(g["ids"]), g["V"],
+                              g["eps"], g["eps"], g["beta"], O.AGG_SEQ_MEAN_TOKEN_MEAN,
+                              entropy=np.array(g["entropy"]), entropy_coef=g["entropy_coef"])
+    for k in ("loss", "pg_loss", "kl_loss", "kl_mean", "ratio_mean", "clipfrac", "entropy_mean",
+              "entropy_loss"):
+        assert out[k] == pytest.approx(g[k], rel=1e-12, abs=1e-15), k
+    for k in ("n_clipped", "n_bad_ids", "n_valid", "n_seq_valid"):
+        assert out[k] == g[k], k
+    np.testing.assert_allclose(out["grad_logp"], g["grad_logp"], rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(out["grad_entropy"], g["grad_entropy"], rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("A", [2.0, -3.0])
+def test_clip_exactly_on_the_bound_takes_the_interior_gradient(A):
+    """rho exactly on a bound (reading R4: strict inequalities): with eps = 0
+    and logp = old, rho = 1 is both bounds and the gradient is -A rho; with
+    eps_high = 1 and logp - old = ln 2 (rho = 2 exactly in fp64), likewise."""
+    ss = np.array([0, 1], np.int32)
+    mask = np.ones(1, np.uint8)
+    lp = np.array([-0.75])
+    out = O.ppo_clip_loss_fwd(lp, lp.copy(), None, np.array([A]), mask, ss, None, None,
+                              0.0, 0.0, 0.0, 0)
+    assert out["n_clipped"] == 0 and out["clipfrac"] == 0.0
+    assert out["grad_logp"][0] == -A
+    assert out["pg_loss"] == -A
+    old = lp - math.log(2.0)
+    assert math.exp(lp[0] - old[0]) == 2.0
+    out = O.ppo_clip_loss_fwd(lp, old, None, np.array([abs(A)]), mask, ss, None, None,
+                              0.0, 1.0, 0.0, 0)
+    assert out["n_clipped"] == 0 and out["grad_logp"][0] == -abs(A) * 2.0
+    # just past the bound: clipped, gradient 0, value at the bound
+    out = O.ppo_clip_loss_fwd(lp, old - 1e-9, None, np.array([abs(A)]), mask, ss, None, None,
+                              0.0, 1.0, 0.0, 0)
+    assert out["n_clipped"] == 1 and out["grad_logp"][0] == 0.0
+    assert out["pg_loss"] == -abs(A) * 2.0
+
+
+def test_clip_value_and_gradient_agree_near_a_bound():
+    """On tokens a hair inside and outside each bound the gradient is the
+    slope of the value: central differences of pg with a step far smaller
+    than the distance to the bound."""
+    ss = np.array([0, 1], np.int32)
+    mask = np.ones(1, np.uint8)
+    for A, rho in ((1.0, 1.2 * (1 - 1e-7)), (1.0, 1.2 * (1 + 1e-7)), (-1.0, 0.8 * (1 - 1e-7)),
+                   (-1.0, 0.8 * (1 + 1e-7))):
+        lp = np.array([-1.0])
+        old = lp - math.log(rho)
+        out = O.ppo_clip_loss_fwd(lp, old, None, np.array([A]), mask, ss, None, None,
+                                  0.2, 0.2, 0.0, 0)
+        h = 1e-11
+        f = lambda x: O.ppo_clip_loss_fwd(np.array([x]), old, None, np.array([A]), mask, ss,
+                                          None, None, 0.2, 0.2, 0.0, 0)["pg_loss"]
+        fd = (f(lp[0] + h) - f(lp[0] - h)) / (2 * h)
+        assert fd == pytest.approx(out["grad_logp"][0], rel=1e-3, abs=1e-6), (A, rho)
+
+
+def test_golden_mix_entropy_mean_over_every_valid_token():
+    """Under MIX the entropy mean covers every valid token, expert ones
+    included, while the GRPO metrics cover the non-expert rollouts
+    (hand-derived fixture, reading R10)."""
+    g = GOLD["mix_entropy_mean_scope"]
+    lp = np.array(g["logp"])
+    out = O.ppo_clip_loss_fwd(lp, lp.copy(), lp.copy(), np.array(g["adv"]), np.ones(3, np.uint8),
+                              np.array(g["seq_start"], np.int32), np.array(g["ids"]), g["V"],
+                              0.2, 0.2, 0.0, O.AGG_SEQ_MEAN_TOKEN_MEAN,
+                              entropy=np.array(g["entropy"]),
+                              is_expert=np.array(g["is_expert"], np.uint8), mix_mu=g["mu"])
+    for k in ("loss", "pg_loss", "sft_loss", "entropy_mean", "entropy_loss", "ratio_mean",
+              "clipfrac"):
+        assert out[k] == pytest.approx(g[k], rel=1e-13, abs=1e-15), k
+    assert out["n_expert"] == g["n_expert"] and out["n_valid"] == g["n_valid"]
+    np.testing.assert_allclose(out["grad_logp"], g["grad_logp"], rtol=1e-13)
+
+
 # --------------------------------------------------------------- gradients --
 def _loss_of(H, W, ids, mask, ss, old, ref, adv, eps_l, eps_h, beta, agg):
     lp, _, _ = O.token_logprobs(H, W, ids, mask)

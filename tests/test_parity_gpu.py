@@ -139,16 +139,25 @@ def test_loss_fwd_bit_exact_decisions(agg, eps_hi, denom):
     el, eh, be = oracle_eps(cfg)
     o = O.ppo_clip_loss_fwd(logp, old, ref, adv, b.mask, b.seq_start, b.ids, cfg.V, el, eh, be,
                             agg, denom, entropy=ent)
-    assert s["n_clipped"] == o["n_clipped"] and o["n_clipped"] > 0
+    # The kernel decides in fp32 on logp - old, the oracle by the definition
+    # in fp64: they may differ only for a token within 1e-6 of a bound.
+    near = o["margin"] < 1e-6
+    n_near = int(near.sum())
+    print(f"[loss-fwd agg={agg} eps_hi={eps_hi}] clipped {o['n_clipped']}, "
+          f"{n_near} tokens within 1e-6 of a bound", flush=True)
+    assert abs(s["n_clipped"] - o["n_clipped"]) <= n_near and o["n_clipped"] > 0
     assert s["n_valid"] == o["n_valid"] and s["n_seq_valid"] == o["n_seq_valid"]
     assert s["n_bad_ids"] == 0
-    for k in ("loss", "pg_loss", "kl_loss"):
+    for k in ("loss", "pg_loss", "kl_loss", "entropy_loss"):
         assert abs(s[k] - o[k]) <= TOL_LOSS_REL * abs(o[k]) + TOL_LOSS_ABS, (k, s[k], o[k])
-    for k in ("kl_mean", "ratio_mean", "clipfrac", "entropy_mean"):
+    for k in ("kl_mean", "ratio_mean", "entropy_mean"):
         assert abs(s[k] - o[k]) <= 1e-5 * max(1.0, abs(o[k])), (k, s[k], o[k])
+    assert abs(s["clipfrac"] - o["clipfrac"]) <= n_near / o["n_valid"] + 1e-12
     g = cpu(grad)
     assert np.all(g[~m] == 0)
-    np.testing.assert_allclose(g, o["grad_logp"], rtol=1e-4, atol=1e-7 * np.abs(o["grad_logp"]).max())
+    rows = o["weights_rows"][~near]
+    np.testing.assert_allclose(g[rows], o["grad_logp"][rows], rtol=1e-4,
+                               atol=1e-7 * np.abs(o["grad_logp"]).max())
 
 
 def test_loss_ratio_one_is_minus_mean_advantage():
@@ -307,8 +316,8 @@ def test_out_of_range_ids():
     assert np.all(g["dH"][valid[0]] == 0) and np.all(g["dH"][valid[5]] == 0)
     o = oracle_step(b, old, ref)
     assert o["fwd"]["n_bad_ids"] == 2
-    assert abs(g["stats"]["loss"] - o["fwd"]["loss"]) <= TOL_LOSS_REL * abs(o["fwd"]["loss"]) + TOL_LOSS_ABS
-    assert rel_fro(g["dW"], o["dW"]) <= TOL_GRAD_FRO
+    # every statistic, the per-token gradients and both weight gradients
+    compare_step(g, o, b)
 
 
 def test_run_to_run_determinism():
