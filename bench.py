@@ -8,6 +8,12 @@ log-probs and entropy through the lm_head (online log-sum-exp, logits kept only
 for one chunk of rows), the PPO-clip/KL loss, and the backward to the hidden
 states and the lm_head weight (the loss-only workload: log-softmax statistics,
 loss and d_logits from given logits in one fused call).  Prints one JSON line.
+
+The default run (the 7B-shape step) also frees that batch and times the
+loss-only workload (``lossonly``: its HBM fraction), and measures two ceilings
+on the same device (``ceilings``): a device copy moving the loss-only call's
+read and write bytes, and the best rate of the vendor bf16 GEMM (hipBLASLt
+through torch) on large shapes of the step's GEMMs.
 """
 from __future__ import annotations
 
@@ -93,6 +99,162 @@ def copy_probe(gb):
     ms = e0.elapsed_time(e1) / 3
     print(json.dumps({"copy_probe_bytes_each_way": n * 4, "ms_per_copy": ms,
                       "GB_per_s_read_plus_write": 2 * n * 4 / ms / 1e6}), flush=True)
+
+
+def _stats_ms(xs):
+    import numpy as np
+    a = np.asarray(xs, dtype=np.float64)
+    return {"median": float(np.median(a)), "mean": float(a.mean()), "min": float(a.min()),
+            "max": float(a.max())}
+
+
+def source_rev():
+    """git revision of the tree when .git is there, and a hash of the sources
+    that the measured path runs (the library sources, the header, this file),
+    which identifies the code also where the tree was copied without .git."""
+    import hashlib
+    import subprocess
+    rev = None
+    try:
+        r = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short=12", "HEAD"],
+                           capture_output=True, text=True, timeout=10)
+        if r.returncode == 0:
+            rev = r.stdout.strip()
+            d = subprocess.run(["git", "-C", ROOT, "status", "--porcelain", "--untracked-files=no"],
+                               capture_output=True, text=True, timeout=10)
+            if d.returncode == 0 and d.stdout.strip():
+                rev += "-dirty"
+    except Exception:
+        rev = None
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2505_17826_amd", "csrc")
+    for f in sorted(os.listdir(csrc)) + ["../../include/rft.h", "../../bench.py"]:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return {"git_rev": rev, "source_sha16": h.hexdigest()[:16]}
+
+
+def _time_events(fn, reps):
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, z in ev:
+        a.record()
+        fn()
+        z.record()
+    torch.cuda.synchronize()
+    return [a.elapsed_time(z) for a, z in ev]
+
+
+def measure_ceilings(read_gb, write_gb, reps=5):
+    """Ceilings measured on this device.
+
+    copy_mix: a device copy of read_gb gigabytes (read once, written once) plus
+    a fill of the remaining write_gb - read_gb gigabytes (written only), the
+    byte mix of the loss-only call (every valid row read once, every row of
+    d_logits written once); rate = (read_gb + write_gb) / (copy + fill time),
+    best of torch's copy and an elementwise copy kernel.
+    gemm_bf16: hipBLASLt (torch.matmul, bf16 in, fp32 accumulate) on the
+    shapes of the step's forward (M x V-slab x d) and d_hidden (M x d x V-slab)
+    GEMMs, best of the two, against the 2.5 PFLOP/s bf16 peak."""
+    import torch
+    out = {}
+    n_rd = int(read_gb * 1e9) // 4
+    n_fill = max(0, int((write_gb - read_gb) * 1e9) // 4)
+    x = torch.randn(n_rd, device="cuda")
+    y = torch.empty_like(x)
+    f = torch.empty(max(n_fill, 1), device="cuda")
+    for fn in (lambda: y.copy_(x), lambda: torch.mul(x, 1.0, out=y), lambda: f.zero_()):
+        fn()
+    torch.cuda.synchronize()
+    best = None
+    for name, cp in (("torch copy_", lambda: y.copy_(x)),
+                     ("elementwise mul by 1", lambda: torch.mul(x, 1.0, out=y))):
+        t_cp = _stats_ms(_time_events(cp, reps))["median"]
+        t_fill = _stats_ms(_time_events(lambda: f.zero_(), reps))["median"] if n_fill else 0.0
+        gbs = (read_gb + write_gb) / ((t_cp + t_fill) / 1e3)
+        if best is None or gbs > best["GB_per_s"]:
+            best = {"GB_per_s": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS, "kernel": name,
+                    "copy_ms": t_cp, "fill_ms": t_fill, "read_GB": read_gb, "write_GB": write_gb}
+    out["copy_mix"] = best
+    del x, y, f
+    torch.cuda.empty_cache()
+    gemms = []
+    for (M, Nn, K, what) in ((32768, 19008, 3584, "forward-like: rows x V/8 x d"),
+                             (32768, 3584, 38016, "d_hidden-like: rows x d x V/4")):
+        a = torch.randn(M, K, device="cuda").to(torch.bfloat16)
+        bT = torch.randn(Nn, K, device="cuda").to(torch.bfloat16)
+        mm = lambda: torch.matmul(a, bT.t())
+        mm()
+        torch.cuda.synchronize()
+        ms = _stats_ms(_time_events(mm, reps))["median"]
+        tf = 2.0 * M * Nn * K / (ms / 1e3) / 1e12
+        gemms.append({"shape": [M, Nn, K], "what": what, "ms": ms, "TFLOP_per_s": tf,
+                      "frac_of_peak": tf / PEAK_BF16_TFLOPS})
+        del a, bT
+        torch.cuda.empty_cache()
+    best_g = max(gemms, key=lambda g: g["TFLOP_per_s"])
+    out["gemm_bf16"] = {"TFLOP_per_s": best_g["TFLOP_per_s"],
+                        "frac_of_peak": best_g["frac_of_peak"],
+                        "kernel": "hipBLASLt via torch.matmul (NT, bf16)", "shapes": gemms}
+    return out
+
+
+def measure_lossonly(R, synth, dev, steps, warmup):
+    """The loss-only workload (fp32 logits [32768, 151936], 10% of rows masked):
+    group advantages + rft_ppo_clip_fused_logits per step; per-call event
+    times of the fused call, its algorithmic bytes and HBM fraction."""
+    import numpy as np
+    import torch
+    cfg = synth.config(4)
+    b = synth.make_batch(cfg, dev)
+    tok = R.Tokens(b.seq_start, b.mask, b.ids)
+    N = int(b.mask.sum().item())
+    T, V = b.T, cfg.V
+    params = R.ppo_params(cfg.eps_low, cfg.eps_high, cfg.beta, cfg.agg)
+    f32 = dict(dtype=torch.float32, device=dev)
+    adv = torch.empty(cfg.n_seq, **f32)
+    logp, ent, lse, grad = (torch.empty(T, **f32) for _ in range(4))
+    stats = torch.zeros(R.STATS_BYTES, dtype=torch.uint8, device=dev)
+    dl = torch.empty_like(b.logits)
+    ws = torch.empty(max(1, R.workspace_bytes(R.RFT_OP_PPO_FUSED_LOGITS, tok, 0, V)),
+                     dtype=torch.uint8, device=dev)
+    R.rft_token_logprobs_from_logits(tok, b.logits, logp=logp, entropy=ent, lse=lse)
+    old = torch.where(b.mask.bool(), logp + b.old_noise, torch.zeros_like(logp))
+    ref = torch.where(b.mask.bool(), logp + b.ref_noise, torch.zeros_like(logp))
+    evs = []
+
+    def step(ev=None):
+        R.rft_group_advantages(b.rewards, cfg.group, out=adv)
+        if ev is not None:
+            ev[0].record()
+        R.rft_ppo_clip_fused_logits(tok, b.logits, old, ref, adv, params, logp=logp, entropy=ent,
+                                    lse=lse, grad_logp=grad, d_logits=dl, stats=stats, ws=ws)
+        if ev is not None:
+            ev[1].record()
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    call_ms = [a.elapsed_time(z) for a, z in evs]
+    st = _stats_ms(call_ms)
+    gb = (N * V * 4 + T * V * 4) / 1e9
+    res = {"workload": cfg.name, "valid_tokens": N, "T": T, "V": V,
+           "kernel": "k_logits_fused_cached (one workgroup per row: stats, loss, d_logits)",
+           "calls": steps, "ms_per_call": st, "algorithmic_GB_per_call": gb,
+           "GB_per_s": gb / (st["mean"] / 1e3), "GB_per_s_median": gb / (st["median"] / 1e3),
+           "peak_GB_per_s": PEAK_HBM_GBS, "frac": gb / (st["mean"] / 1e3) / PEAK_HBM_GBS,
+           "tokens_per_s": N / (st["median"] / 1e3),
+           "traffic": traffic_gb("lossonly"), "traffic_unit": "GB per launch",
+           "loss": R.stats_to_dict(stats)["loss"],
+           "read_GB": N * V * 4 / 1e9, "write_GB": T * V * 4 / 1e9}
+    del b, dl, ws
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(batch, target_s, extra):
@@ -262,6 +424,10 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # per step: one event pair around the whole step (advantages + the call)
+    # and one around the call alone (the dominant launch sequence)
+    sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
@@ -269,10 +435,14 @@ def main():
     torch.cuda.synchronize()
     t_start.record()
     for k in range(args.steps):
+        sev[k][0].record()
         step(evs[k])
+        sev[k][1].record()
     t_end.record()
     torch.cuda.synchronize()
-    ms = t_start.elapsed_time(t_end) / max(args.steps, 1)
+    ms_total = t_start.elapsed_time(t_end) / max(args.steps, 1)
+    step_ms = _stats_ms([a.elapsed_time(z) for a, z in sev])
+    ms = step_ms["median"]
     dom_ms = float(np.mean([a.elapsed_time(z) for a, z in evs])) if args.steps else float("nan")
     st = R.stats_to_dict(stats)
     tokens_per_s = N / (ms / 1e3)
@@ -280,6 +450,8 @@ def main():
     out = {
         "metric": METRIC, "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "ms_per_step_stats": {**step_ms, "mean_over_timed_region": ms_total,
+                              "note": "value and ms_per_step use the median step"},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": {"bf16": "bf16", "f32": "f32", "logits": "f32"}[cfg.dtype],
         "data": "synthetic (seeded; shapes and distributions of the workload, no dataset)",
@@ -314,6 +486,19 @@ def main():
             "traffic": traffic_gb(args.workload), "traffic_unit": "GB per launch"}
     out["loss"] = st["loss"]
     out["clipfrac"] = st["clipfrac"]
+    out["rev"] = source_rev()
+    if cfg.dtype == "logits":
+        lo_read, lo_write = N * V * 4 / 1e9, T * V * 4 / 1e9
+    else:
+        # the second target: the loss-only workload's HBM fraction, timed after
+        # this workload's buffers are freed
+        del dH, dW, ws_fwd, ws_step
+        torch.cuda.empty_cache()
+        print("[bench] loss-only workload", file=sys.stderr, flush=True)
+        out["lossonly"] = measure_lossonly(R, synth, dev, max(args.steps, 5), args.warmup)
+        lo_read, lo_write = out["lossonly"]["read_GB"], out["lossonly"]["write_GB"]
+    print("[bench] ceilings", file=sys.stderr, flush=True)
+    out["ceilings"] = measure_ceilings(lo_read, lo_write)
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on a CPU sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(b, args.cpu_seconds, {})

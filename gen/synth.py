@@ -14,6 +14,9 @@ large arrays):
   input dtype with round-to-nearest-even.  Masked rows of ``H`` are zero, or
   NaN when ``poison=True``.
 * Loss-only workload: ``logits[T, V]`` ~ N(0, 2^2) in fp32.
+* ``logit_std`` (2 by default, the value above) scales W or the given logits;
+  the stress tests raise it to 10-20, the spread of a trained model's logits,
+  so that rows are peaked (a few entries carry most of the probability).
 * Token ids are drawn from softmax of the rollout logits ``h . W^T`` (or of
   ``logits``) by the Gumbel-max rule ``argmax_j (z_j - log(-log u_j))``.
   This stands in for the rollout model of the explorer, not for the trainer;
@@ -67,6 +70,7 @@ class Config:
     mask_frac: float = 0.0
     old_var: float = 0.05
     ref_var: float = 0.1
+    logit_std: float = 2.0     # std of the logits: W = logit_std N(0,1)/sqrt(d), or given logits
 
     @property
     def n_seq(self) -> int:
@@ -207,7 +211,7 @@ def make_batch(cfg: Config, device="cpu", poison: bool = False, seed_key=None,
             H[r0:r1] = torch.randn((r1 - r0, cfg.d), generator=gH, device=dev).to(tdt)
         gW = _torch_gen(key, "W", dev)
         W = torch.empty((cfg.V, cfg.d), dtype=tdt, device=dev)
-        scale = 2.0 / math.sqrt(cfg.d)
+        scale = cfg.logit_std / math.sqrt(cfg.d)
         for r0 in range(0, cfg.V, chunk_rows):
             r1 = min(cfg.V, r0 + chunk_rows)
             W[r0:r1] = (torch.randn((r1 - r0, cfg.d), generator=gW, device=dev) * scale).to(tdt)
@@ -223,7 +227,7 @@ def make_batch(cfg: Config, device="cpu", poison: bool = False, seed_key=None,
         logits = torch.empty((T, cfg.V), dtype=torch.float32, device=dev)
         for r0 in range(0, T, chunk_rows):
             r1 = min(T, r0 + chunk_rows)
-            logits[r0:r1] = torch.randn((r1 - r0, cfg.V), generator=gL, device=dev) * 2.0
+            logits[r0:r1] = torch.randn((r1 - r0, cfg.V), generator=gL, device=dev) * cfg.logit_std
         for c0 in range(0, valid_rows.numel(), chunk_rows):
             rr = valid_rows[c0:c0 + chunk_rows]
             ids[rr] = _gumbel_argmax(logits[rr], g_samp)

@@ -130,7 +130,7 @@ typedef struct {
   double loss;          /* pg_loss + kl_loss (MIX: see above)        */
   double pg_loss;       /* sum_t w_t * clipped surrogate              */
   double kl_loss;       /* sum_t w_t * beta * kl_t                    */
-  double kl_mean;       /* mean over on-policy tokens of kl_t         */
+  double kl_mean;       /* mean over on-policy tokens of kl_t (0 without ref_logp) */
   double entropy_mean;  /* mean over valid tokens of entropy (0 if no entropy given) */
   double ratio_mean;    /* mean over on-policy tokens of exp(logp - old) */
   double clipfrac;      /* n_clipped / on-policy tokens               */
@@ -254,7 +254,9 @@ rft_status rft_token_logprobs_from_logits(const rft_tokens* tok, const float* lo
  * (strict: on a bound the gradient is -A rho).  The test is taken in fp32 on
  * logp - old against fp32(log(1 +/- eps)); it agrees with the exact test
  * except for a token within fp32 rounding (about 1e-7 relative) of a bound.
- * Inputs f32 [T] (adv is [n_seq]); ref_logp may be NULL iff kl_coef == 0;
+ * Inputs f32 [T] (adv is [n_seq]); ref_logp may be NULL when kl_coef == 0
+ * (no KL: kl_mean is 0); when given, kl_mean reports the KL to it whatever
+ * kl_coef, as a metric;
  * entropy may be NULL (entropy_mean 0) unless entropy_coef > 0.  Outputs:
  * grad_logp [T] (0 on masked rows), *stats (device), and, if not NULL,
  * grad_entropy [T]: e_t = d loss / d H_t times -1, i.e. the coefficient of

@@ -348,7 +348,8 @@ def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, e
     T = lp_all.size
     lp = lp_all[rows]
     old = _f64(old_logp)[rows]
-    ref = _f64(ref_logp)[rows] if ref_logp is not None else np.zeros_like(lp)
+    # without a reference policy there is no KL term: ref = logp, kl = 0
+    ref = _f64(ref_logp)[rows] if ref_logp is not None else lp.copy()
     A = _f64(adv_seq)[seq]
     good = np.ones(rows.size, dtype=bool)
     if ids is not None and V is not None:
@@ -373,12 +374,15 @@ def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, e
     clipped = ((A > 0) & (rho > hi)) | ((A < 0) & (rho < lo))
     dk = ref - lp
     kl = np.exp(dk) - dk - 1.0
-    ell = pg + beta * kl
-    g = np.where(clipped, 0.0, -A * rho) + beta * (1.0 - np.exp(dk))
+    # beta = 0 switches the KL term off (kl is still reported as a metric)
+    bkl = beta * kl if beta > 0 else np.zeros_like(kl)
+    ell = pg + bkl
+    g = np.where(clipped, 0.0, -A * rho) + (beta * (1.0 - np.exp(dk)) if beta > 0 else 0.0)
     c = w * g
     # bad ids contribute nothing
     pg = np.where(good, pg, 0.0)
     kl = np.where(good, kl, 0.0)
+    bkl = np.where(good, bkl, 0.0)
     ell = np.where(good, ell, 0.0)
     c = np.where(good, c, 0.0)
     clipped = clipped & good
@@ -396,7 +400,7 @@ def _grpo_loss_fwd(logp, old_logp, ref_logp, adv_seq, mask, seq_start, ids, V, e
         "loss": float((w * ell).sum()) - entropy_coef * ent_w,
         "entropy_loss": ent_w, "grad_entropy": grad_ent,
         "pg_loss": float((w * pg).sum()),
-        "kl_loss": float((w * beta * kl).sum()),
+        "kl_loss": float((w * bkl).sum()),
         "kl_mean": float(kl.sum() / N) if N else 0.0,
         "ratio_mean": float(rho_s.sum() / N) if N else 0.0,
         "clipfrac": float(clipped.sum() / N) if N else 0.0,

@@ -502,7 +502,7 @@ rft_status rft_ppo_clip_loss_fwd(const rft_tokens* tok, int64_t V, const float* 
   hipStream_t s = (hipStream_t)stream;
   RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
   LossConst c = loss_const(params, V, *tok);
-  RFT_HIP(launch_loss_fwd(*tok, w.m, logp, old_logp, params->kl_coef > 0.f ? ref_logp : nullptr,
+  RFT_HIP(launch_loss_fwd(*tok, w.m, logp, old_logp, ref_logp,
                           adv, entropy, c, grad_logp, grad_entropy, w.parts, stats, s),
           fn);
   return RFT_OK;
@@ -625,7 +625,7 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
   RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
   LossConst c = loss_const(params, V, *tok);
   RFT_HIP(launch_logits_fused(logits, *tok, w.m, V, old_logp,
-                              params->kl_coef > 0.f ? ref_logp : nullptr, adv, c, logp, entropy,
+                              ref_logp, adv, c, logp, entropy,
                               lse, grad_logp, d_logits, w.parts, stats, s),
           fn);
   return RFT_OK;
@@ -650,7 +650,7 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
     return fail(RFT_E_NULL, "%s: ref_logp is NULL with kl_coef > 0", fn);
   if (tok->T > 0 && params->entropy_coef > 0.f && !entropy)
     return fail(RFT_E_NULL, "%s: entropy is NULL with entropy_coef > 0", fn);
-  const float* ref = params->kl_coef > 0.f ? ref_logp : nullptr;
+  const float* ref = ref_logp;
   const bool bonus = params->entropy_coef > 0.f;
   if (dtype == RFT_F32) {
     if ((st = check_ws(fn, ws, ws_bytes, step_f32_bytes(*tok, d, V, bwd_align(dtype))))) return st;

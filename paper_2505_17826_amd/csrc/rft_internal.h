@@ -186,7 +186,9 @@ __device__ __forceinline__ TokLoss token_loss(float lp, float old, float ref, fl
   float dk = ref - lp;
   float em1 = expm1f(dk);
   r.kl = em1 - dk;
-  r.g = (r.clipped ? 0.f : -A * r.rho) - c.beta * em1;
+  // with beta = 0 the KL term is off: kl stays a metric and adds nothing
+  // (not even a NaN from 0 * inf) to the loss or the gradient
+  r.g = (r.clipped ? 0.f : -A * r.rho) - (c.beta > 0.f ? c.beta * em1 : 0.f);
   return r;
 }
 
@@ -219,9 +221,10 @@ __device__ __forceinline__ float row_loss(float lp, float old, float ref, float 
   const int Ng = meta[0] - meta[2], Sg = meta[1] - meta[3];
   TokLoss L = token_loss(lp, old, ref, A, n_seq_i, Ng, Sg, c);
   const double scale = c.mix ? 1.0 - (double)c.mu : 1.0;
-  p.loss = scale * (L.w * ((double)L.pg + (double)c.beta * (double)L.kl));
+  const double bkl = c.beta > 0.f ? (double)c.beta * (double)L.kl : 0.0;
+  p.loss = scale * (L.w * ((double)L.pg + bkl));
   p.pg = L.w * (double)L.pg;
-  p.klw = L.w * (double)c.beta * (double)L.kl;
+  p.klw = L.w * bkl;
   p.kl = (double)L.kl;
   p.ratio = (double)L.rho;
   p.clipped = L.clipped ? 1 : 0;

@@ -333,6 +333,25 @@ def test_kl_properties():
     assert o1["kl_mean"] == pytest.approx(g["kl"], rel=1e-13)
 
 
+def test_kl_off_at_zero_coefficient():
+    """beta = 0 switches the KL term off: the loss and gradient equal those
+    without a reference, even where the reference makes kl overflow to inf
+    (ref - logp = 1000); kl_mean still reports the KL to the given reference,
+    and no reference means no KL (kl_mean 0)."""
+    ss, mask, logp, old, ref, adv, ids, V = _loss_case(seed=31)
+    none = O.ppo_clip_loss_fwd(logp, old, None, adv, mask, ss, ids, V, 0.2, 0.2, 0.0, 0)
+    far = O.ppo_clip_loss_fwd(logp, old, logp + 1000.0, adv, mask, ss, ids, V, 0.2, 0.2, 0.0, 0)
+    assert none["kl_mean"] == 0.0 and none["kl_loss"] == 0.0
+    assert far["loss"] == none["loss"] and far["kl_loss"] == 0.0
+    np.testing.assert_array_equal(far["grad_logp"], none["grad_logp"])
+    assert far["kl_mean"] == math.inf
+    near = O.ppo_clip_loss_fwd(logp, old, ref, adv, mask, ss, ids, V, 0.2, 0.2, 0.0, 0)
+    c = O.token_counts(mask, ss)
+    d = (ref - logp)[c["rows"]]
+    assert near["kl_mean"] == pytest.approx(float((np.exp(d) - d - 1).mean()), rel=1e-12)
+    assert near["loss"] == none["loss"]
+
+
 def test_aggregations_coincide_on_equal_lengths():
     rng = np.random.default_rng(9)
     ss = np.arange(5, dtype=np.int32) * 6
