@@ -13,7 +13,7 @@ import torch
 import paper_2505_17826_amd as R
 from gen import synth
 from oracle import rft_oracle as O
-from tests.gpu_cases import (TOL_GRAD_FRO, TOL_LOGP, TOL_LOSS_ABS, TOL_LOSS_REL, cpu, f32,
+from tests.gpu_cases import (TOL_GRAD_FRO, TOL_LOGP, TOL_LOSS_ABS, TOL_LOSS_REL, cpu, f32, near_bound,
                              oracle_eps, params_of, rel_fro, requires_gpu)
 
 pytestmark = [pytest.mark.gpu, requires_gpu]
