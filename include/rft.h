@@ -325,6 +325,27 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
                                      float* d_logits, rft_ppo_stats* stats, void* ws,
                                      size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * call as rft_ppo_clip_fused_logits with the same arguments, results and
+ * errors, but no workspace argument.  Its scratch (token bookkeeping and one
+ * loss partial per row) lives in a device array inside the library, of
+ * rft_noalloc_scratch_bytes() bytes (16 MiB) per GPU, held until the process
+ * ends; the call itself allocates and frees nothing.  Limit: the scratch the
+ * layout needs must fit, which holds for T <= 131072 rows with n_seq <= T
+ * (100 bytes per row plus 4 per rollout, rounded up); a larger layout returns
+ * RFT_E_WORKSPACE before anything is enqueued.  Every call on one GPU shares
+ * that GPU's array: calls that overlap on one GPU (other streams, other host
+ * threads) race and give wrong results, so serialise them.  The array keeps
+ * the last call's contents; nothing in it needs to start at zero. */
+size_t rft_noalloc_scratch_bytes(void);
+rft_status rft_ppo_clip_fused_logits_noalloc(const rft_tokens* tok, const float* logits, int64_t V,
+                                             const float* old_logp, const float* ref_logp,
+                                             const float* adv, const rft_ppo_params* params,
+                                             float* logp, float* entropy, float* lse,
+                                             float* grad_logp, float* d_logits,
+                                             rft_ppo_stats* stats, void* stream);
+
 /* The whole trainer-side step of the policy head in one call (Sec. 3: the
  * trainer's update with the PPO-clip surrogate, k3 KL to the reference model
  * and GRPO advantages, over the masked response tokens): the outputs of

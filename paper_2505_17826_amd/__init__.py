@@ -71,6 +71,10 @@ _SIGS = {
                                               ctypes.c_int]),
     "rft_workspace_min_bytes": (ctypes.c_size_t, [ctypes.c_int, ctypes.POINTER(rft_tokens), _i64,
                                                   _i64, ctypes.c_int]),
+    "rft_noalloc_scratch_bytes": (ctypes.c_size_t, []),
+    "rft_ppo_clip_fused_logits_noalloc": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _i64, _p,
+                                                         _p, _p, ctypes.POINTER(rft_ppo_params),
+                                                         _p, _p, _p, _p, _p, _p, _p]),
     "rft_chunk_rows": (_i64, [ctypes.c_int, ctypes.POINTER(rft_tokens), _i64, _i64, ctypes.c_int,
                               ctypes.c_size_t]),
     "rft_group_advantages": (ctypes.c_int, [_p, _i64, ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
@@ -340,6 +344,20 @@ def rft_ppo_clip_fused_logits(tokens: Tokens, logits, old_logp, ref_logp, adv, p
                                            _ptr(logp), _ptr(entropy), _ptr(lse), _ptr(grad_logp),
                                            _ptr(d_logits), _ptr(stats), _ptr(ws), nb,
                                            _stream(stream)))
+    return logp, d_logits, stats
+
+
+def rft_ppo_clip_fused_logits_noalloc(tokens: Tokens, logits, old_logp, ref_logp, adv, params,
+                                      logp, d_logits, stats, entropy=None, lse=None,
+                                      grad_logp=None, stream=None):
+    """rft_ppo_clip_fused_logits without a workspace: the library's own scratch
+    array is used and nothing is allocated, so every output must be given."""
+    _need_gpu(logits, old_logp, adv, logp, d_logits, stats)
+    tk = tokens.c()
+    _check(lib().rft_ppo_clip_fused_logits_noalloc(
+        ctypes.byref(tk), _ptr(logits), logits.shape[1], _ptr(old_logp), _ptr(ref_logp),
+        _ptr(adv), ctypes.byref(params), _ptr(logp), _ptr(entropy), _ptr(lse), _ptr(grad_logp),
+        _ptr(d_logits), _ptr(stats), _stream(stream)))
     return logp, d_logits, stats
 
 

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <algorithm>
 #include <limits>
+#include <mutex>
 #include <string>
 
 #include "rft_internal.h"
@@ -314,6 +315,56 @@ size_t step_f32_bytes(const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
   return step_f32_front(tok, d, V, Tc) + (size_t)round_up((tok.T > 0 ? tok.T : 1) * 4, 256);
 }
 
+rft_status check_fused_logits(const char* fn, const rft_tokens* tok, const float* logits, int64_t V,
+                              const float* old_logp, const float* ref_logp, const float* adv,
+                              const rft_ppo_params* params, const float* logp,
+                              const float* d_logits, const rft_ppo_stats* stats) {
+  rft_status st = check_tokens(tok, fn);
+  if (st) return st;
+  if ((st = check_params(params, fn))) return st;
+  if (V < 1 || V > (int64_t)std::numeric_limits<int32_t>::max() / 2)
+    return fail(RFT_E_SHAPE, "%s: V=%lld", fn, (long long)V);
+  if (!stats) return fail(RFT_E_NULL, "%s: stats is NULL", fn);
+  if (tok->T > 0 && (!logits || !old_logp || !adv || !logp || !d_logits))
+    return fail(RFT_E_NULL, "%s: logits / old_logp / adv / logp / d_logits is NULL", fn);
+  if (tok->T > 0 && params->kl_coef > 0.f && !ref_logp)
+    return fail(RFT_E_NULL, "%s: ref_logp is NULL with kl_coef > 0", fn);
+  return RFT_OK;
+}
+
+// Scratch of the entry point that allocates nothing
+// (rft_ppo_clip_fused_logits_noalloc): the workspace of the loss-only call
+// (token bookkeeping and one loss partial per row) in a file-scope device
+// array.  Each GPU holds its own copy for the life of the process; in host
+// code `scratch` only names the symbol, so kernels get the device address
+// looked up once per device (scratch_ptr).
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+constexpr int kNoAllocMaxDevices = 64;
+__attribute__((used)) static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kNoAllocMaxDevices] = {};
+
+// Device address of this device's scratch array (looked up on the first call
+// on each device, with that device current); nullptr and *e set on failure.
+void* scratch_ptr(hipError_t* e) {
+  int dev = -1;
+  *e = hipGetDevice(&dev);
+  if (*e != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= kNoAllocMaxDevices) {
+    *e = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    *e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (*e != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 // ================================================================== ABI ==
@@ -608,16 +659,9 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
                                      float* d_logits, rft_ppo_stats* stats, void* ws,
                                      size_t ws_bytes, void* stream) {
   const char* fn = "rft_ppo_clip_fused_logits";
-  rft_status st = check_tokens(tok, fn);
+  rft_status st = check_fused_logits(fn, tok, logits, V, old_logp, ref_logp, adv, params, logp,
+                                     d_logits, stats);
   if (st) return st;
-  if ((st = check_params(params, fn))) return st;
-  if (V < 1 || V > (int64_t)std::numeric_limits<int32_t>::max() / 2)
-    return fail(RFT_E_SHAPE, "%s: V=%lld", fn, (long long)V);
-  if (!stats) return fail(RFT_E_NULL, "%s: stats is NULL", fn);
-  if (tok->T > 0 && (!logits || !old_logp || !adv || !logp || !d_logits))
-    return fail(RFT_E_NULL, "%s: logits / old_logp / adv / logp / d_logits is NULL", fn);
-  if (tok->T > 0 && params->kl_coef > 0.f && !ref_logp)
-    return fail(RFT_E_NULL, "%s: ref_logp is NULL with kl_coef > 0", fn);
   LossWs w = carve_loss(nullptr, *tok, true);
   if ((st = check_ws(fn, ws, ws_bytes, w.bytes))) return st;
   w = carve_loss(ws, *tok, true);
@@ -629,6 +673,35 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
                               lse, grad_logp, d_logits, w.parts, stats, s),
           fn);
   return RFT_OK;
+}
+
+size_t rft_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+rft_status rft_ppo_clip_fused_logits_noalloc(const rft_tokens* tok, const float* logits, int64_t V,
+                                             const float* old_logp, const float* ref_logp,
+                                             const float* adv, const rft_ppo_params* params,
+                                             float* logp, float* entropy, float* lse,
+                                             float* grad_logp, float* d_logits,
+                                             rft_ppo_stats* stats, void* stream) {
+  const char* fn = "rft_ppo_clip_fused_logits_noalloc";
+  rft_status st = check_fused_logits(fn, tok, logits, V, old_logp, ref_logp, adv, params, logp,
+                                     d_logits, stats);
+  if (st) return st;
+  const size_t need = carve_loss(nullptr, *tok, true).bytes;
+  if (need > kNoAllocScratchBytes)
+    return fail(RFT_E_WORKSPACE,
+                "%s: T=%lld rows and n_seq=%lld rollouts need %zu bytes of scratch, more than "
+                "the %zu the library holds; use rft_ppo_clip_fused_logits with a workspace",
+                fn, (long long)tok->T, (long long)tok->n_seq, need, kNoAllocScratchBytes);
+  hipError_t e = hipSuccess;
+  void* ws = scratch_ptr(&e);
+  if (!ws) return hip_fail(e, fn);
+  // every byte of the scratch that the call reads it writes first (the
+  // bookkeeping kernels fill their arrays, every row writes its partial), so
+  // the previous call's contents need no clearing
+  return rft_ppo_clip_fused_logits(tok, logits, V, old_logp, ref_logp, adv, params, logp, entropy,
+                                   lse, grad_logp, d_logits, stats, ws, kNoAllocScratchBytes,
+                                   stream);
 }
 
 rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const void* weight,

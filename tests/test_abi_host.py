@@ -247,3 +247,22 @@ def test_chunk_rows_are_bounded_for_huge_row_counts():
     ws = L.rft_workspace_bytes(R.RFT_OP_PPO_STEP, ctypes.byref(tk), 256, 5000, R.RFT_BF16)
     assert L.rft_chunk_rows(R.RFT_OP_PPO_STEP, ctypes.byref(tk), 256, 5000, R.RFT_BF16, ws) == 4096
     assert L.rft_chunk_rows(R.RFT_OP_PPO_FWD, ctypes.byref(tk), 256, 5000, R.RFT_BF16, ws) == 0
+
+
+def test_noalloc_entry_point_rejects_layouts_beyond_its_scratch():
+    """The entry point without a workspace refuses, before any device call, a
+    layout whose bookkeeping does not fit the library's scratch array."""
+    L = R.lib()
+    assert L.rft_noalloc_scratch_bytes() == 16 << 20
+    fake = ctypes.c_void_p(0x1000)
+    p = R.ppo_params()
+    args = lambda tk: (ctypes.byref(tk), fake, 4, fake, fake, fake, ctypes.byref(p), fake, None,
+                       None, None, fake, fake, None)
+    st = L.rft_ppo_clip_fused_logits_noalloc(*args(_tok(T=200000, n_seq=1)))
+    assert st == R.RFT_E_WORKSPACE
+    assert b"scratch" in L.rft_last_error()
+    # argument errors come first, as in the call with a workspace
+    st = L.rft_ppo_clip_fused_logits_noalloc(ctypes.byref(_tok(T=8, n_seq=2)), fake, 0, fake, fake,
+                                             fake, ctypes.byref(p), fake, None, None, None, fake,
+                                             fake, None)
+    assert st == R.RFT_E_SHAPE
