@@ -263,6 +263,7 @@ constexpr int REG = 56;                  // float4 per thread held in registers
 constexpr int REG_ENT = 54;              // the same with the entropy-bonus term (no spills)
 constexpr int LCAP = 18 * NTC;           // float4 held in LDS (144 KiB)
 constexpr size_t kCachedLds = (size_t)LCAP * 16;
+static_assert(LCAP % NTC == 0, "every thread fills the same number of LDS slots");
 
 // d_logits of four logits; ENT adds the entropy-bonus term e p (z - mu)
 template <bool ENT>
@@ -325,8 +326,32 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
     }
     return;
   }
-  // pass 1: registers, then LDS, then the rest (chunks past the row read as 0
-  // and are left out of the statistics)
+  // The row's scalars for the loss terms (uniform over the workgroup: scalar
+  // loads), issued now so that they have arrived when pass 1 ends.
+  const int y0 = ids[t];
+  const bool ok = y0 >= 0 && (int64_t)y0 < V;
+  const float zy = ok ? logits[t * V + y0] : 0.f;
+  const int i_seq = row_seq[k];
+  const float old_t = old[t], ref_t = ref ? ref[t] : 0.f, adv_i = adv[i_seq];
+  const int n_seq_i = n_i[i_seq];
+  const int32_t meta4[4] = {meta[0], meta[1], meta[2], meta[3]};
+
+  // pass 1.  The LDS part of the row goes straight from HBM into LDS
+  // (buffer_load ... lds, all of a lane's chunks in flight at once: lane l of
+  // wave w fills slot s = c NTC + 64 w + l with chunk j_lds + s, the slot the
+  // same thread reads back), then the register part, then the rest; chunks
+  // past the row read as 0 and are left out of the statistics.
+  const int64_t j_lds = (int64_t)REGS * NTC, j_rest = j_lds + LCAP;
+  {
+    const int w = tid >> 6;
+#pragma unroll
+    for (int c = 0; c < LCAP / NTC; ++c) {
+      const int64_t j = j_lds + (int64_t)c * NTC + tid;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rin, (__attribute__((address_space(3))) void*)(row_lds + c * NTC + w * 64), 16,
+          j < n4 ? (uint32_t)(j * 16) : 0x80000000u, 0, 0, 2);
+    }
+  }
   const int u_full = (int)min((int64_t)REGS, n4 / NTC);  // chunks complete for every thread
   // a lane whose chunk lies past the row takes a vector offset of 2^31, out of
   // range for the descriptor whether or not the scalar offset is counted
@@ -341,22 +366,19 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
   for (int u = 0; u < REGS; ++u) {
     if (u < u_full || (u == u_full && tid + (int64_t)u * NTC < n4)) acc4v(r, regs[u]);
   }
-  const int64_t j_lds = (int64_t)REGS * NTC, j_rest = j_lds + LCAP;
-  for (int64_t j = j_lds + tid, s_ = tid; j < n4 && s_ < LCAP; j += NTC, s_ += NTC) {
-    floatx4 q = (floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, (uint32_t)(j * 16), 0, 2);
-    row_lds[s_] = q;
-    acc4v(r, q);
-  }
+  // the direct-to-LDS loads have landed: this wave's loads are all back
+  // (vmcnt 0), then the barrier (each thread reads back only its own slots)
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+  __syncthreads();
+  for (int64_t j = j_lds + tid, s_ = tid; j < n4 && s_ < LCAP; j += NTC, s_ += NTC)
+    acc4v(r, row_lds[s_]);
   for (int64_t j = j_rest + tid; j < n4; j += NTC)
     acc4v(r, (floatx4)__builtin_amdgcn_raw_buffer_load_b128(rin, (uint32_t)(j * 16), 0, 0));
   r = block_stats<NTC>(r, sh);
-  const float* z = logits + t * V;
   if (tid == 0) {
     float L = r.m + logf(r.s);
     float H = L - r.u / r.s;
-    int y = ids[t];
-    bool ok = y >= 0 && (int64_t)y < V;
-    float lp = ok ? z[y] - L : __int_as_float(0x7fc00000);
+    float lp = ok ? zy - L : __int_as_float(0x7fc00000);
     logp[t] = lp;
     if (ent) ent[t] = H;
     if (lse_out) lse_out[t] = L;
@@ -365,12 +387,11 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
     if (!ok) {
       p.bad = 1;
     } else {
-      int i = row_seq[k];
-      float rf = ref ? ref[t] : lp;
-      const bool ex = cst.is_expert && cst.is_expert[i];
+      float rf = ref ? ref_t : lp;
+      const bool ex = cst.is_expert && cst.is_expert[i_seq];  // MIX only
       LossConst cc = cst;
       if (!ENT) cc.ent_coef = 0.f;  // the launcher picks ENT = (ent_coef > 0)
-      c = row_loss(lp, old[t], rf, adv[i], n_i[i], ex, meta, (double)H, cc, p, &e);
+      c = row_loss(lp, old_t, rf, adv_i, n_seq_i, ex, meta4, (double)H, cc, p, &e);
     }
     if (grad_out) grad_out[t] = c;
     parts[t] = p;
@@ -381,8 +402,7 @@ __global__ void __launch_bounds__(NTC) k_logits_fused_cached(
   }
   __syncthreads();
   const float c = row_c, lk = sh[NTC / 64].m * kLog2e, e = row_e, mu = row_mu;
-  int y = ids[t];
-  y = (y >= 0 && (int64_t)y < V) ? y : -1;
+  const int y = ok ? y0 : -1;
   // pass 2: same three regions; stores past the row are dropped by the descriptor
   uint32_t vo2 = vo;
   int nv2 = nv;
