@@ -261,7 +261,9 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 constexpr int NTC = NT;                  // 2 waves per SIMD
 constexpr int REG = 56;                  // float4 per thread held in registers
 constexpr int REG_ENT = 54;              // the same with the entropy-bonus term (no spills)
-constexpr int LCAP = 18 * NTC;           // float4 held in LDS (144 KiB)
+// float4 held in LDS (152 KiB): with the registers, rows of up to 153600
+// fp32 logits stay on chip (both vocabularies of the workloads)
+constexpr int LCAP = 19 * NTC;
 constexpr size_t kCachedLds = (size_t)LCAP * 16;
 static_assert(LCAP % NTC == 0, "every thread fills the same number of LDS slots");
 

@@ -180,10 +180,11 @@ def test_loss_ratio_one_is_minus_mean_advantage():
 
 # ---------------------------------------------------------- logits paths ----
 # V = 8192: every thread's row chunks fit in registers (ragged across threads);
-# 134692: the part kept in LDS ends mid-way; 152004: a ragged remainder past
-# registers and LDS is read twice; 4099 and 1: scalar path.
+# 134692: the part kept in LDS ends mid-way; 152004: the LDS part ends just
+# before its capacity (rows up to 153600 stay on chip); 160004: a ragged
+# remainder past registers and LDS is read twice; 4099 and 1: scalar path.
 @pytest.mark.parametrize("V,n_prompts", [(8192, 16), (4099, 16), (1, 16), (134692, 2),
-                                         (152004, 2)])
+                                         (152004, 2), (160004, 2)])
 def test_logits_paths(V, n_prompts):
     cfg = synth.config(4, n_prompts=n_prompts, group=8, V=V)  # 8 seqs per prompt x 16 tokens
     b = synth.make_batch(cfg, "cpu", seed_key=(4, V))
