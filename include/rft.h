@@ -202,14 +202,20 @@ rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t 
  * give 0.  mode: RFT_ADV_GRPO (as rft_group_advantages: std + eps, the std
  * unbiased as there),
  * RFT_ADV_MEAN_CENTER, RFT_ADV_LEAVE_ONE_OUT (r_i - (sum_g - r_i) / (G - 1)).
- * Sums in fp64 in index order.  The work grows as n * n_groups (each group
- * scans the ids), meant for batches of up to about 1e5 rollouts.
+ * The rollouts are bucketed by group id (counts, a scan and a scatter in the
+ * workspace) and each group's members are sorted by index, so the work grows
+ * linearly with n (a group of more than 16384 rollouts scans the ids instead);
+ * the fp64 sums over a group's members run in a fixed order, so results are
+ * the same run to run.
  * rewards, adv [n] f32, group_id [n] int32; adv may not alias rewards.
- * Errors: RFT_E_NULL, RFT_E_SHAPE (n < 0, n_groups < 0 or > 2^31 - 1),
- * RFT_E_PARAM (mode unknown, eps < 0 or not finite). */
+ * ws: rft_group_advantages_ids_workspace_bytes(n, n_groups) bytes (about
+ * 4 n + 12 n_groups), 16-byte aligned; may be NULL when n == 0.
+ * Errors: RFT_E_NULL, RFT_E_SHAPE (n or n_groups < 0 or > 2^31 - 1),
+ * RFT_E_PARAM (mode unknown, eps < 0 or not finite), RFT_E_WORKSPACE. */
+size_t rft_group_advantages_ids_workspace_bytes(int64_t n, int64_t n_groups);
 rft_status rft_group_advantages_ids(const float* rewards, const int32_t* group_id, int64_t n,
                                     int64_t n_groups, int32_t mode, float eps, int32_t unbiased,
-                                    float* adv, void* stream);
+                                    float* adv, void* ws, size_t ws_bytes, void* stream);
 
 /* Per-token log-probability of the sampled id, entropy and log-sum-exp of the
  * policy head z_t = weight . hidden_t over the whole vocabulary (Sec. 3.1.1:

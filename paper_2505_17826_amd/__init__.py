@@ -79,8 +79,9 @@ _SIGS = {
                               ctypes.c_size_t]),
     "rft_group_advantages": (ctypes.c_int, [_p, _i64, ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
                                             _p, _p]),
+    "rft_group_advantages_ids_workspace_bytes": (ctypes.c_size_t, [_i64, _i64]),
     "rft_group_advantages_ids": (ctypes.c_int, [_p, _p, _i64, _i64, ctypes.c_int32, ctypes.c_float,
-                                                ctypes.c_int32, _p, _p]),
+                                                ctypes.c_int32, _p, _p, ctypes.c_size_t, _p]),
     "rft_token_logprobs": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _p, ctypes.c_int, _i64,
                                           _i64, _p, _p, _p, _p, ctypes.c_size_t, _p]),
     "rft_token_logprobs_from_logits": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _i64, _p,
@@ -236,11 +237,13 @@ def rft_group_advantages(rewards, group_size, eps=1e-6, out=None, stream=None, u
 
 
 def rft_group_advantages_ids(rewards, group_id, n_groups, mode=RFT_ADV_GRPO, eps=1e-6, out=None,
-                             stream=None, unbiased=True):
+                             stream=None, unbiased=True, ws=None):
     _need_gpu(rewards, group_id)
     out = torch.empty_like(rewards) if out is None else out
+    need = int(lib().rft_group_advantages_ids_workspace_bytes(rewards.numel(), n_groups))
+    ws, nb = _workspace(need, rewards.device, ws)
     _check(lib().rft_group_advantages_ids(_ptr(rewards), _ptr(group_id), rewards.numel(), n_groups,
-                                          mode, eps, 1 if unbiased else 0, _ptr(out),
+                                          mode, eps, 1 if unbiased else 0, _ptr(out), _ptr(ws), nb,
                                           _stream(stream)))
     return out
 

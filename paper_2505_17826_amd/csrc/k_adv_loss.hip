@@ -47,10 +47,21 @@ hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, 
 }
 
 // ------------------------------------------- advantages over group ids ----
-// Explicit, variable-size groups: one workgroup per group id scans the ids
-// (members in index order, fp64 sums reduced in a fixed order) and writes the
-// advantages of its members; rollouts whose id is outside [0, n_groups) get 0
-// from k_adv_left_out.  Modes as rft_adv_mode.
+// Explicit, variable-size groups (modes as rft_adv_mode), in work linear in
+// the number of rollouts:
+//   k_adv_count    count each group's rollouts (integer atomics: exact), and
+//                  give 0 to rollouts whose id is outside [0, n_groups);
+//   k_adv_scan_*   exclusive scan of the counts: group g's members go to
+//                  mem[off[g] .. off[g + 1]);
+//   k_adv_scatter  place each rollout index in its group's range (the order
+//                  inside a range depends on the atomics);
+//   k_adv_member_groups  one workgroup per group: sort the member indices
+//                  (bitonic, in LDS), so the members are in index order
+//                  whatever the scatter did, then fp64 sums over them in a
+//                  fixed order and the advantages.  A group with more members
+//                  than the LDS sort holds scans every id instead (members
+//                  in index order as well), which only such large groups pay.
+// Results are deterministic run to run.
 template <typename Tv>
 __device__ Tv block_sum256(Tv v, Tv* sh) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -62,75 +73,255 @@ __device__ Tv block_sum256(Tv v, Tv* sh) {
   return sh[0] + sh[1] + sh[2] + sh[3];
 }
 
-__global__ void __launch_bounds__(256) k_adv_left_out(const int32_t* __restrict__ gid, int64_t n,
-                                                      int64_t n_groups, float* __restrict__ adv) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n && (gid[i] < 0 || (int64_t)gid[i] >= n_groups)) adv[i] = 0.f;
+__device__ float block_min256(float v, float* sh) {
+  v = wave_min_f(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return fminf(fminf(sh[0], sh[1]), fminf(sh[2], sh[3]));
 }
 
-__global__ void __launch_bounds__(256) k_adv_groups(const float* __restrict__ r,
-                                                    const int32_t* __restrict__ gid, int64_t n,
-                                                    int mode, float eps, int unbiased,
-                                                    float* __restrict__ adv) {
-  __shared__ double shd[4];
+__device__ float block_max256(float v, float* sh) {
+  v = wave_max_f(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(sh[0], sh[1]), fmaxf(sh[2], sh[3]));
+}
+
+constexpr int kAdvScanBlock = 1024;  // counts per block of the scan (4 per thread)
+constexpr int kAdvSortSmall = 256;   // members the small-group kernel sorts (1 KiB of LDS)
+constexpr int kAdvSortCap = 16384;   // members the large-group kernel sorts (64 KiB)
+
+__global__ void __launch_bounds__(256) k_adv_zero2(int32_t* __restrict__ a, int32_t* __restrict__ b,
+                                                   int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) {
+    a[i] = 0;
+    b[i] = 0;
+  }
+}
+
+__global__ void __launch_bounds__(256) k_adv_count(const int32_t* __restrict__ gid, int64_t n,
+                                                   int64_t n_groups, int32_t* __restrict__ cnt,
+                                                   float* __restrict__ adv) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const int g = gid[i];
+  if (g < 0 || (int64_t)g >= n_groups) adv[i] = 0.f;
+  else atomicAdd(cnt + g, 1);
+}
+
+// Per block of kAdvScanBlock counts: the block's total.
+__global__ void __launch_bounds__(256) k_adv_scan_totals(const int32_t* __restrict__ cnt,
+                                                         int64_t ng, int32_t* __restrict__ tot) {
   __shared__ int shi[4];
+  const int64_t b0 = (int64_t)blockIdx.x * kAdvScanBlock;
+  int v = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int64_t g = b0 + threadIdx.x * 4 + k;
+    v += g < ng ? cnt[g] : 0;
+  }
+  v = block_sum256(v, shi);
+  if (threadIdx.x == 0) tot[blockIdx.x] = v;
+}
+
+// Exclusive scan of one int per thread over the 256 threads of a block.
+__device__ int block_excl_scan256(int v, int* sh) {
+  sh[threadIdx.x] = v;
+  __syncthreads();
+  for (int o = 1; o < 256; o <<= 1) {
+    const int add = threadIdx.x >= (unsigned)o ? sh[threadIdx.x - o] : 0;
+    __syncthreads();
+    sh[threadIdx.x] += add;
+    __syncthreads();
+  }
+  const int incl = sh[threadIdx.x];
+  __syncthreads();
+  return incl - v;
+}
+
+// One block: exclusive scan of the block totals, in place.
+__global__ void __launch_bounds__(256) k_adv_scan_top(int32_t* __restrict__ tot, int64_t nb) {
+  __shared__ int sh[256];
+  int carry = 0;
+  for (int64_t b0 = 0; b0 < nb; b0 += 256) {
+    const int64_t b = b0 + threadIdx.x;
+    const int v = b < nb ? tot[b] : 0;
+    const int ex = block_excl_scan256(v, sh);
+    if (b < nb) tot[b] = carry + ex;
+    // the block's total: the last thread's exclusive value plus its own
+    if (threadIdx.x == 255) sh[0] = ex + v;
+    __syncthreads();
+    carry += sh[0];
+    __syncthreads();
+  }
+}
+
+// off[g] = exclusive prefix of the counts; off[ng] = the total.
+__global__ void __launch_bounds__(256) k_adv_scan_apply(const int32_t* __restrict__ cnt,
+                                                        int64_t ng, const int32_t* __restrict__ tot,
+                                                        int32_t* __restrict__ off) {
+  __shared__ int sh[256];
+  const int64_t b0 = (int64_t)blockIdx.x * kAdvScanBlock;
+  int c[4], v = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int64_t g = b0 + threadIdx.x * 4 + k;
+    c[k] = g < ng ? cnt[g] : 0;
+    v += c[k];
+  }
+  int run = tot[blockIdx.x] + block_excl_scan256(v, sh);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int64_t g = b0 + threadIdx.x * 4 + k;
+    if (g < ng) off[g] = run;
+    run += c[k];
+    if (g == ng - 1) off[ng] = run;
+  }
+}
+
+__global__ void __launch_bounds__(256) k_adv_scatter(const int32_t* __restrict__ gid, int64_t n,
+                                                     int64_t n_groups,
+                                                     const int32_t* __restrict__ off,
+                                                     int32_t* __restrict__ cur,
+                                                     int32_t* __restrict__ mem) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const int g = gid[i];
+  if (g < 0 || (int64_t)g >= n_groups) return;
+  mem[off[g] + atomicAdd(cur + g, 1)] = (int32_t)i;
+}
+
+// Advantage of reward v in a group with sum s, mean mu, std sd and G members.
+__device__ __forceinline__ float adv_value(int mode, bool degenerate, double v, double s,
+                                           double mu, double sd, double G, float eps) {
+  if (degenerate) return 0.f;
+  double a;
+  if (mode == RFT_ADV_GRPO) a = (v - mu) / (sd + (double)eps);
+  else if (mode == RFT_ADV_MEAN_CENTER) a = v - mu;
+  else a = v - (s - v) / (G - 1.0);
+  return (float)a;
+}
+
+// Groups with LO < G <= CAP members sort them in LDS; with CAP = kAdvSortCap
+// the kernel also takes the groups beyond it (by scanning the ids).  Two
+// instantiations split the groups so that the many small ones run with little
+// LDS per workgroup.
+template <int LO, int CAP>
+__global__ void __launch_bounds__(256) k_adv_member_groups(
+    const float* __restrict__ r, const int32_t* __restrict__ gid, int64_t n,
+    const int32_t* __restrict__ off, const int32_t* __restrict__ mem, int mode, float eps,
+    int unbiased, float* __restrict__ adv) {
+  __shared__ int32_t key[CAP];
+  __shared__ double shd[4];
   __shared__ float shf[4];
   const int g = (int)blockIdx.x;
-  double s = 0.0;
-  int cnt = 0;
+  const int64_t a0 = off[g];
+  const int G = off[g + 1] - (int32_t)a0;
+  if (G <= LO || (CAP < kAdvSortCap && G > CAP)) return;
+  const int tid = threadIdx.x;
+  double s = 0.0, q = 0.0;
   float mn = INFINITY, mx = -INFINITY;
-  for (int64_t i = threadIdx.x; i < n; i += 256) {
-    if (gid[i] != g) continue;
-    const float v = r[i];
-    s += (double)v;
-    ++cnt;
-    mn = fminf(mn, v);
-    mx = fmaxf(mx, v);
+  if (G <= CAP) {
+    int P = 1;
+    while (P < G) P <<= 1;
+    for (int k = tid; k < P; k += 256) key[k] = k < G ? mem[a0 + k] : 0x7fffffff;
+    __syncthreads();
+    // bitonic sort of key[0, P) ascending
+    for (int size = 2; size <= P; size <<= 1) {
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        for (int k = tid; k < P / 2; k += 256) {
+          const int lo = 2 * k - (k & (stride - 1));
+          const int hi = lo + stride;
+          const bool up = (lo & size) == 0;
+          const int x = key[lo], y = key[hi];
+          if ((x > y) == up) {
+            key[lo] = y;
+            key[hi] = x;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    for (int k = tid; k < G; k += 256) {
+      const float v = r[key[k]];
+      s += (double)v;
+      mn = fminf(mn, v);
+      mx = fmaxf(mx, v);
+    }
+  } else {
+    for (int64_t i = tid; i < n; i += 256) {
+      if (gid[i] != g) continue;
+      const float v = r[i];
+      s += (double)v;
+      mn = fminf(mn, v);
+      mx = fmaxf(mx, v);
+    }
   }
   s = block_sum256(s, shd);
-  cnt = block_sum256(cnt, shi);
-  mn = wave_min_f(mn);
-  mx = wave_max_f(mx);
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) shf[threadIdx.x >> 6] = mn;
-  __syncthreads();
-  mn = fminf(fminf(shf[0], shf[1]), fminf(shf[2], shf[3]));
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) shf[threadIdx.x >> 6] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(shf[0], shf[1]), fmaxf(shf[2], shf[3]));
-  const double G = (double)cnt, mu = cnt > 0 ? s / G : 0.0;
+  mn = block_min256(mn, shf);
+  mx = block_max256(mx, shf);
+  const double Gd = (double)G, mu = s / Gd;
+  const bool degenerate = G < 2 || (mode == RFT_ADV_GRPO && mn == mx);
   double sd = 0.0;
-  if (mode == RFT_ADV_GRPO) {
-    double q = 0.0;
-    for (int64_t i = threadIdx.x; i < n; i += 256) {
-      if (gid[i] != g) continue;
-      const double dv = (double)r[i] - mu;
-      q += dv * dv;
+  if (mode == RFT_ADV_GRPO && !degenerate) {
+    if (G <= CAP) {
+      for (int k = tid; k < G; k += 256) {
+        const double dv = (double)r[key[k]] - mu;
+        q += dv * dv;
+      }
+    } else {
+      for (int64_t i = tid; i < n; i += 256) {
+        if (gid[i] != g) continue;
+        const double dv = (double)r[i] - mu;
+        q += dv * dv;
+      }
     }
     q = block_sum256(q, shd);
-    sd = cnt > 1 ? sqrt(q / (unbiased ? G - 1.0 : G)) : 0.0;
+    sd = sqrt(q / (unbiased ? Gd - 1.0 : Gd));
   }
-  const bool degenerate = cnt < 2 || (mode == RFT_ADV_GRPO && mn == mx);
-  for (int64_t i = threadIdx.x; i < n; i += 256) {
-    if (gid[i] != g) continue;
-    const double v = (double)r[i];
-    double a = 0.0;
-    if (!degenerate) {
-      if (mode == RFT_ADV_GRPO) a = (v - mu) / (sd + (double)eps);
-      else if (mode == RFT_ADV_MEAN_CENTER) a = v - mu;
-      else a = v - (s - v) / (G - 1.0);
+  if (G <= CAP) {
+    for (int k = tid; k < G; k += 256) {
+      const int i = key[k];
+      adv[i] = adv_value(mode, degenerate, (double)r[i], s, mu, sd, Gd, eps);
     }
-    adv[i] = (float)a;
+  } else {
+    for (int64_t i = tid; i < n; i += 256)
+      if (gid[i] == g) adv[i] = adv_value(mode, degenerate, (double)r[i], s, mu, sd, Gd, eps);
   }
+}
+
+AdvIdsWs carve_adv_ids(Carver& c, int64_t n, int64_t n_groups) {
+  AdvIdsWs w;
+  const int64_t ng = n_groups > 0 ? n_groups : 1;
+  w.cnt = c.take<int32_t>((size_t)ng);
+  w.cur = c.take<int32_t>((size_t)ng);
+  w.off = c.take<int32_t>((size_t)ng + 1);
+  w.tot = c.take<int32_t>((size_t)((ng + kAdvScanBlock - 1) / kAdvScanBlock));
+  w.mem = c.take<int32_t>((size_t)(n > 0 ? n : 1));
+  return w;
 }
 
 hipError_t launch_group_adv_ids(const float* r, const int32_t* gid, int64_t n, int64_t n_groups,
-                                int mode, float eps, int unbiased, float* adv, hipStream_t s) {
+                                int mode, float eps, int unbiased, float* adv, const AdvIdsWs& w,
+                                hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  k_adv_left_out<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(gid, n, n_groups, adv);
+  const unsigned nbn = (unsigned)((n + 255) / 256);
   if (n_groups > 0)
-    k_adv_groups<<<(unsigned)n_groups, 256, 0, s>>>(r, gid, n, mode, eps, unbiased, adv);
+    k_adv_zero2<<<(unsigned)((n_groups + 255) / 256), 256, 0, s>>>(w.cnt, w.cur, n_groups);
+  k_adv_count<<<nbn, 256, 0, s>>>(gid, n, n_groups, w.cnt, adv);
+  if (n_groups == 0) return hipGetLastError();
+  const int64_t nbs = (n_groups + kAdvScanBlock - 1) / kAdvScanBlock;
+  k_adv_scan_totals<<<(unsigned)nbs, 256, 0, s>>>(w.cnt, n_groups, w.tot);
+  k_adv_scan_top<<<1, 256, 0, s>>>(w.tot, nbs);
+  k_adv_scan_apply<<<(unsigned)nbs, 256, 0, s>>>(w.cnt, n_groups, w.tot, w.off);
+  k_adv_scatter<<<nbn, 256, 0, s>>>(gid, n, n_groups, w.off, w.cur, w.mem);
+  k_adv_member_groups<0, kAdvSortSmall><<<(unsigned)n_groups, 256, 0, s>>>(
+      r, gid, n, w.off, w.mem, mode, eps, unbiased, adv);
+  k_adv_member_groups<kAdvSortSmall, kAdvSortCap><<<(unsigned)n_groups, 256, 0, s>>>(
+      r, gid, n, w.off, w.mem, mode, eps, unbiased, adv);
   return hipGetLastError();
 }
 

@@ -465,11 +465,21 @@ rft_status rft_group_advantages(const float* rewards, int64_t n_groups, int32_t 
   return RFT_OK;
 }
 
+size_t rft_group_advantages_ids_workspace_bytes(int64_t n, int64_t n_groups) {
+  if (n < 0 || n_groups < 0 || n > (int64_t)std::numeric_limits<int32_t>::max() ||
+      n_groups > (int64_t)std::numeric_limits<int32_t>::max())
+    return 0;
+  Carver c(nullptr);
+  carve_adv_ids(c, n, n_groups);
+  return c.bytes();
+}
+
 rft_status rft_group_advantages_ids(const float* rewards, const int32_t* group_id, int64_t n,
                                     int64_t n_groups, int32_t mode, float eps, int32_t unbiased,
-                                    float* adv, void* stream) {
+                                    float* adv, void* ws, size_t ws_bytes, void* stream) {
   const char* fn = "rft_group_advantages_ids";
-  if (n < 0 || n_groups < 0 || n_groups > (int64_t)std::numeric_limits<int32_t>::max())
+  if (n < 0 || n_groups < 0 || n > (int64_t)std::numeric_limits<int32_t>::max() ||
+      n_groups > (int64_t)std::numeric_limits<int32_t>::max())
     return fail(RFT_E_SHAPE, "%s: n=%lld n_groups=%lld", fn, (long long)n, (long long)n_groups);
   if (n > 0 && (!rewards || !group_id || !adv))
     return fail(RFT_E_NULL, "%s: rewards / group_id / adv is NULL", fn);
@@ -477,7 +487,13 @@ rft_status rft_group_advantages_ids(const float* rewards, const int32_t* group_i
     return fail(RFT_E_PARAM, "%s: mode=%d unknown", fn, mode);
   if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(RFT_E_PARAM, "%s: eps=%g", fn, (double)eps);
   if (n > 0 && rewards == adv) return fail(RFT_E_PARAM, "%s: adv may not alias rewards", fn);
-  RFT_HIP(launch_group_adv_ids(rewards, group_id, n, n_groups, mode, eps, unbiased ? 1 : 0, adv,
+  if (n == 0) return RFT_OK;
+  rft_status st;
+  if ((st = check_ws(fn, ws, ws_bytes, rft_group_advantages_ids_workspace_bytes(n, n_groups))))
+    return st;
+  Carver c(ws);
+  const AdvIdsWs w = carve_adv_ids(c, n, n_groups);
+  RFT_HIP(launch_group_adv_ids(rewards, group_id, n, n_groups, mode, eps, unbiased ? 1 : 0, adv, w,
                                (hipStream_t)stream),
           fn);
   return RFT_OK;

@@ -266,8 +266,16 @@ hipError_t launch_dpo(const rft_tokens& tok, const TokMeta& m, int64_t V, const 
 // ------------------------------------------------------------ launchers --
 hipError_t launch_group_adv(const float* r, int64_t n_groups, int G, float eps, int unbiased,
                             float* adv, hipStream_t s);
+struct AdvIdsWs {
+  int32_t *cnt, *cur;  // [n_groups] members per group, scatter cursors
+  int32_t* off;        // [n_groups + 1] start of each group's members in mem
+  int32_t* tot;        // [ceil(n_groups / 1024)] block totals of the scan
+  int32_t* mem;        // [n] rollout indices grouped by group id
+};
+AdvIdsWs carve_adv_ids(Carver& c, int64_t n, int64_t n_groups);
 hipError_t launch_group_adv_ids(const float* r, const int32_t* gid, int64_t n, int64_t n_groups,
-                                int mode, float eps, int unbiased, float* adv, hipStream_t s);
+                                int mode, float eps, int unbiased, float* adv, const AdvIdsWs& w,
+                                hipStream_t s);
 hipError_t launch_loss_fwd(const rft_tokens& tok, const TokMeta& m, const float* logp,
                            const float* old, const float* ref, const float* adv, const float* ent,
                            const LossConst& c, float* grad, float* egrad, LossPartial* parts,

@@ -98,6 +98,7 @@ def test_argument_validation_returns_codes():
     L = R.lib()
     s = None
     fake = ctypes.c_void_p(0x1000)
+    fake2 = ctypes.c_void_p(0x2000)
     # advantages
     assert L.rft_group_advantages(fake, -1, 8, 1e-6, 1, fake, s) == R.RFT_E_SHAPE
     assert L.rft_group_advantages(fake, 4, 0, 1e-6, 1, fake, s) == R.RFT_E_SHAPE
@@ -169,14 +170,22 @@ def test_argument_validation_returns_codes():
                                ctypes.byref(P(entropy_coef=0.01)), fake, None, fake, fake, fake,
                                fake, 0, fake, fake, 1 << 30, s) == R.RFT_E_NULL
     # advantages over group ids
-    for args, code in [((fake, fake, -1, 4, 0, 1e-6, 1, fake), R.RFT_E_SHAPE),
-                       ((fake, fake, 8, -1, 0, 1e-6, 1, fake), R.RFT_E_SHAPE),
-                       ((fake, fake, 8, 1 << 31, 0, 1e-6, 1, fake), R.RFT_E_SHAPE),
-                       ((fake, None, 8, 4, 0, 1e-6, 1, fake), R.RFT_E_NULL),
-                       ((fake, fake, 8, 4, 3, 1e-6, 1, fake), R.RFT_E_PARAM),
-                       ((fake, fake, 8, 4, 0, -1.0, 1, fake), R.RFT_E_PARAM),
-                       ((fake, fake, 8, 4, 0, 1e-6, 1, fake), R.RFT_E_PARAM)]:  # adv aliases rewards
+    big = 1 << 30
+    for args, code in [((fake, fake, -1, 4, 0, 1e-6, 1, fake2, fake, big), R.RFT_E_SHAPE),
+                       ((fake, fake, 8, -1, 0, 1e-6, 1, fake2, fake, big), R.RFT_E_SHAPE),
+                       ((fake, fake, 8, 1 << 31, 0, 1e-6, 1, fake2, fake, big), R.RFT_E_SHAPE),
+                       ((fake, None, 8, 4, 0, 1e-6, 1, fake2, fake, big), R.RFT_E_NULL),
+                       ((fake, fake, 8, 4, 3, 1e-6, 1, fake2, fake, big), R.RFT_E_PARAM),
+                       ((fake, fake, 8, 4, 0, -1.0, 1, fake2, fake, big), R.RFT_E_PARAM),
+                       ((fake, fake, 8, 4, 0, 1e-6, 1, fake, fake, big), R.RFT_E_PARAM),  # aliasing
+                       ((fake, fake, 8, 4, 0, 1e-6, 1, fake2, None, big), R.RFT_E_WORKSPACE),
+                       ((fake, fake, 8, 4, 0, 1e-6, 1, fake2, fake, 16), R.RFT_E_WORKSPACE)]:
         assert L.rft_group_advantages_ids(*args, s) == code, args
+    # workspace of the advantages over group ids: counts, cursors, offsets and
+    # the members (about 4 n + 12 n_groups bytes), 0 for invalid sizes
+    w = L.rft_group_advantages_ids_workspace_bytes
+    assert w(1000, 10) >= 4 * 1000 + 12 * 10 and w(1000, 10) < 4 * 1000 + 12 * 10 + 2048
+    assert w(10 ** 6, 125000) < w(2 * 10 ** 6, 125000) and w(-1, 4) == 0 and w(8, -1) == 0
     # SFT / DPO parameters and layout
     assert L.rft_sft_loss_fwd(ctypes.byref(tk), 100, fake, 7, 0.0, fake, fake, fake, 1 << 30,
                               s) == R.RFT_E_PARAM
