@@ -61,18 +61,20 @@ __global__ void __launch_bounds__(256) k_step_rows(
   }
 }
 
-// One 512-thread workgroup per 256 x 256 tile of the chunk.  Thread tid owns
-// the 8 x 8 blocks (row block rb, column block cb) with cb = tid % 32 and
-// rb = tid / 32 and tid / 32 + 16: it reads eight 16-byte row pieces (a wave
-// reads two 512-byte rows per instruction) and writes dZ back in place.  The
-// transposed copy is staged in LDS (column c of the tile as a 512-byte row,
+// One 512-thread workgroup per 128 x 256 tile of the chunk (64 KiB of LDS, so
+// two workgroups share a CU and one's loads overlap the other's stores).
+// Thread tid owns the 8 x 8 block (row block rb = tid / 32, column block
+// cb = tid % 32): it issues its eight 16-byte row pieces at once (a wave reads
+// two 512-byte rows per instruction) and writes dZ back in place.  The
+// transposed copy is staged in LDS (column c of the tile as a 256-byte row,
 // its 16-byte chunk j at chunk j ^ ((c >> 3) & 15): the 32 lanes writing one
 // column position of 32 blocks hit 16 distinct bank groups) and leaves as
-// 16-byte stores, a wave writing two 512-byte rows of dZ^T per instruction.
+// 16-byte stores, a wave writing four 256-byte rows of dZ^T per instruction.
 // Rows of the last tile past the count are written as 0 in both layouts (the
 // dW GEMM reads K up to the next multiple of 64).  Tiles wholly past the
 // chunk's count are skipped (the backward GEMMs read rows only up to the count).
 constexpr int kDzT = 512;
+constexpr int kDzRows = 128;  // rows per tile
 
 __device__ __forceinline__ uint32_t bf16_bits(float f) { return (uint32_t)f32_to_bf16(f); }
 
@@ -82,17 +84,23 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
     const int32_t* __restrict__ meta, int64_t c0, const float* __restrict__ pm,
     const float* __restrict__ lse, const float* __restrict__ grad, const float* __restrict__ ce,
     const float* __restrict__ cmu, int ntc, uint16_t* __restrict__ dzt, int64_t ldt) {
-  __shared__ float rL[256], rC[256], rM[256], rE[256], rD[256];
-  __shared__ int rY[256];
-  __shared__ __attribute__((aligned(16))) uint16_t stT[256 * 256];  // [tile column][tile row]
+  __shared__ float rL[kDzRows], rC[kDzRows], rM[kDzRows], rE[kDzRows], rD[kDzRows];
+  __shared__ int rY[kDzRows];
+  __shared__ __attribute__((aligned(16))) uint16_t stT[256 * kDzRows];  // [tile column][tile row]
   const int tid = threadIdx.x;
   const int nt = (int)(blockIdx.x % ntc), mt = (int)(blockIdx.x / ntc);
   int64_t count = (int64_t)meta[0] - c0;
   count = count < 0 ? 0 : (count > Tc ? Tc : count);
-  const int64_t r0 = (int64_t)mt * 256;
+  const int64_t r0 = (int64_t)mt * kDzRows;
   if (r0 >= count) return;
   const int64_t n0 = (int64_t)nt * 256;
-  if (tid < 256) {
+  const int cb = tid & 31, rb = tid >> 5;
+  uint16_t* src = yz + (r0 + rb * 8) * Vpad + n0 + cb * 8;
+  // this thread's eight row pieces, all in flight before the row parameters
+  uint4 in[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) in[r] = *(const uint4*)(src + r * Vpad);
+  if (tid < kDzRows) {
     const int64_t r = r0 + tid;
     float L_ = 0.f, C_ = 0.f, M_ = 0.f, E_ = 0.f, D_ = 0.f;
     int Y_ = -1;
@@ -115,57 +123,48 @@ __global__ void __launch_bounds__(kDzT) k_dz_from_y(
     rY[tid] = Y_;
   }
   __syncthreads();
-  const int cb = tid & 31;
+  uint32_t tcol[8][4];  // column q of the block: its 8 rows as bf16 pairs
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int rb = (tid >> 5) + 16 * h;
-    uint16_t* src = yz + (r0 + rb * 8) * Vpad + n0 + cb * 8;
-    uint4 in[8];
-    uint32_t tcol[8][4];  // column q of the block: its 8 rows as bf16 pairs
+  for (int r = 0; r < 8; ++r) {
+    const int rl = rb * 8 + r;
+    const float Lk = rL[rl], Ck = rC[rl], Mk = rM[rl], Ek = rE[rl], Dk = rD[rl];
+    const int Yk = rY[rl];
+    const bool rv = r0 + rl < count;
+    const uint32_t w[4] = {in[r].x, in[r].y, in[r].z, in[r].w};
+    uint32_t o[4];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) in[r] = *(const uint4*)(src + r * Vpad);
+    for (int q2 = 0; q2 < 4; ++q2) {
+      uint32_t pair = 0;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int rl = rb * 8 + r;
-      const float Lk = rL[rl], Ck = rC[rl], Mk = rM[rl], Ek = rE[rl], Dk = rD[rl];
-      const int Yk = rY[rl];
-      const bool rv = r0 + rl < count;
-      const uint32_t w[4] = {in[r].x, in[r].y, in[r].z, in[r].w};
-      uint32_t o[4];
-#pragma unroll
-      for (int q2 = 0; q2 < 4; ++q2) {
-        uint32_t pair = 0;
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int q = 2 * q2 + hh;
-          const int64_t col = n0 + cb * 8 + q;
-          const uint16_t hb = (uint16_t)(w[q2] >> (hh * 16));
-          const float yv = (float)__builtin_bit_cast(_Float16, hb);
-          const float p = exp2f(fmaf(yv, kLog2e, Mk - Lk));
-          float d = dlogit(Ck, Ek, -Dk, p, yv, col == (int64_t)Yk);
-          d = (rv && col < V) ? d : 0.f;
-          const uint32_t b = bf16_bits(d);
-          pair |= b << (hh * 16);
-          if (r & 1) tcol[q][r >> 1] |= b << 16;
-          else tcol[q][r >> 1] = b;
-        }
-        o[q2] = pair;
+      for (int hh = 0; hh < 2; ++hh) {
+        const int q = 2 * q2 + hh;
+        const int64_t col = n0 + cb * 8 + q;
+        const uint16_t hb = (uint16_t)(w[q2] >> (hh * 16));
+        const float yv = (float)__builtin_bit_cast(_Float16, hb);
+        const float p = exp2f(fmaf(yv, kLog2e, Mk - Lk));
+        float d = dlogit(Ck, Ek, -Dk, p, yv, col == (int64_t)Yk);
+        d = (rv && col < V) ? d : 0.f;
+        const uint32_t b = bf16_bits(d);
+        pair |= b << (hh * 16);
+        if (r & 1) tcol[q][r >> 1] |= b << 16;
+        else tcol[q][r >> 1] = b;
       }
-      *(uint4*)(src + r * Vpad) = make_uint4(o[0], o[1], o[2], o[3]);
+      o[q2] = pair;
     }
+    *(uint4*)(src + r * Vpad) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int c = cb * 8 + q;
-      *(uint4*)(stT + c * 256 + ((rb ^ (cb & 15)) << 3)) =
-          make_uint4(tcol[q][0], tcol[q][1], tcol[q][2], tcol[q][3]);
-    }
+  for (int q = 0; q < 8; ++q) {
+    const int c = cb * 8 + q;
+    *(uint4*)(stT + c * kDzRows + ((rb ^ (cb & 15)) << 3)) =
+        make_uint4(tcol[q][0], tcol[q][1], tcol[q][2], tcol[q][3]);
   }
   __syncthreads();
-  // dZ^T rows n0 .. n0 + 255, columns r0 .. r0 + 255
-#pragma unroll 4
-  for (int it = 0; it < 16; ++it) {
-    const int i = it * kDzT + tid, c = i >> 5, j = i & 31;
-    const uint4 v = *(const uint4*)(stT + c * 256 + ((j ^ ((c >> 3) & 15)) << 3));
+  // dZ^T rows n0 .. n0 + 255, columns r0 .. r0 + 127: 16 chunks per row
+#pragma unroll
+  for (int it = 0; it < 8; ++it) {
+    const int i = it * kDzT + tid, c = i >> 4, j = i & 15;
+    const uint4 v = *(const uint4*)(stT + c * kDzRows + ((j ^ ((c >> 3) & 15)) << 3));
     *(uint4*)(dzt + (n0 + c) * ldt + r0 + j * 8) = v;
   }
 }
@@ -211,7 +210,7 @@ hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
                             const float* ce, const float* cmu, uint16_t* dzt, int64_t ldt,
                             hipStream_t s) {
   const int ntc = (int)(Vpad / 256);
-  const int64_t nb = (Tc / 256) * ntc;
+  const int64_t nb = (Tc / kDzRows) * ntc;
   k_dz_from_y<<<(unsigned)nb, kDzT, 0, s>>>(yz, Vpad, Tc, V, rows, ids, meta, c0, pm, lse, grad,
                                             ce, cmu, ntc, dzt, ldt);
   return hipGetLastError();
