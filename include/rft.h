@@ -339,7 +339,7 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
  * rft_noalloc_scratch_bytes() bytes (16 MiB) per GPU, held until the process
  * ends; the call itself allocates and frees nothing.  Limit: the scratch the
  * layout needs must fit, which holds for T <= 131072 rows with n_seq <= T
- * (100 bytes per row plus 4 per rollout, rounded up); a larger layout returns
+ * (about 101 bytes per row plus 4 per rollout); a larger layout returns
  * RFT_E_WORKSPACE before anything is enqueued.  Every call on one GPU shares
  * that GPU's array: calls that overlap on one GPU (other streams, other host
  * threads) race and give wrong results, so serialise them.  The array keeps

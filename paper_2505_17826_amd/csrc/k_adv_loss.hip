@@ -429,6 +429,19 @@ hipError_t launch_loss_final(const LossPartial* parts, int nparts, const int32_t
   return hipGetLastError();
 }
 
+__global__ void __launch_bounds__(256) k_loss_reduce256(const LossPartial* __restrict__ parts,
+                                                        int64_t n, LossPartial* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  LossPartial p = i < n ? parts[i] : RFT_ZERO_PARTIAL;
+  block_reduce_partial(p, out + blockIdx.x);
+}
+
+hipError_t launch_loss_reduce256(const LossPartial* parts, int64_t n, LossPartial* out,
+                                 hipStream_t s) {
+  if (n > 0) k_loss_reduce256<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(parts, n, out);
+  return hipGetLastError();
+}
+
 // SFT loss of the train-only mode: sum_t w_t (-logp_t) over the valid rows
 // whose id is in range, w_t the aggregation weight; grad = -w_t.
 __global__ void __launch_bounds__(256) k_sft_fwd(

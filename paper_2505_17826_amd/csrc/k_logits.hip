@@ -462,8 +462,8 @@ constexpr size_t kFusedReserve = 96 * 1024;  // bytes of LDS reserved per workgr
 hipError_t launch_logits_fused(const float* logits, const rft_tokens& tok, const TokMeta& m,
                                int64_t V, const float* old, const float* ref, const float* adv,
                                const LossConst& c, float* logp, float* ent, float* lse,
-                               float* grad, float* dl, LossPartial* parts, rft_ppo_stats* st,
-                               hipStream_t s) {
+                               float* grad, float* dl, LossPartial* parts, LossPartial* parts2,
+                               rft_ppo_stats* st, hipStream_t s) {
   if (tok.T > 0) {
     // buffer descriptors span one row: 32-bit byte offsets
     if (vec_ok(logits, V) && vec_ok(dl, V) && V <= ((int64_t)1 << 28)) {
@@ -492,7 +492,10 @@ hipError_t launch_logits_fused(const float* logits, const rft_tokens& tok, const
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_loss_final(parts, (int)tok.T, m.meta, st, s);
+  // one partial per row: first reduced per 256-row block (fixed order), so
+  // that the final single-workgroup sum reads T / 256 partials
+  if ((e = launch_loss_reduce256(parts, tok.T, parts2, s)) != hipSuccess) return e;
+  return launch_loss_final(parts2, (int)((tok.T + 255) / 256), m.meta, st, s);
 }
 
 }  // namespace rft

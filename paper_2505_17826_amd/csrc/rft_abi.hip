@@ -157,6 +157,7 @@ FwdWs carve_fwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dty
 struct LossWs {
   TokMeta m;
   LossPartial* parts;
+  LossPartial* parts2;  // per_row: the partials of 256-row blocks (nullptr otherwise)
   size_t bytes;
 };
 LossWs carve_loss(void* base, const rft_tokens& tok, bool per_row) {
@@ -165,6 +166,8 @@ LossWs carve_loss(void* base, const rft_tokens& tok, bool per_row) {
   w.m = carve_tokmeta(c, tok.T, tok.n_seq);
   int64_t np = per_row ? tok.T : (tok.T + 255) / 256;
   w.parts = c.take<LossPartial>(np > 0 ? np : 1);
+  w.parts2 = per_row ? c.take<LossPartial>((size_t)((np + 255) / 256 > 0 ? (np + 255) / 256 : 1))
+                     : nullptr;
   w.bytes = c.bytes();
   return w;
 }
@@ -686,7 +689,7 @@ rft_status rft_ppo_clip_fused_logits(const rft_tokens* tok, const float* logits,
   LossConst c = loss_const(params, V, *tok);
   RFT_HIP(launch_logits_fused(logits, *tok, w.m, V, old_logp,
                               ref_logp, adv, c, logp, entropy,
-                              lse, grad_logp, d_logits, w.parts, stats, s),
+                              lse, grad_logp, d_logits, w.parts, w.parts2, stats, s),
           fn);
   return RFT_OK;
 }

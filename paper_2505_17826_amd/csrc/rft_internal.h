@@ -251,6 +251,9 @@ __device__ __forceinline__ float dlogit(float c, float e, float mu, float p, flo
 
 hipError_t launch_loss_final(const LossPartial* parts, int nparts, const int32_t* meta,
                              rft_ppo_stats* stats, hipStream_t s, int sft_only = 0);
+// out[b] = the fixed-order sum of parts[256 b .. 256 b + 255] (n parts)
+hipError_t launch_loss_reduce256(const LossPartial* parts, int64_t n, LossPartial* out,
+                                 hipStream_t s);
 hipError_t launch_sft_fwd(const rft_tokens& tok, const TokMeta& m, int64_t V, const float* logp,
                           int agg, double denom, float* grad, LossPartial* parts,
                           rft_ppo_stats* st, hipStream_t s);
@@ -338,8 +341,8 @@ hipError_t launch_logits_bwd(const float* logits, const rft_tokens& tok, int64_t
 hipError_t launch_logits_fused(const float* logits, const rft_tokens& tok, const TokMeta& m,
                                int64_t V, const float* old, const float* ref, const float* adv,
                                const LossConst& c, float* logp, float* ent, float* lse,
-                               float* grad, float* dl, LossPartial* parts, rft_ppo_stats* st,
-                               hipStream_t s);
+                               float* grad, float* dl, LossPartial* parts, LossPartial* parts2,
+                               rft_ppo_stats* st, hipStream_t s);
 
 constexpr int kMfmaTileN = 256;  // vocabulary columns per forward tile (bf16 path)
 constexpr int kSimtTileN = 64;   // (fp32 path)
