@@ -13,6 +13,14 @@
 // The number of rows can come from a device counter, so the host never waits
 // for the count of valid tokens.
 //
+// Operand layouts: row-major with leading dimension ld, or tile-blocked (the
+// layout the fused step keeps its backward operands in): 256-row panels, each
+// 256 x Kp (Kp = ld, a multiple of 64) stored as Kp / 64 consecutive blocks of
+// 256 rows x 64 values, row-major inside a block (blk_index in rft_internal.h).
+// A k-step of a tile then reads one contiguous 32 KiB block per operand instead
+// of 256 pieces of 128 bytes a row pitch apart; with row pitches of hundreds of
+// KiB (dZ, W^T, dZ^T, Hc^T) the scattered pieces cost 10-15% of the GEMM.
+//
 // Epilogues:
 //   EPI_STATS  forward of the policy head: per row and 256-column vocabulary
 //              tile, online log-sum-exp partials (max, sum exp, sum exp*z) and
@@ -64,6 +72,7 @@ struct Args {
   int64_t ldb;
   int M, N, K;        // host values (M, K are caps when taken from the device counter)
   int NB;             // rows of B that exist (read only for n < NB; 0 = N)
+  int a_blk, b_blk;   // operand tile-blocked (ld = Kp; whole 256-row panels are read)
   const int32_t* cnt; // device counter: c = clamp(*cnt - cnt_off, 0, cnt_cap) (nullptr = none)
   int64_t cnt_off;
   int64_t cnt_cap;
@@ -79,7 +88,8 @@ struct Args {
   const float* ent;    //   and entropies, read only with egrad
   float* pm; float* ps; float* pu; int64_t ldp; float* zy;  // EPI_STATS: partials at p_off + m,
   int64_t p_off;                                            //   zy at rows_off + m
-  uint16_t* y; int64_t ldy;                                 // EPI_STATS_Y: fp16 z - tile max
+  uint16_t* y; int64_t ldy;                                 // EPI_STATS_Y: fp16 z - tile max,
+                                                            //   tile-blocked, Kp = ldy
   uint16_t* dz; int64_t ldz; int64_t Vvalid;                  // EPI_DZ
   uint16_t* dzt; int64_t ldzt;                                //   and dZ^T [Vpad, ldzt] (nullptr = none)
   float* C; int64_t ldc; int accumulate; int c_scatter;  // EPI_STORE
@@ -115,6 +125,7 @@ struct LoadGeom {
   uint32_t vA[2], vB[2];  // per-lane byte offsets for even / odd p (k0 = 0)
   int kc[2];              // logical chunk * 8 (first element) for even / odd p
   uint32_t sA, sB;        // bytes between instructions (8 rows)
+  uint32_t kA, kB;        // bytes per element of k0 (2 row-major, 512 blocked)
 };
 
 __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB,
@@ -123,14 +134,14 @@ __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_b
 #pragma unroll
   for (int p = 0; p < NI; ++p) {
     const int q = p & 1;
-    const uint32_t va = k0 + lg.kc[q] < K ? lg.vA[q] + (uint32_t)k0 * 2u : 0x80000000u;
+    const uint32_t va = k0 + lg.kc[q] < K ? lg.vA[q] + (uint32_t)k0 * lg.kA : 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_ptr)(dst + p * 1024), 16,
                                              va + (uint32_t)p * lg.sA, 0, 0, 0);
   }
 #pragma unroll
   for (int p = 0; p < NI; ++p) {
     const int q = p & 1;
-    const uint32_t vb = k0 + lg.kc[q] < K ? lg.vB[q] + (uint32_t)k0 * 2u : 0x80000000u;
+    const uint32_t vb = k0 + lg.kc[q] < K ? lg.vB[q] + (uint32_t)k0 * lg.kB : 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES + p * 1024), 16,
                                              vb + (uint32_t)p * lg.sB, 0, 0, 0);
   }
@@ -196,6 +207,19 @@ __device__ __forceinline__ void stage_copy_out(const char* st, uint16_t* dst, in
   }
 }
 
+// The same tile to the tile-blocked layout: the 256 x 256 tile is four
+// consecutive 256 x 64 blocks (dst = the first), 128 contiguous KiB.  Reads
+// are those of stage_copy_out (16 lanes take 256 contiguous bytes of one LDS
+// row); every 128-byte row piece of a block is written whole.
+__device__ __forceinline__ void stage_copy_out_blk(const char* st, uint16_t* dst, int tid) {
+#pragma unroll 4
+  for (int it = 0; it < 16; ++it) {
+    const int c = it * NT + tid, row = c >> 5, ch = c & 31;
+    const uint4 v = *(const uint4*)(st + row * STG_PITCH + ch * 16);
+    *(uint4*)(dst + (ch >> 3) * (BM * BK) + row * BK + (ch & 7) * 8) = v;
+  }
+}
+
 // Write four 16-bit values (rows r..r+3 of one column, packed in v) into the
 // row-major staging tile.
 __device__ __forceinline__ void stage_col4(char* q0, uint2 v) {
@@ -243,11 +267,13 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     for (int q = 0; q < 2; ++q) {
       const int ch = (lane & 7) ^ (lane >> 4) ^ (q * 4);
       lg.kc[q] = ch * 8;
-      lg.vA[q] = (uint32_t)(ld_row * g.lda * 2 + ch * 16);
-      lg.vB[q] = (uint32_t)(ld_row * g.ldb * 2 + ch * 16);
+      lg.vA[q] = (uint32_t)(ld_row * (g.a_blk ? 64 : g.lda) * 2 + ch * 16);
+      lg.vB[q] = (uint32_t)(ld_row * (g.b_blk ? 64 : g.ldb) * 2 + ch * 16);
     }
-    lg.sA = (uint32_t)(8 * g.lda * 2);
-    lg.sB = (uint32_t)(8 * g.ldb * 2);
+    lg.sA = (uint32_t)(8 * (g.a_blk ? 64 : g.lda) * 2);
+    lg.sB = (uint32_t)(8 * (g.b_blk ? 64 : g.ldb) * 2);
+    lg.kA = g.a_blk ? 512u : 2u;
+    lg.kB = g.b_blk ? 512u : 2u;
   }
   // MFMA tiles: v_mfma_f32_16x16x32_bf16, 4 x 8 tiles of 16 x 16 per wave
   // (measured 3-4% faster than 4 x 2 tiles of 32x32x16 on the same main loop,
@@ -266,8 +292,10 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
     const int m0 = mt * BM, n0 = nt * BN;
 
     // buffer descriptors over the tile's valid rows: everything else reads 0
-    const int rowsA = min(BM, M - m0);
-    const int rowsB = NB > n0 ? min(BN, NB - n0) : 0;
+    // (a blocked operand interleaves the rows of its panel, so the descriptor
+    // spans the whole panel and the panel's rows past the end hold zeros)
+    const int rowsA = g.a_blk ? BM : min(BM, M - m0);
+    const int rowsB = NB > n0 ? (g.b_blk ? BN : min(BN, NB - n0)) : 0;
     const int nb0 = rowsB > 0 ? n0 : 0;
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(g.A + (int64_t)m0 * g.lda, rowsA * g.lda * 2);
     const __amdgpu_buffer_rsrc_t rB = make_rsrc(g.B + (int64_t)nb0 * g.ldb, rowsB * g.ldb * 2);
@@ -430,7 +458,9 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
             stage_col4(lds + (wm * 64 + i * 16 + q4 * 4) * STG_PITCH + (wn * 128 + j * 16 + r16) * 2,
                        hv[i][j]);
         __syncthreads();
-        stage_copy_out(lds, g.y + (int64_t)m0 * g.ldy + n0, g.ldy, tid);
+        // y is tile-blocked (panel m0 of Kp = ldy columns; the tile's blocks
+        // start at column n0)
+        stage_copy_out_blk(lds, g.y + (int64_t)m0 * g.ldy + (int64_t)n0 * BM, tid);
       }
       if (full) {
 #pragma unroll
@@ -606,7 +636,8 @@ hipError_t mfma_fwd_stats(const uint16_t* Hc, int64_t d, const uint16_t* W, int6
 
 // Forward of one chunk of compacted rows [c0, c0 + Tc) for the fused step:
 // partials [ntiles][Tc] indexed by the chunk row, zy by the compacted row, and
-// y = z - (row maximum over the tile) in fp16 into y [Tc, ldy] (ldy = Vpad).
+// y = z - (row maximum over the tile) in fp16 into y, tile-blocked [Tc, Vpad]
+// (Tc a multiple of 256).
 hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V,
                             int64_t Vpad, const int32_t* rows, const int32_t* ids,
                             const int32_t* cnt, int64_t c0, int64_t Tc, float* pm, float* ps,
@@ -645,13 +676,17 @@ hipError_t mfma_dz(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V, 
 }
 
 // C[M, N] (+)= A[M, K] . B[N, K]^T with fp32 output; optional row scatter of C
-// through rows[rows_off + m]; M or K can come from the device counter.
+// through rows[rows_off + m]; M or K can come from the device counter.  A
+// blocked operand (a_blk / b_blk) has ld = Kp and whole 256-row panels whose
+// rows past M (N) and columns past K hold zeros.
 hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
                            int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
                            int64_t cnt_cap, int m_from_cnt, int k_from_cnt, float* C, int64_t ldc,
-                           const int32_t* rows, int64_t rows_off, int accumulate, hipStream_t s) {
+                           const int32_t* rows, int64_t rows_off, int accumulate, hipStream_t s,
+                           int a_blk, int b_blk) {
   mf::Args a = {};
   a.A = A; a.lda = lda; a.B = B; a.ldb = ldb;
+  a.a_blk = a_blk; a.b_blk = b_blk;
   a.M = (int)M; a.N = (int)N; a.K = (int)K;
   a.cnt = cnt; a.cnt_off = cnt_off; a.cnt_cap = cnt_cap; a.m_from_cnt = m_from_cnt;
   a.k_from_cnt = k_from_cnt;

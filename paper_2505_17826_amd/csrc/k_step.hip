@@ -6,13 +6,16 @@
 //                 and the on-policy / expert split of the MIX loss), and, with
 //                 an entropy bonus, its coefficient e_t and the softmax mean
 //                 mu_t = lse_t - H_t of the row;
-//   k_dz_from_y   dZ = c_t (onehot(y_t) - p) + e_t p (z - mu_t) from the fp16
-//                 y = z - (row maximum over the 256-column tile) that the
+//   k_dz_from_y_blk  dZ = c_t (onehot(y_t) - p) + e_t p (z - mu_t) from the
+//                 fp16 y = z - (row maximum over the 256-column tile) that the
 //                 forward GEMM stored, written in place as bf16 [Tc, Vpad]
 //                 (the dH GEMM's operand) and transposed, [Vpad, Tc] (the dW
-//                 GEMM's, K-contiguous);
-//   k_transpose_hc  the chunk's compacted hidden rows transposed, [d, Tc]
-//                 (the dW GEMM's other operand).
+//                 GEMM's, K-contiguous), both tile-blocked;
+//   k_transpose_blk  the chunk's compacted hidden rows transposed, [dpad, Tc],
+//                 and the weight transposed, [dpad, Vpad], tile-blocked (the
+//                 dW and dH GEMMs' other operands).
+// k_transpose_hc writes the row-major transposed hidden rows of the separate
+// backward (rft_ppo_clip_loss_bwd).
 // The arithmetic of k_step_rows is that of k_merge_rows and k_loss_fwd (same
 // merge order, same per-token formula), so the step and the separate calls
 // give the same log-probs and gradients bit for bit.
@@ -61,113 +64,7 @@ __global__ void __launch_bounds__(256) k_step_rows(
   }
 }
 
-// One 512-thread workgroup per 128 x 256 tile of the chunk (64 KiB of LDS, so
-// two workgroups share a CU and one's loads overlap the other's stores).
-// Thread tid owns the 8 x 8 block (row block rb = tid / 32, column block
-// cb = tid % 32): it issues its eight 16-byte row pieces at once (a wave reads
-// two 512-byte rows per instruction) and writes dZ back in place.  The
-// transposed copy is staged in LDS (column c of the tile as a 256-byte row,
-// its 16-byte chunk j at chunk j ^ ((c >> 3) & 15): the 32 lanes writing one
-// column position of 32 blocks hit 16 distinct bank groups) and leaves as
-// 16-byte stores, a wave writing four 256-byte rows of dZ^T per instruction.
-// Rows of the last tile past the count are written as 0 in both layouts (the
-// dW GEMM reads K up to the next multiple of 64).  Tiles wholly past the
-// chunk's count are skipped (the backward GEMMs read rows only up to the count).
-constexpr int kDzT = 512;
-constexpr int kDzRows = 128;  // rows per tile
-
 __device__ __forceinline__ uint32_t bf16_bits(float f) { return (uint32_t)f32_to_bf16(f); }
-
-__global__ void __launch_bounds__(kDzT) k_dz_from_y(
-    uint16_t* __restrict__ yz, int64_t Vpad, int64_t Tc, int64_t V,
-    const int32_t* __restrict__ rows, const int32_t* __restrict__ ids,
-    const int32_t* __restrict__ meta, int64_t c0, const float* __restrict__ pm,
-    const float* __restrict__ lse, const float* __restrict__ grad, const float* __restrict__ ce,
-    const float* __restrict__ cmu, int ntc, uint16_t* __restrict__ dzt, int64_t ldt) {
-  __shared__ float rL[kDzRows], rC[kDzRows], rM[kDzRows], rE[kDzRows], rD[kDzRows];
-  __shared__ int rY[kDzRows];
-  __shared__ __attribute__((aligned(16))) uint16_t stT[256 * kDzRows];  // [tile column][tile row]
-  const int tid = threadIdx.x;
-  const int nt = (int)(blockIdx.x % ntc), mt = (int)(blockIdx.x / ntc);
-  int64_t count = (int64_t)meta[0] - c0;
-  count = count < 0 ? 0 : (count > Tc ? Tc : count);
-  const int64_t r0 = (int64_t)mt * kDzRows;
-  if (r0 >= count) return;
-  const int64_t n0 = (int64_t)nt * 256;
-  const int cb = tid & 31, rb = tid >> 5;
-  uint16_t* src = yz + (r0 + rb * 8) * Vpad + n0 + cb * 8;
-  // this thread's eight row pieces, all in flight before the row parameters
-  uint4 in[8];
-#pragma unroll
-  for (int r = 0; r < 8; ++r) in[r] = *(const uint4*)(src + r * Vpad);
-  if (tid < kDzRows) {
-    const int64_t r = r0 + tid;
-    float L_ = 0.f, C_ = 0.f, M_ = 0.f, E_ = 0.f, D_ = 0.f;
-    int Y_ = -1;
-    if (r < count) {
-      const int t = rows[c0 + r];
-      L_ = lse[t];
-      C_ = grad[t];
-      Y_ = ids[t];
-      M_ = pm[(int64_t)nt * Tc + r];
-      if (ce) {
-        E_ = ce[r];
-        D_ = M_ - cmu[r];  // z - mu = y + (tile maximum - mu)
-      }
-    }
-    rL[tid] = L_ * kLog2e;
-    rC[tid] = C_;
-    rM[tid] = M_ * kLog2e;
-    rE[tid] = E_;
-    rD[tid] = D_;
-    rY[tid] = Y_;
-  }
-  __syncthreads();
-  uint32_t tcol[8][4];  // column q of the block: its 8 rows as bf16 pairs
-#pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    const int rl = rb * 8 + r;
-    const float Lk = rL[rl], Ck = rC[rl], Mk = rM[rl], Ek = rE[rl], Dk = rD[rl];
-    const int Yk = rY[rl];
-    const bool rv = r0 + rl < count;
-    const uint32_t w[4] = {in[r].x, in[r].y, in[r].z, in[r].w};
-    uint32_t o[4];
-#pragma unroll
-    for (int q2 = 0; q2 < 4; ++q2) {
-      uint32_t pair = 0;
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int q = 2 * q2 + hh;
-        const int64_t col = n0 + cb * 8 + q;
-        const uint16_t hb = (uint16_t)(w[q2] >> (hh * 16));
-        const float yv = (float)__builtin_bit_cast(_Float16, hb);
-        const float p = exp2f(fmaf(yv, kLog2e, Mk - Lk));
-        float d = dlogit(Ck, Ek, -Dk, p, yv, col == (int64_t)Yk);
-        d = (rv && col < V) ? d : 0.f;
-        const uint32_t b = bf16_bits(d);
-        pair |= b << (hh * 16);
-        if (r & 1) tcol[q][r >> 1] |= b << 16;
-        else tcol[q][r >> 1] = b;
-      }
-      o[q2] = pair;
-    }
-    *(uint4*)(src + r * Vpad) = make_uint4(o[0], o[1], o[2], o[3]);
-  }
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int c = cb * 8 + q;
-    *(uint4*)(stT + c * kDzRows + ((rb ^ (cb & 15)) << 3)) =
-        make_uint4(tcol[q][0], tcol[q][1], tcol[q][2], tcol[q][3]);
-  }
-  __syncthreads();
-  // dZ^T rows n0 .. n0 + 255, columns r0 .. r0 + 127: 16 chunks per row
-#pragma unroll
-  for (int it = 0; it < 8; ++it) {
-    const int i = it * kDzT + tid, c = i >> 4, j = i & 15;
-    const uint4 v = *(const uint4*)(stT + c * kDzRows + ((j ^ ((c >> 3) & 15)) << 3));
-    *(uint4*)(dzt + (n0 + c) * ldt + r0 + j * 8) = v;
-  }
-}
 
 // Hc^T [d, ldt] of the chunk's compacted hidden rows [c0, c0 + count): 64 x 64
 // tiles through LDS; columns count .. (next multiple of 256) are written as 0.
@@ -193,6 +90,156 @@ __global__ void __launch_bounds__(256) k_transpose_hc(const uint16_t* __restrict
   }
 }
 
+// Tile-blocked variant (the layout the step's backward GEMMs read, blk_index):
+// y, and dZ in its place, are [Tc, Vpad] blocked; dZ^T is [Vpad, Tc] blocked.
+// One 256-thread workgroup per (256-row panel, 256-column vocabulary tile):
+// the tile's four 256 x 64 blocks, 128 contiguous KiB of y.  Thread tid owns
+// the 8 x 8 piece (rows rb * 8 .., columns cb * 8 ..) of each block; the next
+// block's eight row pieces are in flight while a block is converted (about
+// 120 registers, so four workgroups share a CU).  dZ goes back in place, and
+// column q of a piece (eight consecutive chunk rows of dZ^T row v) is 16
+// contiguous bytes of dZ^T, so the transposed copy needs no LDS: the 8 lanes
+// with one cb fill a whole 128-byte row piece of a dZ^T block.  Rows of the
+// panel past the count and columns past V are written as 0 in both layouts
+// (the dW GEMM reads K up to the next multiple of 64); panels wholly past the
+// count are skipped (the backward GEMMs read rows only up to the count).
+constexpr int kDzbT = 256;
+
+template <bool BONUS>
+__global__ void __launch_bounds__(kDzbT, BONUS ? 2 : 3) k_dz_from_y_blk(
+    uint16_t* __restrict__ yz, int64_t Vpad, int64_t Tc, int64_t V,
+    const int32_t* __restrict__ rows, const int32_t* __restrict__ ids,
+    const int32_t* __restrict__ meta, int64_t c0, const float* __restrict__ pm,
+    const float* __restrict__ lse, const float* __restrict__ grad, const float* __restrict__ ce,
+    const float* __restrict__ cmu, int ntc, uint16_t* __restrict__ dzt) {
+  __shared__ float rL[256], rC[256], rE[256], rD[256];
+  __shared__ int rY[256];
+  const int tid = threadIdx.x;
+  const int nt = (int)(blockIdx.x % ntc), pn = (int)(blockIdx.x / ntc);
+  int64_t count = (int64_t)meta[0] - c0;
+  count = count < 0 ? 0 : (count > Tc ? Tc : count);
+  const int64_t r0 = (int64_t)pn * 256;
+  if (r0 >= count) return;
+  const int cb = tid & 7, rb = tid >> 3;
+  uint16_t* const blk = yz + (((int64_t)pn * (Vpad >> 6) + (int64_t)nt * 4) << 14) + rb * 512 + cb * 8;
+  uint4 cur[8], nxt[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) cur[r] = *(const uint4*)(blk + r * 64);
+  {
+    const int64_t r = r0 + tid;
+    float L_ = 0.f, C_ = 0.f, M_ = 0.f, E_ = 0.f, D_ = 0.f;
+    int Y_ = -1;
+    if (r < count) {
+      const int t = rows[c0 + r];
+      L_ = lse[t];
+      C_ = grad[t];
+      Y_ = ids[t];
+      M_ = pm[(int64_t)nt * Tc + r];
+      if (BONUS) {
+        E_ = ce[r];
+        D_ = M_ - cmu[r];  // z - mu = y + (tile maximum - mu)
+      }
+    }
+    rL[tid] = (M_ - L_) * kLog2e;  // p = 2^(y log2 e + (tile maximum - lse) log2 e)
+    rC[tid] = C_;
+    rE[tid] = E_;
+    rD[tid] = D_;
+    rY[tid] = Y_;
+  }
+  __syncthreads();
+  uint16_t* const tb = dzt + (((int64_t)nt * (Tc >> 6) + (r0 >> 6) + (rb >> 3)) << 14) + ((rb & 7) << 3);
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    if (kb < 3) {
+#pragma unroll
+      for (int r = 0; r < 8; ++r) nxt[r] = *(const uint4*)(blk + (kb + 1) * 16384 + r * 64);
+    }
+    uint32_t tcol[8][4];  // column q of the piece: its 8 rows as bf16 pairs
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int rl = rb * 8 + r;
+      const float Lk = rL[rl], Ck = rC[rl];
+      const float Ek = BONUS ? rE[rl] : 0.f, Dk = BONUS ? rD[rl] : 0.f;
+      const int Yk = rY[rl];
+      const bool rv = r0 + rl < count;
+      const uint32_t w[4] = {cur[r].x, cur[r].y, cur[r].z, cur[r].w};
+      uint32_t o[4];
+#pragma unroll
+      for (int q2 = 0; q2 < 4; ++q2) {
+        uint32_t pair = 0;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int q = 2 * q2 + hh;
+          const int64_t col = (int64_t)nt * 256 + kb * 64 + cb * 8 + q;
+          const uint16_t hb = (uint16_t)(w[q2] >> (hh * 16));
+          const float yv = (float)__builtin_bit_cast(_Float16, hb);
+          const float p = exp2f(fmaf(yv, kLog2e, Lk));
+          float d = BONUS ? dlogit(Ck, Ek, -Dk, p, yv, col == (int64_t)Yk)
+                          : Ck * ((col == (int64_t)Yk ? 1.f : 0.f) - p);
+          d = (rv && col < V) ? d : 0.f;
+          const uint32_t b = bf16_bits(d);
+          pair |= b << (hh * 16);
+          if (r & 1) tcol[q][r >> 1] |= b << 16;
+          else tcol[q][r >> 1] = b;
+        }
+        o[q2] = pair;
+      }
+      *(uint4*)(blk + kb * 16384 + r * 64) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      *(uint4*)(tb + ((kb * 64 + cb * 8 + q) << 6)) =
+          make_uint4(tcol[q][0], tcol[q][1], tcol[q][2], tcol[q][3]);
+    if (kb < 3) {
+#pragma unroll
+      for (int r = 0; r < 8; ++r) cur[r] = nxt[r];
+    }
+  }
+}
+
+// Row-major src [rows, ncols] (bf16) to the tile-blocked transpose dst
+// [ncols_pad, Kp]: dst(j, t) = src[r0 + t][j] for the rows t < n (n = nrows,
+// or the device count minus r0 clamped to [0, nrows] when meta is given);
+// rows t in [n, next multiple of 256) and columns j in [ncols, ncols_pad) are
+// written as 0.  A 64 x 64 tile per workgroup through LDS; the output piece
+// (64 rows j of 64 consecutive t) is 8 contiguous KiB of one block.
+__global__ void __launch_bounds__(256) k_transpose_blk(const uint16_t* __restrict__ src,
+                                                       int64_t ncols,
+                                                       const int32_t* __restrict__ meta,
+                                                       int64_t r0, int64_t nrows, int64_t Kp,
+                                                       uint16_t* __restrict__ dst) {
+  __shared__ uint16_t t[64][66];
+  int64_t n = nrows;
+  if (meta) {
+    n = (int64_t)meta[0] - r0;
+    n = n < 0 ? 0 : (n > nrows ? nrows : n);
+  }
+  const int64_t kend = (n + 255) / 256 * 256;
+  const int64_t t0 = (int64_t)blockIdx.x * 64, j0 = (int64_t)blockIdx.y * 64;
+  if (t0 >= kend) return;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int c = it * 256 + tid, row = c >> 3, ch = c & 7;
+    const int64_t tt = t0 + row, j = j0 + ch * 8;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (tt < n && j < ncols) v = *(const uint4*)(src + (r0 + tt) * ncols + j);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t[row][ch * 8 + e] = (uint16_t)(w[e >> 1] >> ((e & 1) * 16));
+  }
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int c = it * 256 + tid, jr = c >> 3, tc = c & 7;
+    uint32_t o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      o[e] = (uint32_t)t[tc * 8 + 2 * e][jr] | ((uint32_t)t[tc * 8 + 2 * e + 1][jr] << 16);
+    *(uint4*)(dst + blk_index(j0 + jr, t0 + tc * 8, Kp)) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
 hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int64_t c0,
                             int64_t Tc, const float* pm, const float* ps, const float* pu,
                             int ntiles, const float* zy, const float* old, const float* ref,
@@ -204,22 +251,34 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
   return hipGetLastError();
 }
 
-hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
-                            const int32_t* rows, const int32_t* ids, const int32_t* meta,
-                            int64_t c0, const float* pm, const float* lse, const float* grad,
-                            const float* ce, const float* cmu, uint16_t* dzt, int64_t ldt,
-                            hipStream_t s) {
-  const int ntc = (int)(Vpad / 256);
-  const int64_t nb = (Tc / kDzRows) * ntc;
-  k_dz_from_y<<<(unsigned)nb, kDzT, 0, s>>>(yz, Vpad, Tc, V, rows, ids, meta, c0, pm, lse, grad,
-                                            ce, cmu, ntc, dzt, ldt);
-  return hipGetLastError();
-}
-
 hipError_t launch_transpose_hc(const uint16_t* hc, int64_t d, const int32_t* meta, int64_t c0,
                                int64_t Tc, uint16_t* hct, int64_t ldt, hipStream_t s) {
   const dim3 grid((unsigned)(Tc / 64), (unsigned)((d + 63) / 64));
   k_transpose_hc<<<grid, 256, 0, s>>>(hc, d, meta, c0, Tc, hct, ldt);
+  return hipGetLastError();
+}
+
+hipError_t launch_dz_from_y_blk(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
+                                const int32_t* rows, const int32_t* ids, const int32_t* meta,
+                                int64_t c0, const float* pm, const float* lse, const float* grad,
+                                const float* ce, const float* cmu, uint16_t* dzt, hipStream_t s) {
+  const int ntc = (int)(Vpad / 256);
+  const int64_t nb = (Tc / 256) * ntc;
+  if (nb > 0 && ce)
+    k_dz_from_y_blk<true><<<(unsigned)nb, kDzbT, 0, s>>>(yz, Vpad, Tc, V, rows, ids, meta, c0, pm,
+                                                         lse, grad, ce, cmu, ntc, dzt);
+  else if (nb > 0)
+    k_dz_from_y_blk<false><<<(unsigned)nb, kDzbT, 0, s>>>(yz, Vpad, Tc, V, rows, ids, meta, c0,
+                                                          pm, lse, grad, ce, cmu, ntc, dzt);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_blk(const uint16_t* src, int64_t ncols, const int32_t* meta,
+                                int64_t r0, int64_t nrows, int64_t Kp, int64_t ncols_pad,
+                                uint16_t* dst, hipStream_t s) {
+  const dim3 grid((unsigned)(Kp / 64), (unsigned)(ncols_pad / 64));
+  if (Kp > 0 && ncols_pad > 0)
+    k_transpose_blk<<<grid, 256, 0, s>>>(src, ncols, meta, r0, nrows, Kp, dst);
   return hipGetLastError();
 }
 

@@ -229,7 +229,8 @@ BwdWs carve_bwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dty
 int64_t bwd_align(int dtype) { return dtype == RFT_BF16 ? kBf16Align : kF32Align; }
 
 // Upper bound of a row chunk: the dW GEMM reads 256-row tiles of the
-// transposed chunk buffers (row pitch Tc + kLdtPad, bf16) through one buffer
+// transposed chunk buffers (row pitch Tc + kLdtPad, bf16, or 256-row panels
+// of 256 Tc values in the fused step's blocked layout) through one buffer
 // descriptor with 32-bit offsets, so 256 (Tc + kLdtPad) 2 bytes must stay
 // below 2^31.  2^21 rows is below that bound for both dtypes.
 constexpr int64_t kMaxTc = (int64_t)1 << 21;
@@ -257,7 +258,9 @@ int64_t bwd_tc_for(const rft_tokens& tok, int64_t d, int64_t V, int dtype, size_
 // Fused step (bf16): compacted hidden rows, transposed weight, per-chunk
 // log-sum-exp partials, the sampled logits, the loss partials, the chunk
 // buffer (fp16 y, then bf16 dZ, in dz) and the chunk's dZ^T [Vpad, Tc] and
-// hidden rows transposed [d, Tc] (the weight gradient's K-contiguous operands).
+// hidden rows transposed [dpad, Tc] (the weight gradient's K-contiguous
+// operands).  W^T, dz, dZ^T and Hc^T are tile-blocked (blk_index): every
+// k-step of the backward GEMMs reads contiguous 32 KiB blocks.
 struct StepWs {
   TokMeta m;
   uint16_t *hc, *wt, *dz, *dzt, *hct;
@@ -265,7 +268,7 @@ struct StepWs {
   float *ce, *cmu;  // per chunk row: entropy-bonus coefficient and softmax mean
   LossPartial* parts;
   int ntiles;
-  int64_t Tc, Vpad, ldt;
+  int64_t Tc, Vpad, dpad;
   size_t bytes;
 };
 StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
@@ -276,8 +279,9 @@ StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64
   w.Tc = Tc;
   w.Vpad = round_up(V, kBf16Align);
   w.ntiles = (int)(w.Vpad / kMfmaTileN);
+  w.dpad = round_up(d, kBf16Align);
   w.hc = c.take<uint16_t>((size_t)T1 * d);
-  w.wt = c.take<uint16_t>((size_t)d * w.Vpad);
+  w.wt = c.take<uint16_t>((size_t)w.dpad * w.Vpad);
   w.pm = c.take<float>((size_t)w.ntiles * Tc);
   w.ps = c.take<float>((size_t)w.ntiles * Tc);
   w.pu = c.take<float>((size_t)w.ntiles * Tc);
@@ -286,9 +290,8 @@ StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64
   w.cmu = c.take<float>((size_t)Tc);
   w.parts = c.take<LossPartial>((size_t)((T1 + 255) / 256));
   w.dz = c.take<uint16_t>((size_t)Tc * w.Vpad);
-  w.ldt = Tc + kLdtPad;
-  w.dzt = c.take<uint16_t>((size_t)w.Vpad * w.ldt);
-  w.hct = c.take<uint16_t>((size_t)d * w.ldt);
+  w.dzt = c.take<uint16_t>((size_t)w.Vpad * Tc);
+  w.hct = c.take<uint16_t>((size_t)w.dpad * Tc);
   w.bytes = c.bytes();
   return w;
 }
@@ -780,7 +783,7 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
     RFT_HIP(launch_fill_zero(lse, T, s), fn);
     if (entropy) RFT_HIP(launch_fill_zero(entropy, T, s), fn);
     RFT_HIP(launch_gather_rows16(H, d, w.m.rows, cnt, T, w.hc, s), fn);
-    RFT_HIP(launch_transpose_w(W, V, d, w.wt, w.Vpad, s), fn);
+    RFT_HIP(launch_transpose_blk(W, d, nullptr, 0, V, w.Vpad, w.dpad, w.wt, s), fn);
   }
   for (int64_t ci = 0; ci < nchunks; ++ci) {
     const int64_t c0 = ci * Tc;
@@ -791,16 +794,16 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
                              old_logp, ref, adv, c, logp, entropy, lse, grad_logp,
                              bonus ? w.ce : nullptr, w.cmu, s),
             fn);
-    RFT_HIP(launch_dz_from_y(w.dz, w.Vpad, Tc, V, w.m.rows, tok->token_ids, cnt, c0, w.pm, lse,
-                             grad_logp, bonus ? w.ce : nullptr, w.cmu, w.dzt, w.ldt, s),
+    RFT_HIP(launch_dz_from_y_blk(w.dz, w.Vpad, Tc, V, w.m.rows, tok->token_ids, cnt, c0, w.pm,
+                                 lse, grad_logp, bonus ? w.ce : nullptr, w.cmu, w.dzt, s),
             fn);
-    RFT_HIP(launch_transpose_hc(w.hc, d, cnt, c0, Tc, w.hct, w.ldt, s), fn);
+    RFT_HIP(launch_transpose_blk(w.hc, d, cnt, c0, Tc, Tc, w.dpad, w.hct, s), fn);
     RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
-                            d_hidden, d, w.m.rows, c0, 0, s),
+                            d_hidden, d, w.m.rows, c0, 0, s, 1, 1),
             fn);
     // dW = dZ^T . Hc with both operands K-contiguous (K = the chunk's rows)
-    RFT_HIP(mfma_gemm_store(w.dzt, w.ldt, w.hct, w.ldt, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight, d,
-                            nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s),
+    RFT_HIP(mfma_gemm_store(w.dzt, Tc, w.hct, Tc, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight, d,
+                            nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s, 1, 1),
             fn);
   }
   if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);

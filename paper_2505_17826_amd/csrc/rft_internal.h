@@ -299,13 +299,15 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
                             int ntiles, const float* zy, const float* old, const float* ref,
                             const float* adv, const LossConst& c, float* logp, float* ent,
                             float* lse, float* grad, float* ce, float* cmu, hipStream_t s);
-hipError_t launch_dz_from_y(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
-                            const int32_t* rows, const int32_t* ids, const int32_t* meta,
-                            int64_t c0, const float* pm, const float* lse, const float* grad,
-                            const float* ce, const float* cmu, uint16_t* dzt, int64_t ldt,
-                            hipStream_t s);
 hipError_t launch_transpose_hc(const uint16_t* hc, int64_t d, const int32_t* meta, int64_t c0,
                                int64_t Tc, uint16_t* hct, int64_t ldt, hipStream_t s);
+hipError_t launch_dz_from_y_blk(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
+                                const int32_t* rows, const int32_t* ids, const int32_t* meta,
+                                int64_t c0, const float* pm, const float* lse, const float* grad,
+                                const float* ce, const float* cmu, uint16_t* dzt, hipStream_t s);
+hipError_t launch_transpose_blk(const uint16_t* src, int64_t ncols, const int32_t* meta,
+                                int64_t r0, int64_t nrows, int64_t Kp, int64_t ncols_pad,
+                                uint16_t* dst, hipStream_t s);
 hipError_t mfma_dz(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
                    const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
@@ -313,7 +315,8 @@ hipError_t mfma_dz(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V, i
 hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, int64_t ldb,
                            int64_t M, int64_t N, int64_t K, const int32_t* cnt, int64_t cnt_off,
                            int64_t cnt_cap, int m_from_cnt, int k_from_cnt, float* C, int64_t ldc,
-                           const int32_t* rows, int64_t rows_off, int accumulate, hipStream_t s);
+                           const int32_t* rows, int64_t rows_off, int accumulate, hipStream_t s,
+                           int a_blk = 0, int b_blk = 0);
 hipError_t simt_fwd_stats(const float* H, int64_t d, const float* W, int64_t V, const int32_t* rows,
                           const int32_t* ids, const int32_t* cnt, int64_t cap, float* pm, float* ps,
                           float* pu, int64_t ldp, float* zy, hipStream_t s);
@@ -345,6 +348,14 @@ hipError_t launch_logits_fused(const float* logits, const rft_tokens& tok, const
                                rft_ppo_stats* st, hipStream_t s);
 
 constexpr int kMfmaTileN = 256;  // vocabulary columns per forward tile (bf16 path)
+
+// Tile-blocked layout of a bf16 GEMM operand X [R, K] (K-contiguous; R padded
+// to a multiple of 256, K to a multiple of 64 = Kp): 256-row panels, each
+// Kp / 64 consecutive blocks of 256 rows x 64 values, row-major in a block.
+// A k-step of a 256-row GEMM tile reads one contiguous 32 KiB block.
+__host__ __device__ constexpr int64_t blk_index(int64_t r, int64_t k, int64_t Kp) {
+  return (((r >> 8) * (Kp >> 6) + (k >> 6)) << 14) + ((r & 255) << 6) + (k & 63);
+}
 constexpr int kSimtTileN = 64;   // (fp32 path)
 
 }  // namespace rft
