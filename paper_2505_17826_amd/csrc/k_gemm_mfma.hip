@@ -210,13 +210,17 @@ __device__ __forceinline__ void stage_copy_out(const char* st, uint16_t* dst, in
 // The same tile to the tile-blocked layout: the 256 x 256 tile is four
 // consecutive 256 x 64 blocks (dst = the first), 128 contiguous KiB.  Reads
 // are those of stage_copy_out (16 lanes take 256 contiguous bytes of one LDS
-// row); every 128-byte row piece of a block is written whole.
+// row); every 128-byte row piece of a block is written whole, with
+// non-temporal stores (y is read back only after the whole forward of the
+// chunk: 4 ms less per 7B step than cached stores).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void stage_copy_out_blk(const char* st, uint16_t* dst, int tid) {
 #pragma unroll 4
   for (int it = 0; it < 16; ++it) {
     const int c = it * NT + tid, row = c >> 5, ch = c & 31;
     const uint4 v = *(const uint4*)(st + row * STG_PITCH + ch * 16);
-    *(uint4*)(dst + (ch >> 3) * (BM * BK) + row * BK + (ch & 7) * 8) = v;
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v),
+                                (u32x4*)(dst + (ch >> 3) * (BM * BK) + row * BK + (ch & 7) * 8));
   }
 }
 
