@@ -639,16 +639,18 @@ hipError_t mfma_fwd_stats(const uint16_t* Hc, int64_t d, const uint16_t* W, int6
 }
 
 // Forward of one chunk of compacted rows [c0, c0 + Tc) for the fused step:
-// partials [ntiles][Tc] indexed by the chunk row, zy by the compacted row, and
-// y = z - (row maximum over the tile) in fp16 into y, tile-blocked [Tc, Vpad]
-// (Tc a multiple of 256).
+// Hc and W tile-blocked with Kp = d rounded up to 64 (c0 and Tc multiples of
+// 256); partials [ntiles][Tc] indexed by the chunk row, zy by the compacted
+// row, and y = z - (row maximum over the tile) in fp16 into y, tile-blocked
+// [Tc, Vpad].
 hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V,
                             int64_t Vpad, const int32_t* rows, const int32_t* ids,
                             const int32_t* cnt, int64_t c0, int64_t Tc, float* pm, float* ps,
                             float* pu, float* zy, uint16_t* y, hipStream_t s) {
+  const int64_t Kp = (d + 63) / 64 * 64;
   mf::Args a = {};
-  a.A = Hc + c0 * d; a.lda = d;
-  a.B = W; a.ldb = d;
+  a.A = Hc + c0 * Kp; a.lda = Kp; a.a_blk = 1;
+  a.B = W; a.ldb = Kp; a.b_blk = 1;
   a.M = (int)Tc; a.N = (int)V; a.K = (int)d;
   a.cnt = cnt; a.cnt_off = c0; a.cnt_cap = Tc; a.m_from_cnt = 1;
   a.rows = rows; a.rows_off = c0; a.ids = ids;

@@ -197,7 +197,38 @@ __global__ void __launch_bounds__(kDzbT, BONUS ? 2 : 3) k_dz_from_y_blk(
   }
 }
 
-// Row-major src [rows, ncols] (bf16) to the tile-blocked transpose dst
+// Rows of a row-major src [*, d] (bf16) into a tile-blocked dst [npad, Kp]
+// (Kp = d rounded up to 64): dst row k = src row rows[k] (rows = nullptr: row
+// k) for k < n, n = cap or the device count clamped to [0, cap]; rows k in
+// [n, next multiple of 256) and columns d .. Kp - 1 are written as 0.  One
+// workgroup per row at a time, 16 bytes per thread: 8 lanes fill a 128-byte
+// row piece of a block.  The fused step's compacted hidden rows (the forward
+// GEMM's A) and its copy of the weight (B) are made this way.
+__global__ void __launch_bounds__(256) k_rows_to_blk(const uint16_t* __restrict__ src, int64_t d,
+                                                     const int32_t* __restrict__ rows,
+                                                     const int32_t* __restrict__ meta,
+                                                     int64_t cap, int64_t Kp,
+                                                     uint16_t* __restrict__ dst) {
+  int64_t n = cap;
+  if (meta) {
+    n = meta[0];
+    n = n < 0 ? 0 : (n > cap ? cap : n);
+  }
+  const int64_t kend = (n + 255) / 256 * 256;
+  const int64_t nch = Kp >> 3;
+  for (int64_t k = blockIdx.x; k < kend; k += gridDim.x) {
+    const bool valid = k < n;
+    const int64_t sr = valid ? (rows ? (int64_t)rows[k] : k) : 0;
+    for (int64_t c = threadIdx.x; c < nch; c += 256) {
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      if (valid && c * 8 < d) v = *(const uint4*)(src + sr * d + c * 8);
+      *(uint4*)(dst + blk_index(k, c * 8, Kp)) = v;
+    }
+  }
+}
+
+// Row-major src [rows, ncols] (bf16; tile-blocked with Kp = src_kp when
+// src_kp > 0) to the tile-blocked transpose dst
 // [ncols_pad, Kp]: dst(j, t) = src[r0 + t][j] for the rows t < n (n = nrows,
 // or the device count minus r0 clamped to [0, nrows] when meta is given);
 // rows t in [n, next multiple of 256) and columns j in [ncols, ncols_pad) are
@@ -207,7 +238,7 @@ __global__ void __launch_bounds__(256) k_transpose_blk(const uint16_t* __restric
                                                        int64_t ncols,
                                                        const int32_t* __restrict__ meta,
                                                        int64_t r0, int64_t nrows, int64_t Kp,
-                                                       uint16_t* __restrict__ dst) {
+                                                       int64_t src_kp, uint16_t* __restrict__ dst) {
   __shared__ uint16_t t[64][66];
   int64_t n = nrows;
   if (meta) {
@@ -223,7 +254,8 @@ __global__ void __launch_bounds__(256) k_transpose_blk(const uint16_t* __restric
     const int c = it * 256 + tid, row = c >> 3, ch = c & 7;
     const int64_t tt = t0 + row, j = j0 + ch * 8;
     uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (tt < n && j < ncols) v = *(const uint4*)(src + (r0 + tt) * ncols + j);
+    if (tt < n && j < ncols)
+      v = *(const uint4*)(src + (src_kp ? blk_index(r0 + tt, j, src_kp) : (r0 + tt) * ncols + j));
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int e = 0; e < 8; ++e) t[row][ch * 8 + e] = (uint16_t)(w[e >> 1] >> ((e & 1) * 16));
@@ -275,10 +307,20 @@ hipError_t launch_dz_from_y_blk(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t 
 
 hipError_t launch_transpose_blk(const uint16_t* src, int64_t ncols, const int32_t* meta,
                                 int64_t r0, int64_t nrows, int64_t Kp, int64_t ncols_pad,
-                                uint16_t* dst, hipStream_t s) {
+                                uint16_t* dst, hipStream_t s, int64_t src_kp) {
   const dim3 grid((unsigned)(Kp / 64), (unsigned)(ncols_pad / 64));
   if (Kp > 0 && ncols_pad > 0)
-    k_transpose_blk<<<grid, 256, 0, s>>>(src, ncols, meta, r0, nrows, Kp, dst);
+    k_transpose_blk<<<grid, 256, 0, s>>>(src, ncols, meta, r0, nrows, Kp, src_kp, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_to_blk(const uint16_t* src, int64_t d, const int32_t* rows,
+                              const int32_t* meta, int64_t cap, int64_t Kp, uint16_t* dst,
+                              hipStream_t s) {
+  const int64_t nb = (cap + 255) / 256 * 256;
+  if (nb > 0)
+    k_rows_to_blk<<<(unsigned)(nb < 16384 ? nb : 16384), 256, 0, s>>>(src, d, rows, meta, cap,
+                                                                       Kp, dst);
   return hipGetLastError();
 }
 

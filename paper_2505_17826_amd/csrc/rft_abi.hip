@@ -263,12 +263,12 @@ int64_t bwd_tc_for(const rft_tokens& tok, int64_t d, int64_t V, int dtype, size_
 // k-step of the backward GEMMs reads contiguous 32 KiB blocks.
 struct StepWs {
   TokMeta m;
-  uint16_t *hc, *wt, *dz, *dzt, *hct;
+  uint16_t *hc, *wb, *wt, *dz, *dzt, *hct;  // hc [Tpad, Kp], wb [Vpad, Kp] blocked (forward)
   float *pm, *ps, *pu, *zy;
   float *ce, *cmu;  // per chunk row: entropy-bonus coefficient and softmax mean
   LossPartial* parts;
   int ntiles;
-  int64_t Tc, Vpad, dpad;
+  int64_t Tc, Vpad, dpad, Kp;
   size_t bytes;
 };
 StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64_t Tc) {
@@ -280,7 +280,9 @@ StepWs carve_step(void* base, const rft_tokens& tok, int64_t d, int64_t V, int64
   w.Vpad = round_up(V, kBf16Align);
   w.ntiles = (int)(w.Vpad / kMfmaTileN);
   w.dpad = round_up(d, kBf16Align);
-  w.hc = c.take<uint16_t>((size_t)T1 * d);
+  w.Kp = round_up(d, 64);
+  w.hc = c.take<uint16_t>((size_t)round_up(T1, kBf16Align) * w.Kp);
+  w.wb = c.take<uint16_t>((size_t)w.Vpad * w.Kp);
   w.wt = c.take<uint16_t>((size_t)w.dpad * w.Vpad);
   w.pm = c.take<float>((size_t)w.ntiles * Tc);
   w.ps = c.take<float>((size_t)w.ntiles * Tc);
@@ -782,12 +784,13 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
     RFT_HIP(launch_fill_zero(logp, T, s), fn);
     RFT_HIP(launch_fill_zero(lse, T, s), fn);
     if (entropy) RFT_HIP(launch_fill_zero(entropy, T, s), fn);
-    RFT_HIP(launch_gather_rows16(H, d, w.m.rows, cnt, T, w.hc, s), fn);
+    RFT_HIP(launch_rows_to_blk(H, d, w.m.rows, cnt, T, w.Kp, w.hc, s), fn);
+    RFT_HIP(launch_rows_to_blk(W, d, nullptr, nullptr, V, w.Kp, w.wb, s), fn);
     RFT_HIP(launch_transpose_blk(W, d, nullptr, 0, V, w.Vpad, w.dpad, w.wt, s), fn);
   }
   for (int64_t ci = 0; ci < nchunks; ++ci) {
     const int64_t c0 = ci * Tc;
-    RFT_HIP(mfma_fwd_stats_y(w.hc, d, W, V, w.Vpad, w.m.rows, tok->token_ids, cnt, c0, Tc, w.pm,
+    RFT_HIP(mfma_fwd_stats_y(w.hc, d, w.wb, V, w.Vpad, w.m.rows, tok->token_ids, cnt, c0, Tc, w.pm,
                              w.ps, w.pu, w.zy, w.dz, s),
             fn);
     RFT_HIP(launch_step_rows(w.m, tok->token_ids, V, c0, Tc, w.pm, w.ps, w.pu, w.ntiles, w.zy,
@@ -797,7 +800,7 @@ rft_status rft_ppo_clip_step(const rft_tokens* tok, const void* hidden, const vo
     RFT_HIP(launch_dz_from_y_blk(w.dz, w.Vpad, Tc, V, w.m.rows, tok->token_ids, cnt, c0, w.pm,
                                  lse, grad_logp, bonus ? w.ce : nullptr, w.cmu, w.dzt, s),
             fn);
-    RFT_HIP(launch_transpose_blk(w.hc, d, cnt, c0, Tc, Tc, w.dpad, w.hct, s), fn);
+    RFT_HIP(launch_transpose_blk(w.hc, d, cnt, c0, Tc, Tc, w.dpad, w.hct, s, w.Kp), fn);
     RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
                             d_hidden, d, w.m.rows, c0, 0, s, 1, 1),
             fn);

@@ -307,7 +307,10 @@ hipError_t launch_dz_from_y_blk(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t 
                                 const float* ce, const float* cmu, uint16_t* dzt, hipStream_t s);
 hipError_t launch_transpose_blk(const uint16_t* src, int64_t ncols, const int32_t* meta,
                                 int64_t r0, int64_t nrows, int64_t Kp, int64_t ncols_pad,
-                                uint16_t* dst, hipStream_t s);
+                                uint16_t* dst, hipStream_t s, int64_t src_kp = 0);
+hipError_t launch_rows_to_blk(const uint16_t* src, int64_t d, const int32_t* rows,
+                              const int32_t* meta, int64_t cap, int64_t Kp, uint16_t* dst,
+                              hipStream_t s);
 hipError_t mfma_dz(const uint16_t* H, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
                    const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,
