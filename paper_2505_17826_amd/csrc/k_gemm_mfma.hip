@@ -29,8 +29,8 @@
 //              tile, rounded to fp16, row-major [rows, Vpad] (the backward
 //              then forms dZ from it instead of recomputing z).
 //   EPI_DZ     backward recompute: dZ = c (onehot(y) - p) + e p (z - mu) in bf16,
-//              written row-major [rows, Vpad] (the dH operand) and transposed
-//              [Vpad, ldzt] (the dW operand, K-contiguous).
+//              written tile-blocked [rows, Vpad] (the dH operand) and
+//              transposed, [Vpad, ldzt] (the dW operand, K-contiguous).
 //   EPI_STORE  fp32 result, optionally scattered to rows through a map and
 //              optionally added to the existing values.
 #include "rft_internal.h"
@@ -90,8 +90,8 @@ struct Args {
   int64_t p_off;                                            //   zy at rows_off + m
   uint16_t* y; int64_t ldy;                                 // EPI_STATS_Y: fp16 z - tile max,
                                                             //   tile-blocked, Kp = ldy
-  uint16_t* dz; int64_t ldz; int64_t Vvalid;                  // EPI_DZ
-  uint16_t* dzt; int64_t ldzt;                                //   and dZ^T [Vpad, ldzt] (nullptr = none)
+  uint16_t* dz; int64_t ldz; int64_t Vvalid;                  // EPI_DZ, tile-blocked (Kp = ldz)
+  uint16_t* dzt; int64_t ldzt;                                //   and dZ^T [Vpad, ldzt] blocked (nullptr = none)
   float* C; int64_t ldc; int accumulate; int c_scatter;  // EPI_STORE
 };
 
@@ -110,9 +110,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int64
 // one logical chunk) then touches 16 distinct 16-byte bank groups in every
 // group of 16 lanes, so fragment reads are conflict free.
 //
-// Stage loader: waves 0-3 issue the loads, wave w fills rows [w*64, w*64+64)
-// of the A tile and then of the B tile with 8 + 8 instructions of 8 rows each;
-// waves 4-7 only compute.  (Measured on gfx950: four loader waves issuing A
+// Stage loader: waves 0 .. NLOAD-1 issue the loads (NLOAD = 4: wave w fills
+// rows [w*64, w*64+64) of the A tile and then of the B tile with 8 + 8
+// instructions of 8 rows each; NLOAD = 2: 128 rows with 16 + 16); the other
+// waves only compute.  (Measured on gfx950: four loader waves issuing A
 // and B in two separate runs keep the L2 round trip of the direct-to-LDS
 // loads markedly shorter than eight waves or interleaved A/B loads.)  Lane l
 // writes LDS slot l of an instruction (row p*8 + l/8 of the wave's rows,
@@ -120,7 +121,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int64
 // (l%8) ^ (((p*8 + l/8) >> 1) & 7) = (l%8) ^ (l/16) ^ 4*(p&1); the two
 // parities of p take the offsets vA[0|1], vB[0|1].  Chunks at or past K are
 // read from outside the descriptor (0).
-constexpr int NLOAD = 4;
+// Loader waves per epilogue: four for the forward GEMMs, two for the fp32-store
+// GEMMs (dH, dW on blocked operands: 1-1.7% faster than four, one or eight
+// slower).
+template <int EPI> constexpr int kNLoad = EPI == EPI_STORE ? 2 : 4;
 struct LoadGeom {
   uint32_t vA[2], vB[2];  // per-lane byte offsets for even / odd p (k0 = 0)
   int kc[2];              // logical chunk * 8 (first element) for even / odd p
@@ -128,6 +132,7 @@ struct LoadGeom {
   uint32_t kA, kB;        // bytes per element of k0 (2 row-major, 512 blocked)
 };
 
+template <int NLOAD>
 __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB,
                                            char* dst, int k0, int K, const LoadGeom& lg) {
   constexpr int NI = 32 / NLOAD;  // instructions per operand per loader wave
@@ -195,30 +200,21 @@ __device__ __forceinline__ void barrier_lds() {
   asm volatile("" ::: "memory");
 }
 
-// Copy a staged 256 x 256 tile of 16-bit values (rows STG_PITCH bytes apart in
-// LDS) to dst with row stride ld: each instruction of a wave writes two
-// 512-byte rows with 16-byte stores.
-__device__ __forceinline__ void stage_copy_out(const char* st, uint16_t* dst, int64_t ld, int tid) {
-#pragma unroll 4
-  for (int it = 0; it < 16; ++it) {
-    const int c = it * NT + tid, row = c >> 5, ch = c & 31;
-    const uint4 v = *(const uint4*)(st + row * STG_PITCH + ch * 16);
-    *(uint4*)(dst + (int64_t)row * ld + ch * 8) = v;
-  }
-}
-
-// The same tile to the tile-blocked layout: the 256 x 256 tile is four
+// Copy a staged 256 x 256 tile of 16-bit values to the tile-blocked layout:
+// the 256 x 256 tile is four
 // consecutive 256 x 64 blocks (dst = the first), 128 contiguous KiB.  Reads
 // are those of stage_copy_out (16 lanes take 256 contiguous bytes of one LDS
-// row); every 128-byte row piece of a block is written whole, with
-// non-temporal stores (y is read back only after the whole forward of the
-// chunk: 4 ms less per 7B step than cached stores).
+// row, rows PITCH bytes apart); every 128-byte row piece of a block is
+// written whole, with non-temporal stores (the forward's y is read back only
+// after the whole forward of the chunk: 4 ms less per 7B step than cached
+// stores).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+template <int PITCH>
 __device__ __forceinline__ void stage_copy_out_blk(const char* st, uint16_t* dst, int tid) {
 #pragma unroll 4
   for (int it = 0; it < 16; ++it) {
     const int c = it * NT + tid, row = c >> 5, ch = c & 31;
-    const uint4 v = *(const uint4*)(st + row * STG_PITCH + ch * 16);
+    const uint4 v = *(const uint4*)(st + row * PITCH + ch * 16);
     __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v),
                                 (u32x4*)(dst + (ch >> 3) * (BM * BK) + row * BK + (ch & 7) * 8));
   }
@@ -263,6 +259,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   const int nk = (K + BK - 1) / BK;
 
   // per-lane load geometry (see load_stage): row w*64 + p*8 + (lane>>3)
+  constexpr int NLOAD = kNLoad<EPI>;
   const bool loader = wid < NLOAD;
   LoadGeom lg;
   {
@@ -342,11 +339,11 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       for (int j = 0; j < 8; ++j) acc4[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
 
     char* const ldsw = lds + (wid % NLOAD) * ((256 / NLOAD) * 128);
-    if (nk > 0 && loader) load_stage(rA, rB, ldsw, 0, K, lg);
+    if (nk > 0 && loader) load_stage<NLOAD>(rA, rB, ldsw, 0, K, lg);
     __syncthreads();  // first stage and the per-row parameters are visible to every wave
     for (int kt = 0; kt < nk; ++kt) {
       if (kt + 1 < nk && loader)
-        load_stage(rA, rB, ldsw + ((kt + 1) & 1) * STAGE, (kt + 1) * BK, K, lg);
+        load_stage<NLOAD>(rA, rB, ldsw + ((kt + 1) & 1) * STAGE, (kt + 1) * BK, K, lg);
       const char* As = lds + (kt & 1) * STAGE;
       const char* Bs = As + A_BYTES;
       {
@@ -464,7 +461,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
         __syncthreads();
         // y is tile-blocked (panel m0 of Kp = ldy columns; the tile's blocks
         // start at column n0)
-        stage_copy_out_blk(lds, g.y + (int64_t)m0 * g.ldy + (int64_t)n0 * BM, tid);
+        stage_copy_out_blk<STG_PITCH>(lds, g.y + (int64_t)m0 * g.ldy + (int64_t)n0 * BM, tid);
       }
       if (full) {
 #pragma unroll
@@ -569,7 +566,9 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
           stage_col4(st + (wm * 64 + i * 16 + q4 * 4) * STG_PITCH + (wn * 128 + j * 16 + r16) * 2,
                      hv[i][j]);
       __syncthreads();
-      stage_copy_out(st, g.dz + (int64_t)m0 * g.ldz + n0, g.ldz, tid);
+      // dZ and dZ^T are tile-blocked: the tile is four consecutive blocks of
+      // each (dZ panel m0, blocks from column n0; dZ^T panel n0, blocks from m0)
+      stage_copy_out_blk<STG_PITCH>(st, g.dz + (int64_t)m0 * g.ldz + (int64_t)n0 * BM, tid);
       if (g.dzt) {
         // dZ^T: tile column c (vocabulary) as a 512-byte row of the 256 chunk rows
         __syncthreads();  // the row-major copy has left the staging tile
@@ -580,12 +579,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
             *(uint2*)(st + (wn * 128 + j * 16 + r16) * STG_PITCH_T +
                       (wm * 64 + i * 16 + q4 * 4) * 2) = hv[i][j];
         __syncthreads();
-#pragma unroll 4
-        for (int it = 0; it < 16; ++it) {
-          const int c = it * NT + tid, row = c >> 5, ch = c & 31;
-          const uint4 v = *(const uint4*)(st + row * STG_PITCH_T + ch * 16);
-          *(uint4*)(g.dzt + (int64_t)(n0 + row) * g.ldzt + m0 + ch * 8) = v;
-        }
+        stage_copy_out_blk<STG_PITCH_T>(st, g.dzt + (int64_t)n0 * g.ldzt + (int64_t)m0 * BM, tid);
       }
     } else {  // EPI_STORE
 #pragma unroll
@@ -661,7 +655,8 @@ hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, in
 }
 
 // Backward recompute of one chunk of compacted rows [c0, c0 + Tc): dZ (bf16)
-// into dz [Tc, ldz].
+// into dz [Tc, Vpad] and dZ^T into dzt [Vpad, ldzt], both tile-blocked
+// (Tc a multiple of 256, ldzt = Tc).
 hipError_t mfma_dz(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V, int64_t Vpad,
                    const int32_t* rows, const int32_t* ids, const float* lse, const float* cgrad,
                    const float* egrad, const float* ent, const int32_t* cnt, int64_t c0,

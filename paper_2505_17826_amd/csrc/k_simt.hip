@@ -227,24 +227,6 @@ hipError_t simt_gemm_store(const float* A, int64_t sam, int64_t sak, const float
 }
 
 // ------------------------------------------------------- layout helpers ----
-// Wt[d, ldt] = W[V, d]^T (bf16), columns V..ldt-1 zero.  32x32 tiles via LDS.
-__global__ void __launch_bounds__(256) k_transpose_w(const uint16_t* __restrict__ W, int64_t V,
-                                                     int64_t d, uint16_t* __restrict__ Wt,
-                                                     int64_t ldt) {
-  __shared__ uint16_t tile[64][65];
-  int64_t v0 = (int64_t)blockIdx.x * 64, k0 = (int64_t)blockIdx.y * 64;
-  int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int r = ty; r < 64; r += 4) {
-    int64_t v = v0 + r, k = k0 + tx;
-    tile[r][tx] = (v < V && k < d) ? W[v * d + k] : (uint16_t)0;
-  }
-  __syncthreads();
-  for (int r = ty; r < 64; r += 4) {
-    int64_t k = k0 + r, v = v0 + tx;
-    if (k < d && v < ldt) Wt[k * ldt + v] = tile[tx][r];
-  }
-}
-
 // Hc[k, :] = H[rows[k], :] for the valid rows k < count (bf16, 16-byte copies):
 // the compacted hidden states every GEMM of the bf16 path reads.
 __global__ void __launch_bounds__(256) k_gather_rows16(const uint16_t* __restrict__ H, int64_t d,
@@ -281,13 +263,6 @@ hipError_t launch_fill_zero(float* out, int64_t n, hipStream_t s) {
     int64_t b = (n + 255) / 256;
     k_fill_zero<<<(unsigned)(b < 8192 ? b : 8192), 256, 0, s>>>(out, n);
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_transpose_w(const uint16_t* W, int64_t V, int64_t d, uint16_t* Wt, int64_t ldt,
-                              hipStream_t s) {
-  dim3 grid((unsigned)((ldt + 63) / 64), (unsigned)((d + 63) / 64));
-  k_transpose_w<<<grid, 256, 0, s>>>(W, V, d, Wt, ldt);
   return hipGetLastError();
 }
 

@@ -14,8 +14,8 @@
 //   k_transpose_blk  the chunk's compacted hidden rows transposed, [dpad, Tc],
 //                 and the weight transposed, [dpad, Vpad], tile-blocked (the
 //                 dW and dH GEMMs' other operands).
-// k_transpose_hc writes the row-major transposed hidden rows of the separate
-// backward (rft_ppo_clip_loss_bwd).
+// The separate backward (rft_ppo_clip_loss_bwd) uses the same blocked
+// transposes.
 // The arithmetic of k_step_rows is that of k_merge_rows and k_loss_fwd (same
 // merge order, same per-token formula), so the step and the separate calls
 // give the same log-probs and gradients bit for bit.
@@ -65,30 +65,6 @@ __global__ void __launch_bounds__(256) k_step_rows(
 }
 
 __device__ __forceinline__ uint32_t bf16_bits(float f) { return (uint32_t)f32_to_bf16(f); }
-
-// Hc^T [d, ldt] of the chunk's compacted hidden rows [c0, c0 + count): 64 x 64
-// tiles through LDS; columns count .. (next multiple of 256) are written as 0.
-__global__ void __launch_bounds__(256) k_transpose_hc(const uint16_t* __restrict__ hc, int64_t d,
-                                                      const int32_t* __restrict__ meta, int64_t c0,
-                                                      int64_t Tc, uint16_t* __restrict__ hct,
-                                                      int64_t ldt) {
-  __shared__ uint16_t t[64][66];
-  int64_t count = (int64_t)meta[0] - c0;
-  count = count < 0 ? 0 : (count > Tc ? Tc : count);
-  const int64_t kend = (count + 255) / 256 * 256;
-  const int64_t k0 = (int64_t)blockIdx.x * 64, j0 = (int64_t)blockIdx.y * 64;
-  if (k0 >= kend) return;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int r = ty; r < 64; r += 4) {
-    const int64_t k = k0 + r, j = j0 + tx;
-    t[r][tx] = (k < count && j < d) ? hc[(c0 + k) * d + j] : (uint16_t)0;
-  }
-  __syncthreads();
-  for (int r = ty; r < 64; r += 4) {
-    const int64_t j = j0 + r, k = k0 + tx;
-    if (j < d) hct[j * ldt + k] = t[tx][r];
-  }
-}
 
 // Tile-blocked variant (the layout the step's backward GEMMs read, blk_index):
 // y, and dZ in its place, are [Tc, Vpad] blocked; dZ^T is [Vpad, Tc] blocked.
@@ -280,13 +256,6 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
   const int nb = (int)((Tc + 255) / 256);
   k_step_rows<<<nb, 256, 0, s>>>(m.rows, m.row_seq, m.n_i, m.meta, ids, V, c0, Tc, pm, ps, pu,
                                  ntiles, zy, old, ref, adv, c, logp, ent, lse, grad, ce, cmu);
-  return hipGetLastError();
-}
-
-hipError_t launch_transpose_hc(const uint16_t* hc, int64_t d, const int32_t* meta, int64_t c0,
-                               int64_t Tc, uint16_t* hct, int64_t ldt, hipStream_t s) {
-  const dim3 grid((unsigned)(Tc / 64), (unsigned)((d + 63) / 64));
-  k_transpose_hc<<<grid, 256, 0, s>>>(hc, d, meta, c0, Tc, hct, ldt);
   return hipGetLastError();
 }
 

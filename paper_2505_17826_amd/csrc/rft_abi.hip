@@ -192,15 +192,11 @@ DpoCarve carve_dpo(void* base, const rft_tokens& tok) {
 
 struct BwdWs {
   TokMeta m;
-  uint16_t *hc, *wt, *dz, *dzt, *hct;  // bf16 path (dZ^T, Hc^T: [*, Tc + 128])
+  uint16_t *hc, *wt, *dz, *dzt, *hct;  // bf16 path: wt, dz, dZ^T, Hc^T tile-blocked
   float* dz32;                         // fp32 path
-  int64_t Tc, Vpad, ldt;
+  int64_t Tc, Vpad, dpad;
   size_t bytes;
 };
-// Row pitch of the transposed chunk buffers: Tc plus 128 elements, so that
-// rows are not a power of two apart (Tc is a multiple of 256; power-of-two
-// strides put every row of a tile in the same memory channel).
-constexpr int64_t kLdtPad = 128;
 constexpr int64_t kBf16Align = 256;   // row chunk / vocabulary padding of the bf16 path
 constexpr int64_t kF32Align = 64;
 constexpr int64_t kRecommendTc = 131072;
@@ -212,12 +208,12 @@ BwdWs carve_bwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dty
   w.Tc = Tc;
   if (dtype == RFT_BF16) {
     w.Vpad = round_up(V, kBf16Align);
+    w.dpad = round_up(d, kBf16Align);
     w.hc = c.take<uint16_t>((size_t)(tok.T > 0 ? tok.T : 1) * d);
-    w.wt = c.take<uint16_t>((size_t)d * w.Vpad);
+    w.wt = c.take<uint16_t>((size_t)w.dpad * w.Vpad);
     w.dz = c.take<uint16_t>((size_t)Tc * w.Vpad);
-    w.ldt = Tc + kLdtPad;
-    w.dzt = c.take<uint16_t>((size_t)w.Vpad * w.ldt);
-    w.hct = c.take<uint16_t>((size_t)d * w.ldt);
+    w.dzt = c.take<uint16_t>((size_t)w.Vpad * Tc);
+    w.hct = c.take<uint16_t>((size_t)w.dpad * Tc);
   } else {
     w.Vpad = round_up(V, kF32Align);
     w.dz32 = c.take<float>((size_t)Tc * w.Vpad);
@@ -228,13 +224,12 @@ BwdWs carve_bwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dty
 
 int64_t bwd_align(int dtype) { return dtype == RFT_BF16 ? kBf16Align : kF32Align; }
 
-// Upper bound of a row chunk: the dW GEMM reads 256-row tiles of the
-// transposed chunk buffers (row pitch Tc + kLdtPad, bf16, or 256-row panels
-// of 256 Tc values in the fused step's blocked layout) through one buffer
-// descriptor with 32-bit offsets, so 256 (Tc + kLdtPad) 2 bytes must stay
-// below 2^31.  2^21 rows is below that bound for both dtypes.
+// Upper bound of a row chunk: the dW GEMM reads 256-row panels of the
+// tile-blocked transposed chunk buffers (256 Tc bf16 values) through one
+// buffer descriptor with 32-bit offsets, so 256 Tc 2 bytes must stay below
+// 2^31.  2^21 rows is below that bound for both dtypes.
 constexpr int64_t kMaxTc = (int64_t)1 << 21;
-static_assert(256 * (kMaxTc + kLdtPad) * 2 < ((int64_t)1 << 31), "chunk tile must fit a descriptor");
+static_assert(256 * kMaxTc * 2 < ((int64_t)1 << 31), "chunk panel must fit a descriptor");
 
 int64_t bwd_tc_max(const rft_tokens& tok, int dtype) {
   int64_t a = bwd_align(dtype);
@@ -615,21 +610,21 @@ rft_status rft_ppo_clip_loss_bwd(const rft_tokens* tok, const void* hidden, cons
     const uint16_t* W = (const uint16_t*)weight;
     if (nchunks > 0) {
       RFT_HIP(launch_gather_rows16(H, d, w.m.rows, cnt, T, w.hc, s), fn);
-      RFT_HIP(launch_transpose_w(W, V, d, w.wt, w.Vpad, s), fn);
+      RFT_HIP(launch_transpose_blk(W, d, nullptr, 0, V, w.Vpad, w.dpad, w.wt, s), fn);
     }
     for (int64_t ci = 0; ci < nchunks; ++ci) {
       int64_t c0 = ci * Tc;
       RFT_HIP(mfma_dz(w.hc, d, W, V, w.Vpad, w.m.rows, tok->token_ids, lse, grad_logp,
-                      grad_entropy, entropy, cnt, c0, Tc, w.dz, w.dzt, w.ldt, s),
+                      grad_entropy, entropy, cnt, c0, Tc, w.dz, w.dzt, Tc, s),
               fn);
-      RFT_HIP(launch_transpose_hc(w.hc, d, cnt, c0, Tc, w.hct, w.ldt, s), fn);
+      RFT_HIP(launch_transpose_blk(w.hc, d, cnt, c0, Tc, Tc, w.dpad, w.hct, s), fn);
       // dH rows of this chunk: dZ [count, Vpad] . Wt[d, Vpad]^T, scattered to token rows
       RFT_HIP(mfma_gemm_store(w.dz, w.Vpad, w.wt, w.Vpad, Tc, d, w.Vpad, cnt, c0, Tc, 1, 0,
-                              d_hidden, d, w.m.rows, c0, 0, s),
+                              d_hidden, d, w.m.rows, c0, 0, s, 1, 1),
               fn);
       // dW += dZ^T . Hc over the chunk's rows, both operands K-contiguous (K = rows)
-      RFT_HIP(mfma_gemm_store(w.dzt, w.ldt, w.hct, w.ldt, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight,
-                              d, nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s),
+      RFT_HIP(mfma_gemm_store(w.dzt, Tc, w.hct, Tc, V, d, Tc, cnt, c0, Tc, 0, 1, d_weight, d,
+                              nullptr, 0, (ci > 0 || accumulate_dw) ? 1 : 0, s, 1, 1),
               fn);
     }
     if (nchunks == 0 && !accumulate_dw) RFT_HIP(launch_fill_zero(d_weight, V * d, s), fn);

@@ -299,8 +299,6 @@ hipError_t launch_step_rows(const TokMeta& m, const int32_t* ids, int64_t V, int
                             int ntiles, const float* zy, const float* old, const float* ref,
                             const float* adv, const LossConst& c, float* logp, float* ent,
                             float* lse, float* grad, float* ce, float* cmu, hipStream_t s);
-hipError_t launch_transpose_hc(const uint16_t* hc, int64_t d, const int32_t* meta, int64_t c0,
-                               int64_t Tc, uint16_t* hct, int64_t ldt, hipStream_t s);
 hipError_t launch_dz_from_y_blk(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t V,
                                 const int32_t* rows, const int32_t* ids, const int32_t* meta,
                                 int64_t c0, const float* pm, const float* lse, const float* grad,
@@ -332,8 +330,6 @@ hipError_t simt_gemm_store(const float* A, int64_t sam, int64_t sak, const float
                            int64_t K, const int32_t* cnt, int64_t cnt_off, int64_t cnt_cap,
                            int m_from_cnt, int k_from_cnt, float* C, int64_t ldc,
                            const int32_t* rows, int64_t rows_off, int accumulate, hipStream_t s);
-hipError_t launch_transpose_w(const uint16_t* W, int64_t V, int64_t d, uint16_t* Wt, int64_t ldt,
-                              hipStream_t s);
 hipError_t launch_gather_rows16(const uint16_t* H, int64_t d, const int32_t* rows,
                                 const int32_t* cnt, int64_t cap, uint16_t* Hc, hipStream_t s);
 hipError_t launch_fill_zero(float* out, int64_t n, hipStream_t s);
