@@ -74,6 +74,9 @@ def parse():
                     help="workspace of the fused step in GB (default 0: the library's "
                          "recommended size); the step takes the largest row chunk that fits, "
                          "so a smaller workspace means more, smaller chunks")
+    ap.add_argument("--ws-one-chunk", action="store_true",
+                    help="size the workspace so that one row chunk holds the batch's valid "
+                         "rows (rft_workspace_bytes_rows)")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GB",
                     help="only run a plain device copy of GB gigabytes (the known-size kernel "
                          "that scales the HBM byte counters) and exit")
@@ -382,8 +385,12 @@ def main():
         ws_fwd = torch.empty(R.workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, tok, d, V, dt),
                              dtype=torch.uint8, device=dev)
         ws_step_bytes = R.workspace_bytes(R.RFT_OP_PPO_STEP, tok, d, V, dt)
+        if args.ws_one_chunk:
+            # N is known here, outside the timed region
+            ws_step_bytes = R.workspace_bytes_rows(R.RFT_OP_PPO_STEP, tok, d, V, dt, max(N, 1))
         if args.ws_gb > 0:
             ws_step_bytes = int(args.ws_gb * 1e9)
+        chunk_rows = R.chunk_rows(R.RFT_OP_PPO_STEP, tok, d, V, dt, ws_step_bytes)
         ws_step = torch.empty(ws_step_bytes, dtype=torch.uint8, device=dev)
         # rollout-side log-probs for the old / reference policies (setup, untimed)
         R.rft_token_logprobs(tok, b.H, b.W, logp=logp, entropy=ent, lse=lse, ws=ws_fwd)
@@ -454,6 +461,7 @@ def main():
         "data": "synthetic (seeded; shapes and distributions of the workload, no dataset)",
         "config": {"workload": cfg.name, "n_seq": n_seq, "group": cfg.group, "T": T,
                    "workspace_bytes": (ws_step_bytes if cfg.dtype != "logits" else None),
+                   "chunk_rows": (chunk_rows if cfg.dtype != "logits" else None),
                    "valid_tokens": N, "V": V, "d": cfg.d, "eps": [cfg.eps_low, cfg.eps_high],
                    "kl_coef": cfg.beta, "agg": cfg.agg},
     }

@@ -174,6 +174,15 @@ const char* rft_last_error(void);
 size_t rft_workspace_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
 size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
 
+/* Workspace bytes with which RFT_OP_PPO_BWD or RFT_OP_PPO_STEP processes row
+ * chunks of chunk_rows rows (rounded up to the chunk alignment, 256 for bf16 and
+ * 64 for fp32, and capped at the largest chunk the layout can use).  A caller
+ * that knows its count of valid rows can size the workspace so that one chunk
+ * holds them all (the step then runs each GEMM once instead of once per chunk).
+ * Returns 0 for other operations or invalid arguments. */
+size_t rft_workspace_bytes_rows(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype,
+                                int64_t chunk_rows);
+
 /* Rows per chunk that RFT_OP_PPO_BWD or RFT_OP_PPO_STEP processes with a
  * workspace of ws_bytes for this layout and sizes (the calls loop over
  * ceil(T / chunk) chunks); 0 if the workspace is too small, the operation has

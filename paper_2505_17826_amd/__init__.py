@@ -75,6 +75,8 @@ _SIGS = {
     "rft_ppo_clip_fused_logits_noalloc": (ctypes.c_int, [ctypes.POINTER(rft_tokens), _p, _i64, _p,
                                                          _p, _p, ctypes.POINTER(rft_ppo_params),
                                                          _p, _p, _p, _p, _p, _p, _p]),
+    "rft_workspace_bytes_rows": (ctypes.c_size_t, [ctypes.c_int, ctypes.POINTER(rft_tokens), _i64,
+                                                   _i64, ctypes.c_int, _i64]),
     "rft_chunk_rows": (_i64, [ctypes.c_int, ctypes.POINTER(rft_tokens), _i64, _i64, ctypes.c_int,
                               ctypes.c_size_t]),
     "rft_group_advantages": (ctypes.c_int, [_p, _i64, ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
@@ -211,6 +213,12 @@ def workspace_bytes(op, tokens: Tokens, d=0, V=1, dtype=RFT_F32, minimum=False) 
     tk = tokens.c()
     f = L.rft_workspace_min_bytes if minimum else L.rft_workspace_bytes
     return int(f(op, ctypes.byref(tk), d, V, dtype))
+
+
+def workspace_bytes_rows(op, tokens: Tokens, d, V, dtype, rows) -> int:
+    """Workspace with which RFT_OP_PPO_BWD / RFT_OP_PPO_STEP runs row chunks of `rows` rows."""
+    tk = tokens.c()
+    return int(lib().rft_workspace_bytes_rows(op, ctypes.byref(tk), d, V, dtype, rows))
 
 
 def chunk_rows(op, tokens: Tokens, d, V, dtype, ws_bytes) -> int:

@@ -437,6 +437,20 @@ size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t
   return rft_workspace_bytes(op, tok, d, V, dtype);
 }
 
+size_t rft_workspace_bytes_rows(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype,
+                                int64_t chunk_rows) {
+  if (op != RFT_OP_PPO_BWD && op != RFT_OP_PPO_STEP) return 0;
+  if (!tok || tok->T < 0 || tok->n_seq < 0 || V < 1 || d < 1 || chunk_rows < 1) return 0;
+  if (dtype != RFT_F32 && dtype != RFT_BF16) return 0;
+  int64_t tc = round_up(chunk_rows, bwd_align(dtype));
+  const int64_t tmax = bwd_tc_max(*tok, dtype);
+  if (tc > tmax) tc = tmax;
+  if (op == RFT_OP_PPO_STEP)
+    return dtype == RFT_BF16 ? carve_step(nullptr, *tok, d, V, tc).bytes
+                             : step_f32_bytes(*tok, d, V, tc);
+  return carve_bwd(nullptr, *tok, d, V, dtype, tc).bytes;
+}
+
 int64_t rft_chunk_rows(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype,
                        size_t ws_bytes) {
   if (!tok || tok->T < 0 || tok->n_seq < 0 || V < 1 || d < 1) return 0;

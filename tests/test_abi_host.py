@@ -229,9 +229,9 @@ def test_header_documents_every_entry_point():
 
 def test_chunk_rows_are_bounded_for_huge_row_counts():
     """A huge T with a tiny vocabulary and a workspace big enough for one
-    chunk of every row: the chunk stays at or below 2^21 rows, so the
-    transposed chunk tiles of the weight-gradient GEMM (256 rows of pitch
-    chunk + 128, bf16) fit one 2 GiB buffer descriptor."""
+    chunk of every row: the chunk stays at or below 2^21 rows, so a 256-row
+    panel of the weight-gradient GEMM's tile-blocked transposed chunk buffers
+    (256 x chunk bf16 values) fits one 2 GiB buffer descriptor."""
     L = R.lib()
     T = (1 << 30) - 256
     tk = _tok(T=T, n_seq=1 << 20)
@@ -240,7 +240,7 @@ def test_chunk_rows_are_bounded_for_huge_row_counts():
             ws = 1 << 50   # far more than any chunk needs
             c = L.rft_chunk_rows(op, ctypes.byref(tk), 8, 256, dt, ws)
             assert 0 < c <= (1 << 21), (op, dt, c)
-            assert 256 * (c + 128) * 2 < (1 << 31)
+            assert 256 * c * 2 < (1 << 31)
             assert c % (256 if dt == R.RFT_BF16 else 64) == 0
             # too small a workspace gives 0, the minimum one the smallest chunk
             mn = L.rft_workspace_min_bytes(op, ctypes.byref(tk), 8, 256, dt)
@@ -275,3 +275,37 @@ def test_noalloc_entry_point_rejects_layouts_beyond_its_scratch():
                                              fake, ctypes.byref(p), fake, None, None, None, fake,
                                              fake, None)
     assert st == R.RFT_E_SHAPE
+
+
+def test_workspace_for_a_chosen_chunk():
+    """rft_workspace_bytes_rows: the workspace it gives runs chunks of the rows
+    asked for (rounded up to the alignment; at least that many for the fp32
+    step, whose small-chunk workspace is set by its forward), one chunk for a batch's
+    valid rows when asked for their count; it grows with the chunk, caps at
+    the largest chunk the layout allows, and is 0 for other operations and
+    invalid arguments."""
+    L = R.lib()
+    d, V = 3584, 152064
+    tk = _tok(T=262144, n_seq=128)
+    for op in (R.RFT_OP_PPO_STEP, R.RFT_OP_PPO_BWD):
+        for dt, a in ((R.RFT_BF16, 256), (R.RFT_F32, 64)):
+            for rows in (1, 1000, 131072, 167973):
+                ws = L.rft_workspace_bytes_rows(op, ctypes.byref(tk), d, V, dt, rows)
+                want = (rows + a - 1) // a * a
+                got = L.rft_chunk_rows(op, ctypes.byref(tk), d, V, dt, ws)
+                if op == R.RFT_OP_PPO_STEP and dt == R.RFT_F32:
+                    # the fp32 step's workspace is set by its forward's partials for
+                    # small chunks, which leaves room for a larger backward chunk
+                    assert got >= want, (op, dt, rows, got)
+                else:
+                    assert got == want, (op, dt, rows, got)
+            small = L.rft_workspace_bytes_rows(op, ctypes.byref(tk), d, V, dt, 1000)
+            big = L.rft_workspace_bytes_rows(op, ctypes.byref(tk), d, V, dt, 100000)
+            assert L.rft_workspace_min_bytes(op, ctypes.byref(tk), d, V, dt) <= small < big
+            # beyond the layout's rows: capped at a chunk of all of them
+            cap = L.rft_workspace_bytes_rows(op, ctypes.byref(tk), d, V, dt, 1 << 40)
+            assert cap == L.rft_workspace_bytes_rows(op, ctypes.byref(tk), d, V, dt, 262144)
+    assert L.rft_workspace_bytes_rows(R.RFT_OP_PPO_FWD, ctypes.byref(tk), d, V, R.RFT_BF16, 4096) == 0
+    assert L.rft_workspace_bytes_rows(R.RFT_OP_PPO_STEP, ctypes.byref(tk), d, V, R.RFT_BF16, 0) == 0
+    assert L.rft_workspace_bytes_rows(R.RFT_OP_PPO_STEP, ctypes.byref(tk), d, V, 7, 4096) == 0
+    assert L.rft_workspace_bytes_rows(R.RFT_OP_PPO_STEP, None, d, V, R.RFT_BF16, 4096) == 0
