@@ -64,15 +64,16 @@ __global__ void __launch_bounds__(256) k_step_rows(
   }
 }
 
-__device__ __forceinline__ uint32_t bf16_bits(float f) { return (uint32_t)f32_to_bf16(f); }
-
 // Tile-blocked variant (the layout the step's backward GEMMs read, blk_index):
 // y, and dZ in its place, are [Tc, Vpad] blocked; dZ^T is [Vpad, Tc] blocked.
 // One 256-thread workgroup per (256-row panel, 256-column vocabulary tile):
 // the tile's four 256 x 64 blocks, 128 contiguous KiB of y.  Thread tid owns
 // the 8 x 8 piece (rows rb * 8 .., columns cb * 8 ..) of each block; the next
-// block's eight row pieces are in flight while a block is converted (about
-// 120 registers, so four workgroups share a CU).  dZ goes back in place, and
+// block's eight row pieces are in flight while a block is converted (168
+// registers without the entropy bonus: three workgroups per CU).  The
+// conversion has no branches (the hardware exp2 and packed bf16 conversion,
+// 32-bit indices, column masks only in the last vocabulary tile); the pass
+// is bound by HBM (5.3 TB/s on its 153 GB at the 7B shape).  dZ goes back in place, and
 // column q of a piece (eight consecutive chunk rows of dZ^T row v) is 16
 // contiguous bytes of dZ^T, so the transposed copy needs no LDS: the 8 lanes
 // with one cb fill a whole 128-byte row piece of a dZ^T block.  Rows of the
@@ -81,23 +82,85 @@ __device__ __forceinline__ uint32_t bf16_bits(float f) { return (uint32_t)f32_to
 // count are skipped (the backward GEMMs read rows only up to the count).
 constexpr int kDzbT = 256;
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+// Two fp32 values to a packed bf16 pair (a in the low half), rounded to
+// nearest even by the hardware conversion.
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+
+// dZ of one thread's 8 x 8 piece of a block (zrow: its first row in the block;
+// zcol: its first row of the transposed piece in the dZ^T block; rows rb * 8 ..
+// of the panel, columns colb ..):
+// p = 2^(y log2 e + (tile maximum - lse) log2 e) with the hardware exp2 (its
+// argument is <= 0), dZ = c (onehot - p) (+ e p (z - mu) with the entropy
+// bonus); rows at or past nvalid give 0, and with MASKCOL columns at or past V.
+// Two rows at a time: the row pairs of a row and the column pairs of the
+// transposed piece are each one packed conversion.
+template <bool BONUS, bool MASKCOL>
+__device__ __forceinline__ void dz_piece(const uint4 (&cur)[8], int rb, int colb, int V,
+                                         const float* rL, const float* rC, const float* rE,
+                                         const float* rD, const int* rY, int nvalid,
+                                         uint16_t* zrow, uint16_t* zcol) {
+  uint32_t tcol[8][4];  // column q of the piece: its 8 rows as bf16 pairs
+#pragma unroll
+  for (int r = 0; r < 8; r += 2) {
+    float d[2][8];
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr) {
+      const int rl = rb * 8 + r + rr;
+      const float Lk = rL[rl], Ck = rC[rl];
+      const float Ek = BONUS ? rE[rl] : 0.f, Dk = BONUS ? rD[rl] : 0.f;
+      const int Yk = rY[rl];
+      const bool rv = rl < nvalid;
+      const uint32_t w[4] = {cur[r + rr].x, cur[r + rr].y, cur[r + rr].z, cur[r + rr].w};
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int col = colb + q;
+        const uint16_t hb = (uint16_t)(w[q >> 1] >> ((q & 1) * 16));
+        const float yv = (float)__builtin_bit_cast(_Float16, hb);
+        const float p = __builtin_amdgcn_exp2f(fmaf(yv, kLog2e, Lk));
+        float v = BONUS ? dlogit(Ck, Ek, -Dk, p, yv, col == Yk)
+                        : Ck * ((col == Yk ? 1.f : 0.f) - p);
+        if (MASKCOL) v = col < V ? v : 0.f;
+        d[rr][q] = rv ? v : 0.f;
+      }
+    }
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr)
+      *(uint4*)(zrow + (r + rr) * 64) =
+          make_uint4(pk_bf16(d[rr][0], d[rr][1]), pk_bf16(d[rr][2], d[rr][3]),
+                     pk_bf16(d[rr][4], d[rr][5]), pk_bf16(d[rr][6], d[rr][7]));
+#pragma unroll
+    for (int q = 0; q < 8; ++q) tcol[q][r >> 1] = pk_bf16(d[0][q], d[1][q]);
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q)
+    *(uint4*)(zcol + (q << 6)) = make_uint4(tcol[q][0], tcol[q][1], tcol[q][2], tcol[q][3]);
+}
+
 template <bool BONUS>
 __global__ void __launch_bounds__(kDzbT, BONUS ? 2 : 3) k_dz_from_y_blk(
     uint16_t* __restrict__ yz, int64_t Vpad, int64_t Tc, int64_t V,
     const int32_t* __restrict__ rows, const int32_t* __restrict__ ids,
     const int32_t* __restrict__ meta, int64_t c0, const float* __restrict__ pm,
     const float* __restrict__ lse, const float* __restrict__ grad, const float* __restrict__ ce,
-    const float* __restrict__ cmu, int ntc, uint16_t* __restrict__ dzt) {
+    const float* __restrict__ cmu, uint16_t* __restrict__ dzt) {
   __shared__ float rL[256], rC[256], rE[256], rD[256];
   __shared__ int rY[256];
   const int tid = threadIdx.x;
-  const int nt = (int)(blockIdx.x % ntc), pn = (int)(blockIdx.x / ntc);
+  constexpr int NB = 4;                  // blocks of 64 columns per workgroup
+  const int ng = (int)(Vpad / 64) / NB;  // workgroups per panel
+  const int g = (int)(blockIdx.x % ng), pn = (int)(blockIdx.x / ng);
+  const int kb0 = g * NB;                // first block of the panel
+  const int nt = kb0 >> 2;               // its 256-column vocabulary tile
   int64_t count = (int64_t)meta[0] - c0;
   count = count < 0 ? 0 : (count > Tc ? Tc : count);
   const int64_t r0 = (int64_t)pn * 256;
   if (r0 >= count) return;
   const int cb = tid & 7, rb = tid >> 3;
-  uint16_t* const blk = yz + (((int64_t)pn * (Vpad >> 6) + (int64_t)nt * 4) << 14) + rb * 512 + cb * 8;
+  uint16_t* const blk = yz + (((int64_t)pn * (Vpad >> 6) + kb0) << 14) + rb * 512 + cb * 8;
   uint4 cur[8], nxt[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) cur[r] = *(const uint4*)(blk + r * 64);
@@ -124,49 +187,23 @@ __global__ void __launch_bounds__(kDzbT, BONUS ? 2 : 3) k_dz_from_y_blk(
   }
   __syncthreads();
   uint16_t* const tb = dzt + (((int64_t)nt * (Tc >> 6) + (r0 >> 6) + (rb >> 3)) << 14) + ((rb & 7) << 3);
+  const bool colfull = (int64_t)(nt + 1) * 256 <= V;  // every column of the tile is < V
+  const int nvalid = (int)(count - r0 < 256 ? count - r0 : 256);
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    if (kb < 3) {
+  for (int i = 0; i < NB; ++i) {
+    if (i + 1 < NB) {
 #pragma unroll
-      for (int r = 0; r < 8; ++r) nxt[r] = *(const uint4*)(blk + (kb + 1) * 16384 + r * 64);
+      for (int r = 0; r < 8; ++r) nxt[r] = *(const uint4*)(blk + (i + 1) * 16384 + r * 64);
     }
-    uint32_t tcol[8][4];  // column q of the piece: its 8 rows as bf16 pairs
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int rl = rb * 8 + r;
-      const float Lk = rL[rl], Ck = rC[rl];
-      const float Ek = BONUS ? rE[rl] : 0.f, Dk = BONUS ? rD[rl] : 0.f;
-      const int Yk = rY[rl];
-      const bool rv = r0 + rl < count;
-      const uint32_t w[4] = {cur[r].x, cur[r].y, cur[r].z, cur[r].w};
-      uint32_t o[4];
-#pragma unroll
-      for (int q2 = 0; q2 < 4; ++q2) {
-        uint32_t pair = 0;
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int q = 2 * q2 + hh;
-          const int64_t col = (int64_t)nt * 256 + kb * 64 + cb * 8 + q;
-          const uint16_t hb = (uint16_t)(w[q2] >> (hh * 16));
-          const float yv = (float)__builtin_bit_cast(_Float16, hb);
-          const float p = exp2f(fmaf(yv, kLog2e, Lk));
-          float d = BONUS ? dlogit(Ck, Ek, -Dk, p, yv, col == (int64_t)Yk)
-                          : Ck * ((col == (int64_t)Yk ? 1.f : 0.f) - p);
-          d = (rv && col < V) ? d : 0.f;
-          const uint32_t b = bf16_bits(d);
-          pair |= b << (hh * 16);
-          if (r & 1) tcol[q][r >> 1] |= b << 16;
-          else tcol[q][r >> 1] = b;
-        }
-        o[q2] = pair;
-      }
-      *(uint4*)(blk + kb * 16384 + r * 64) = make_uint4(o[0], o[1], o[2], o[3]);
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q)
-      *(uint4*)(tb + ((kb * 64 + cb * 8 + q) << 6)) =
-          make_uint4(tcol[q][0], tcol[q][1], tcol[q][2], tcol[q][3]);
-    if (kb < 3) {
+    const int kb = (kb0 & 3) + i;  // block within the vocabulary tile
+    uint16_t* const zrow = blk + i * 16384;
+    uint16_t* const zcol = tb + ((kb * 64 + cb * 8) << 6);
+    const int colb = nt * 256 + kb * 64 + cb * 8;
+    if (colfull)
+      dz_piece<BONUS, false>(cur, rb, colb, (int)V, rL, rC, rE, rD, rY, nvalid, zrow, zcol);
+    else
+      dz_piece<BONUS, true>(cur, rb, colb, (int)V, rL, rC, rE, rD, rY, nvalid, zrow, zcol);
+    if (i + 1 < NB) {
 #pragma unroll
       for (int r = 0; r < 8; ++r) cur[r] = nxt[r];
     }
@@ -263,14 +300,13 @@ hipError_t launch_dz_from_y_blk(uint16_t* yz, int64_t Vpad, int64_t Tc, int64_t 
                                 const int32_t* rows, const int32_t* ids, const int32_t* meta,
                                 int64_t c0, const float* pm, const float* lse, const float* grad,
                                 const float* ce, const float* cmu, uint16_t* dzt, hipStream_t s) {
-  const int ntc = (int)(Vpad / 256);
-  const int64_t nb = (Tc / 256) * ntc;
+  const int64_t nb = (Tc / 256) * (Vpad / 256);
   if (nb > 0 && ce)
     k_dz_from_y_blk<true><<<(unsigned)nb, kDzbT, 0, s>>>(yz, Vpad, Tc, V, rows, ids, meta, c0, pm,
-                                                         lse, grad, ce, cmu, ntc, dzt);
+                                                         lse, grad, ce, cmu, dzt);
   else if (nb > 0)
     k_dz_from_y_blk<false><<<(unsigned)nb, kDzbT, 0, s>>>(yz, Vpad, Tc, V, rows, ids, meta, c0,
-                                                          pm, lse, grad, ce, cmu, ntc, dzt);
+                                                          pm, lse, grad, ce, cmu, dzt);
   return hipGetLastError();
 }
 
