@@ -26,8 +26,9 @@
 //              tile, online log-sum-exp partials (max, sum exp, sum exp*z) and
 //              the logit of the sampled token.  Logits are never stored.
 //   EPI_STATS_Y  EPI_STATS, and also z minus the row's maximum over the
-//              tile, rounded to fp16, row-major [rows, Vpad] (the backward
-//              then forms dZ from it instead of recomputing z).
+//              tile, rounded to fp16, each 256 x 256 tile column-major in the
+//              128 KiB that the tile-blocked [rows, Vpad] layout gives it (the
+//              backward then forms dZ from it instead of recomputing z).
 //   EPI_DZ     backward recompute: dZ = c (onehot(y) - p) + e p (z - mu) in bf16,
 //              written tile-blocked [rows, Vpad] (the dH operand) and
 //              transposed, [Vpad, ldzt] (the dW operand, K-contiguous).
@@ -45,9 +46,10 @@ constexpr int STAGE = A_BYTES + B_BYTES;  // 64 KiB
 constexpr int ROWP = BM * 20;             // per-row epilogue parameters (five words)
 // dZ epilogue: one 256x256 bf16 tile staged in LDS, rows padded to 528 bytes
 // (conflict-free 2- and 8-byte writes, contiguous 16-byte reads); the
-// transposed tile uses rows of 544 bytes (a lane's 8-byte write of four
-// consecutive K: the 16 columns of a lane group 8 banks apart, the 4 K groups
-// 2 banks apart, so a wave's 64 writes cover every bank twice)
+// transposed tile (dZ^T, and the forward's y, staged column by column) uses
+// rows of 544 bytes (a lane's 8-byte write of four consecutive rows of one
+// column: the 16 columns of a lane group 8 banks apart, the 4 row groups 2
+// banks apart, so a wave's 64 writes cover every bank twice)
 constexpr int STG_PITCH = 528;
 constexpr int STG_PITCH_T = 544;
 constexpr int STG_BYTES = 256 * STG_PITCH_T;
@@ -88,8 +90,9 @@ struct Args {
   const float* ent;    //   and entropies, read only with egrad
   float* pm; float* ps; float* pu; int64_t ldp; float* zy;  // EPI_STATS: partials at p_off + m,
   int64_t p_off;                                            //   zy at rows_off + m
-  uint16_t* y; int64_t ldy;                                 // EPI_STATS_Y: fp16 z - tile max,
-                                                            //   tile-blocked, Kp = ldy
+  uint16_t* y; int64_t ldy;                                 // EPI_STATS_Y: fp16 z - tile max, the
+                                                            //   tiles of a blocked [rows, ldy]
+                                                            //   buffer, each column-major
   uint16_t* dz; int64_t ldz; int64_t Vvalid;                  // EPI_DZ, tile-blocked (Kp = ldz)
   uint16_t* dzt; int64_t ldzt;                                //   and dZ^T [Vpad, ldzt] blocked (nullptr = none)
   float* C; int64_t ldc; int accumulate; int c_scatter;  // EPI_STORE
@@ -220,6 +223,21 @@ __device__ __forceinline__ void stage_copy_out_blk(const char* st, uint16_t* dst
   }
 }
 
+// Copy a 256 x 256 tile of 16-bit values staged column by column (column c
+// at c * PITCH bytes) to dst as 256 columns of 512 contiguous bytes (the
+// tile column-major, 128 contiguous KiB): 32 lanes take one column, with
+// non-temporal stores (the forward's y is read back only after the whole
+// forward of the chunk).
+template <int PITCH>
+__device__ __forceinline__ void stage_copy_out_cm(const char* st, uint16_t* dst, int tid) {
+#pragma unroll 4
+  for (int it = 0; it < 16; ++it) {
+    const int c = it * NT + tid, col = c >> 5, ch = c & 31;
+    const uint4 v = *(const uint4*)(st + col * PITCH + ch * 16);
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), (u32x4*)(dst + col * 256 + ch * 8));
+  }
+}
+
 // Write four 16-bit values (rows r..r+3 of one column, packed in v) into the
 // row-major staging tile.
 __device__ __forceinline__ void stage_col4(char* q0, uint2 v) {
@@ -229,8 +247,12 @@ __device__ __forceinline__ void stage_col4(char* q0, uint2 v) {
   *(uint16_t*)(q0 + 3 * STG_PITCH) = (uint16_t)(v.y >> 16);
 }
 
-__device__ __forceinline__ uint32_t f16_bits(float f) {
-  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
+// Two fp32 values to a packed fp16 pair (a in the low half), rounded to
+// nearest even (one v_cvt_pk_f16_f32).
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pk_f16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, f16x2_t));
 }
 
 template <int EPI>
@@ -412,16 +434,29 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
       }
       row16_max_n(mx);
       // logit of the sampled token, picked with selects outside the store's
-      // branch (a dynamic index there makes the compiler copy the tiles)
+      // branch (a dynamic index there makes the compiler copy the tiles); a
+      // row's token lies in a given 128-column half tile with probability
+      // 128 / V, so the wave skips the picking unless one of its rows has it
+      {
+        int yl[16];
+        bool here = false;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int rl = wm * 64 + (e >> 2) * 16 + q4 * 4 + (e & 3);
-        const int yl = rp_i[rl] - (n0 + wn * 128);
-        const int jj = yl >> 4;
-        float z = acc4[e >> 2][0][e & 3];
+        for (int e = 0; e < 16; ++e) {
+          const int rl = wm * 64 + (e >> 2) * 16 + q4 * 4 + (e & 3);
+          yl[e] = rp_i[rl] - (n0 + wn * 128);
+          here = here || (unsigned)yl[e] < 128u;
+        }
+        if (__builtin_amdgcn_ballot_w64(here)) {
 #pragma unroll
-        for (int j = 1; j < 8; ++j) z = jj == j ? acc4[e >> 2][j][e & 3] : z;
-        if (yl >= 0 && yl < 128 && (yl & 15) == r16) g.zy[g.rows_off + m0 + rl] = z;
+          for (int e = 0; e < 16; ++e) {
+            const int rl = wm * 64 + (e >> 2) * 16 + q4 * 4 + (e & 3);
+            const int jj = yl[e] >> 4;
+            float z = acc4[e >> 2][0][e & 3];
+#pragma unroll
+            for (int j = 1; j < 8; ++j) z = jj == j ? acc4[e >> 2][j][e & 3] : z;
+            if ((unsigned)yl[e] < 128u && (yl[e] & 15) == r16) g.zy[g.rows_off + m0 + rl] = z;
+          }
+        }
       }
       // lane r16 of group q4 owns row e = r16 of that group
       const int rl = wm * 64 + (r16 >> 2) * 16 + q4 * 4 + (r16 & 3);
@@ -445,23 +480,22 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
           for (int q = 0; q < 4; ++q) mr[q] = fmaxf(mx[i * 4 + q], xmax[(1 - wn) * 256 + rl0 + q]);
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
-            uint32_t hb[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) hb[q] = f16_bits(acc4[i][j][q] - mr[q]);
-            hv[i][j].x = hb[0] | (hb[1] << 16);
-            hv[i][j].y = hb[2] | (hb[3] << 16);
+            hv[i][j].x = pk_f16(acc4[i][j][0] - mr[0], acc4[i][j][1] - mr[1]);
+            hv[i][j].y = pk_f16(acc4[i][j][2] - mr[2], acc4[i][j][3] - mr[3]);
           }
         }
+        // staged column by column: a lane's four rows of a column in one
+        // 8-byte write
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int j = 0; j < 8; ++j)
-            stage_col4(lds + (wm * 64 + i * 16 + q4 * 4) * STG_PITCH + (wn * 128 + j * 16 + r16) * 2,
-                       hv[i][j]);
+            *(uint2*)(lds + (wn * 128 + j * 16 + r16) * STG_PITCH_T + (wm * 64 + i * 16 + q4 * 4) * 2) =
+                hv[i][j];
         __syncthreads();
-        // y is tile-blocked (panel m0 of Kp = ldy columns; the tile's blocks
-        // start at column n0)
-        stage_copy_out_blk<STG_PITCH>(lds, g.y + (int64_t)m0 * g.ldy + (int64_t)n0 * BM, tid);
+        // y: the tile's 128 KiB of the tile-blocked [Tc, Vpad] buffer (panel
+        // m0, from block n0 / 64), holding the tile column-major
+        stage_copy_out_cm<STG_PITCH_T>(lds, g.y + (int64_t)m0 * g.ldy + (int64_t)n0 * BM, tid);
       }
       if (full) {
 #pragma unroll
@@ -635,8 +669,9 @@ hipError_t mfma_fwd_stats(const uint16_t* Hc, int64_t d, const uint16_t* W, int6
 // Forward of one chunk of compacted rows [c0, c0 + Tc) for the fused step:
 // Hc and W tile-blocked with Kp = d rounded up to 64 (c0 and Tc multiples of
 // 256); partials [ntiles][Tc] indexed by the chunk row, zy by the compacted
-// row, and y = z - (row maximum over the tile) in fp16 into y, tile-blocked
-// [Tc, Vpad].
+// row, and y = z - (row maximum over the tile) in fp16 into y [Tc, Vpad]:
+// each 256 x 256 tile in the 128 KiB the tile-blocked layout gives it,
+// column-major.
 hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V,
                             int64_t Vpad, const int32_t* rows, const int32_t* ids,
                             const int32_t* cnt, int64_t c0, int64_t Tc, float* pm, float* ps,

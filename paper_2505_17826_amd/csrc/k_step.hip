@@ -65,12 +65,16 @@ __global__ void __launch_bounds__(256) k_step_rows(
 }
 
 // Tile-blocked variant (the layout the step's backward GEMMs read, blk_index):
-// y, and dZ in its place, are [Tc, Vpad] blocked; dZ^T is [Vpad, Tc] blocked.
-// One 256-thread workgroup per (256-row panel, 256-column vocabulary tile):
-// the tile's four 256 x 64 blocks, 128 contiguous KiB of y.  Thread tid owns
-// the 8 x 8 piece (rows rb * 8 .., columns cb * 8 ..) of each block; the next
-// block's eight row pieces are in flight while a block is converted (168
-// registers without the entropy bonus: three workgroups per CU).  The
+// dZ is [Tc, Vpad] blocked, in the place of y, whose 256 x 256 tiles the
+// forward stored column-major in the same 128 KiB (the forward then stages
+// a tile in LDS with one 8-byte write per four rows of a column); dZ^T is
+// [Vpad, Tc] blocked.  One 256-thread workgroup per (256-row panel,
+// 256-column vocabulary tile).  Thread tid owns the 8 x 8 piece (rows
+// rb * 8 .., columns cb * 8 ..) of each 256 x 64 block: y's block i is the
+// same 32 KiB as dZ's block i, read as eight 16-byte column pieces; the next
+// block's pieces are in flight while a block is converted, and every thread
+// has read a block before any thread writes dZ over it (168 registers
+// without the entropy bonus: three workgroups per CU).  The
 // conversion has no branches (the hardware exp2 and packed bf16 conversion,
 // 32-bit indices, column masks only in the last vocabulary tile); the pass
 // is bound by HBM (5.3 TB/s on its 153 GB at the 7B shape).  dZ goes back in place, and
@@ -90,9 +94,9 @@ __device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
-// dZ of one thread's 8 x 8 piece of a block (zrow: its first row in the block;
-// zcol: its first row of the transposed piece in the dZ^T block; rows rb * 8 ..
-// of the panel, columns colb ..):
+// dZ of one thread's 8 x 8 piece of a block (cur[q]: the piece's column q,
+// rows rb * 8 .. rb * 8 + 7 of y; zrow: its first row in the dZ block; zcol:
+// its first row of the transposed piece in the dZ^T block; columns colb ..):
 // p = 2^(y log2 e + (tile maximum - lse) log2 e) with the hardware exp2 (its
 // argument is <= 0), dZ = c (onehot - p) (+ e p (z - mu) with the entropy
 // bonus); rows at or past nvalid give 0, and with MASKCOL columns at or past V.
@@ -114,11 +118,12 @@ __device__ __forceinline__ void dz_piece(const uint4 (&cur)[8], int rb, int colb
       const float Ek = BONUS ? rE[rl] : 0.f, Dk = BONUS ? rD[rl] : 0.f;
       const int Yk = rY[rl];
       const bool rv = rl < nvalid;
-      const uint32_t w[4] = {cur[r + rr].x, cur[r + rr].y, cur[r + rr].z, cur[r + rr].w};
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const int col = colb + q;
-        const uint16_t hb = (uint16_t)(w[q >> 1] >> ((q & 1) * 16));
+        const int rp = r + rr;  // row of the piece: half rp & 1 of word rp >> 1 of column q
+        const uint32_t w = rp < 2 ? cur[q].x : rp < 4 ? cur[q].y : rp < 6 ? cur[q].z : cur[q].w;
+        const uint16_t hb = (uint16_t)(w >> ((rp & 1) * 16));
         const float yv = (float)__builtin_bit_cast(_Float16, hb);
         const float p = __builtin_amdgcn_exp2f(fmaf(yv, kLog2e, Lk));
         float v = BONUS ? dlogit(Ck, Ek, -Dk, p, yv, col == Yk)
@@ -160,10 +165,12 @@ __global__ void __launch_bounds__(kDzbT, BONUS ? 2 : 3) k_dz_from_y_blk(
   const int64_t r0 = (int64_t)pn * 256;
   if (r0 >= count) return;
   const int cb = tid & 7, rb = tid >> 3;
-  uint16_t* const blk = yz + (((int64_t)pn * (Vpad >> 6) + kb0) << 14) + rb * 512 + cb * 8;
+  uint16_t* const tile = yz + (((int64_t)pn * (Vpad >> 6) + kb0) << 14);
+  uint16_t* const blk = tile + rb * 512 + cb * 8;         // dZ: row rb * 8 of the block, column cb * 8
+  const uint16_t* const ycol = tile + cb * 8 * 256 + rb * 8;  // y: column cb * 8, row rb * 8
   uint4 cur[8], nxt[8];
 #pragma unroll
-  for (int r = 0; r < 8; ++r) cur[r] = *(const uint4*)(blk + r * 64);
+  for (int q = 0; q < 8; ++q) cur[q] = *(const uint4*)(ycol + q * 256);
   {
     const int64_t r = r0 + tid;
     float L_ = 0.f, C_ = 0.f, M_ = 0.f, E_ = 0.f, D_ = 0.f;
@@ -191,10 +198,24 @@ __global__ void __launch_bounds__(kDzbT, BONUS ? 2 : 3) k_dz_from_y_blk(
   const int nvalid = (int)(count - r0 < 256 ? count - r0 : 256);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
+    // the next block's loads come after the previous block's stores, so that
+    // the count of outstanding accesses below covers exactly those loads
+    asm volatile("" ::: "memory");
     if (i + 1 < NB) {
 #pragma unroll
-      for (int r = 0; r < 8; ++r) nxt[r] = *(const uint4*)(blk + (i + 1) * 16384 + r * 64);
+      for (int q = 0; q < 8; ++q) nxt[q] = *(const uint4*)(ycol + (i + 1) * 16384 + q * 256);
     }
+    // every thread has its piece of block i (its loads before the eight just
+    // issued are complete) before any thread writes dZ over the block; the
+    // empty asm statements keep the compiler from moving memory accesses
+    // across the wait and the barrier
+    asm volatile("" ::: "memory");
+    if (i + 1 < NB)
+      __builtin_amdgcn_s_waitcnt(0x0F78);  // vmcnt(8)
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
     const int kb = (kb0 & 3) + i;  // block within the vocabulary tile
     uint16_t* const zrow = blk + i * 16384;
     uint16_t* const zcol = tb + ((kb * 64 + cb * 8) << 6);
