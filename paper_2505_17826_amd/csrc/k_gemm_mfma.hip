@@ -124,10 +124,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int64
 // (l%8) ^ (((p*8 + l/8) >> 1) & 7) = (l%8) ^ (l/16) ^ 4*(p&1); the two
 // parities of p take the offsets vA[0|1], vB[0|1].  Chunks at or past K are
 // read from outside the descriptor (0).
-// Loader waves per epilogue: four for the forward GEMMs, two for the fp32-store
-// GEMMs (dH, dW on blocked operands: 1-1.7% faster than four, one or eight
-// slower).
-template <int EPI> constexpr int kNLoad = EPI == EPI_STORE ? 2 : 4;
+// Loader waves per epilogue: two for the GEMMs on tile-blocked operands (dH
+// and dW: 1-1.7% faster than four; the fused step's forward: 3% faster than
+// four, one 15% slower), four for the forward on row-major operands.
+template <int EPI> constexpr int kNLoad = (EPI == EPI_STORE || EPI == EPI_STATS_Y) ? 2 : 4;
 struct LoadGeom {
   uint32_t vA[2], vB[2];  // per-lane byte offsets for even / odd p (k0 = 0)
   int kc[2];              // logical chunk * 8 (first element) for even / odd p
