@@ -512,7 +512,21 @@ __global__ void __launch_bounds__(256) k_merge_rows(
     return;
   }
   float m = -INFINITY, sm = 0.f, u = 0.f;
-  for (int j = 0; j < ntiles; ++j) {
+  // eight tiles' partials loaded ahead, merged in tile order
+  int j = 0;
+  for (; j + 8 <= ntiles; j += 8) {
+    float a[8], b[8], c[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int64_t o = (int64_t)(j + q) * ld + k;
+      a[q] = pm[o];
+      b[q] = ps[o];
+      c[q] = pu[o];
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) lse_merge(m, sm, u, a[q], b[q], c[q]);
+  }
+  for (; j < ntiles; ++j) {
     int64_t o = (int64_t)j * ld + k;
     lse_merge(m, sm, u, pm[o], ps[o], pu[o]);
   }

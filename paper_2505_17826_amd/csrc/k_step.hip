@@ -37,7 +37,21 @@ __global__ void __launch_bounds__(256) k_step_rows(
   if (kl >= Tc || k >= (int64_t)meta[0]) return;
   const int t = rows[k];
   float m = -INFINITY, sm = 0.f, u = 0.f;
-  for (int j = 0; j < ntiles; ++j) {
+  // eight tiles' partials loaded ahead, merged in tile order
+  int j = 0;
+  for (; j + 8 <= ntiles; j += 8) {
+    float a[8], b[8], c[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int64_t o = (int64_t)(j + q) * Tc + kl;
+      a[q] = pm[o];
+      b[q] = ps[o];
+      c[q] = pu[o];
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) lse_merge(m, sm, u, a[q], b[q], c[q]);
+  }
+  for (; j < ntiles; ++j) {
     const int64_t o = (int64_t)j * Tc + kl;
     lse_merge(m, sm, u, pm[o], ps[o], pu[o]);
   }
