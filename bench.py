@@ -39,12 +39,12 @@ WORKLOADS = {"tiny": 0, "1.5b": 1, "7b": 2, "longcot": 3, "lossonly": 4}
 TRAFFIC = {
     # forward GEMM alone (k_gemm<EPI_STATS>, one launch over all valid rows)
     "7b": {"sources": {'k_gemm_mfma.hip': 'cf4dd9c3b173d995', 'rft_internal.h': '608db1a569cef60d'},
-           "bytes": 140489575.1 * 1024 * 2.0 + 1174404.3 * 1024 * 1.0},
+           "bytes": 144945797.0 * 1024 * 2.0 + 1174409.3 * 1024 * 1.0},
     # every kernel of one rft_ppo_clip_step call (26 dispatches, two row chunks)
-    "step_7b": {"sources": {'k_gemm_mfma.hip': 'cf4dd9c3b173d995', 'k_step.hip': '354a3fcb28388265', 'k_simt.hip': '79fa372b0122fc73', 'k_adv_loss.hip': '572ab23ae603a178', 'k_tokens.hip': 'd52b04cf394f6696', 'rft_internal.h': '608db1a569cef60d', 'rft_abi.hip': 'fe8c4e32bc03c808'},
-                "bytes": 491892286.9 * 1024 * 2.0 + 163544249.0 * 1024 * 1.0},
+    "step_7b": {"sources": {'k_gemm_mfma.hip': 'cf4dd9c3b173d995', 'k_step.hip': '39fcacd3c55e6f75', 'k_simt.hip': '79fa372b0122fc73', 'k_adv_loss.hip': 'fe9e2b4d1d0b6332', 'k_tokens.hip': 'd52b04cf394f6696', 'rft_internal.h': '608db1a569cef60d', 'rft_abi.hip': 'fe8c4e32bc03c808'},
+                "bytes": 496730382.7 * 1024 * 2.0 + 163521939.5 * 1024 * 1.0},
     "lossonly": {"sources": {'k_logits.hip': '784099cf37962bf5', 'rft_internal.h': '608db1a569cef60d'},
-                 "bytes": 8758808.2 * 1024 * 2.0 + 19477895.9 * 1024 * 1.0},
+                 "bytes": 8758808.5 * 1024 * 2.0 + 19477472.1 * 1024 * 1.0},
 }
 
 
