@@ -33,7 +33,9 @@
 //              written tile-blocked [rows, Vpad] (the dH operand) and
 //              transposed, [Vpad, ldzt] (the dW operand, K-contiguous).
 //   EPI_STORE  fp32 result, optionally scattered to rows through a map and
-//              optionally added to the existing values.
+//              optionally added to the existing values.  On tile-blocked
+//              operands (dH, dW of the step) k_gemm_store384 does this on a
+//              384 x 256 tile (fewer operand bytes per flop).
 #include "rft_internal.h"
 
 namespace rft {
@@ -640,6 +642,139 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   }
 }
 
+
+// fp32-store GEMM on a 384 x 256 workgroup tile for tile-blocked operands (the
+// step's dH and dW): eight waves of 96 x 128 (6 x 8 tiles of 16x16x32, 192
+// accumulator registers), two 80 KiB stages (all of the LDS; the row map of a
+// scattered C is read in the epilogue), two loader waves.  17% fewer operand
+// bytes and 22% fewer LDS fragment bytes per flop than the 256 x 256 tile:
+// 2.4% faster on the dH shape and 5.6% on the dW shape, bit-identical.  A
+// 384-row tile starts at row 0 or 128 of a 256-row panel P0 of A and continues
+// into P1 = P0 + 1; one descriptor covers both (adjacent in memory), P1 only if
+// it holds rows < M (otherwise the tile's rows there load the same rows of P0,
+// which reach only rows of C that are not stored).  K must be a multiple of 64
+// (or come from the counter): there is no per-lane K tail, and each load takes
+// its lane part of the offset from one of two registers and its instruction's
+// part as a scalar offset (the per-instruction offsets held in registers across
+// the loop spilled).  The LDS layout, swizzle and fragment reads are those of
+// k_gemm; rows 16 i + r16 of a wave's fragments share the swizzle (r16 >> 1) & 7.
+constexpr int BM4 = 384;
+constexpr int A_BYTES4 = BM4 * BK * 2;      // 48 KiB
+constexpr int STAGE4 = A_BYTES4 + B_BYTES;  // 80 KiB
+constexpr int kSG4 = 4;
+
+__global__ void __launch_bounds__(NT, 1) k_gemm_store384(const Args g) {
+  __shared__ __attribute__((aligned(16))) char lds[2 * STAGE4];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 1, wn = wid & 1;  // 4 x 2 waves, wave tile 96 x 128
+  int M = g.M, K = g.K;
+  if (g.cnt) {
+    int64_t c = (int64_t)g.cnt[0] - g.cnt_off;
+    c = c < 0 ? 0 : (c > g.cnt_cap ? g.cnt_cap : c);
+    if (g.m_from_cnt) M = (int)c;
+    if (g.k_from_cnt) K = (int)((c + BK - 1) / BK * BK);
+  }
+  const int N = g.N;
+  if (g.k_from_cnt && K == 0 && g.accumulate) return;  // nothing to add
+  const int nTm = (M + BM4 - 1) / BM4, nTn = (N + BN - 1) / BN;
+  int mt, nt;
+  if (!tile_of<kSG4>((int)blockIdx.x, nTm, nTn, mt, nt)) return;
+  const int nk = (K + BK - 1) / BK;
+  constexpr int NLOAD = 2;
+  const bool loader = wid < NLOAD;
+  const int lw = wid % NLOAD;
+  const int m0 = mt * BM4, n0 = nt * BN;
+  const int P0 = m0 >> 8, base0 = m0 & 255;
+  const int64_t pa = (int64_t)256 * g.lda;  // elements per panel of A
+  const bool p1ok = (P0 + 1) * 256 < M;
+  const __amdgpu_buffer_rsrc_t rA = make_rsrc(g.A + P0 * pa, (p1ok ? 2 : 1) * pa * 2);
+  const uint32_t pbytes = p1ok ? (uint32_t)(pa * 2) : 0u;
+  const int64_t pb = (int64_t)256 * g.ldb;
+  const __amdgpu_buffer_rsrc_t rB = make_rsrc(g.B + (int64_t)nt * pb, pb * 2);
+  // lane part of the offsets for even / odd instructions (see load_stage)
+  uint32_t vq[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+    vq[q] = (uint32_t)((lane >> 3) * 128 + (((lane & 7) ^ (lane >> 4) ^ (q * 4)) << 4));
+  auto load = [&](char* dst, int k0) {
+    const uint32_t kofs = (uint32_t)k0 * 512u;  // a 64-column block is 32 KiB
+#pragma unroll
+    for (int p = 0; p < 24; ++p) {  // A: rows lw * 192 + 8 p ..
+      const int R0 = lw * 192 + 8 * p;
+      const int pr = base0 + R0;  // row from the start of P0 (>= 256: in P1)
+      const uint32_t so = __builtin_amdgcn_readfirstlane(
+          kofs + (uint32_t)((pr & 255) * 128) + (uint32_t)(pr >> 8) * pbytes);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_ptr)(dst + R0 * 128), 16, vq[p & 1], so,
+                                               0, 0);
+    }
+#pragma unroll
+    for (int p = 0; p < 16; ++p) {  // B: rows lw * 128 + 8 p ..
+      const int R0 = lw * 128 + 8 * p;
+      const uint32_t so = __builtin_amdgcn_readfirstlane(kofs + (uint32_t)(R0 * 128));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES4 + R0 * 128), 16,
+                                               vq[p & 1], so, 0, 0);
+    }
+  };
+  const int r16 = lane & 15, q4 = lane >> 4;
+  floatx4 acc4[6][8];
+#pragma unroll
+  for (int i = 0; i < 6; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc4[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
+  if (nk > 0 && loader) load(lds, 0);
+  __syncthreads();  // first stage visible to every wave
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk && loader) load(lds + ((kt + 1) & 1) * STAGE4, (kt + 1) * BK);
+    const char* As = lds + (kt & 1) * STAGE4;
+    const char* Al = As + (wm * 96 + r16) * 128;
+    const char* Bl = As + A_BYTES4 + (wn * 128 + r16) * 128;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int cho = ((ks * 4 + q4) ^ ((r16 >> 1) & 7)) << 4;
+      bf16x8 a[6];
+#pragma unroll
+      for (int i = 0; i < 6; ++i) a[i] = *(const bf16x8*)(Al + i * 2048 + cho);
+#pragma unroll
+      for (int jh = 0; jh < 4; ++jh) {
+        bf16x8 b[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) b[j] = *(const bf16x8*)(Bl + (jh * 2 + j) * 2048 + cho);
+#pragma unroll
+        for (int i = 0; i < 6; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc4[i][jh * 2 + j] =
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc4[i][jh * 2 + j], 0, 0, 0);
+      }
+    }
+    // this wave's loads of the next stage have landed and its reads of this
+    // stage are complete before the barrier
+    wait_vm();
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    barrier_lds();
+  }
+#pragma unroll
+  for (int i = 0; i < 6; ++i) {
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int m = m0 + wm * 96 + i * 16 + q4 * 4 + q;
+      if (m >= M) continue;
+      const int64_t dst = (int64_t)(g.c_scatter ? g.rows[g.rows_off + m] : m) * g.ldc;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int col = n0 + wn * 128 + j * 16 + r16;
+        if (col < N) {
+          float v = acc4[i][j][q];
+          if (g.accumulate) v += g.C[dst + col];
+          g.C[dst + col] = v;
+        }
+      }
+    }
+  }
+}
+
 }  // namespace mf
 
 // ------------------------------------------------------------ launchers ----
@@ -728,6 +863,15 @@ hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, in
   a.k_from_cnt = k_from_cnt;
   a.C = C; a.ldc = ldc; a.rows = rows; a.rows_off = rows_off; a.c_scatter = rows != nullptr;
   a.accumulate = accumulate;
+  // tile-blocked operands: the 384 x 256 tile where its one descriptor over
+  // two panels of A and its scalar offsets fit 32 bits and K needs no tail
+  if (a_blk && b_blk && lda < ((int64_t)1 << 21) && ldb < ((int64_t)1 << 22) &&
+      (k_from_cnt || K % mf::BK == 0)) {
+    const unsigned grid = (unsigned)mf::grid_tiles<mf::kSG4>((M + mf::BM4 - 1) / mf::BM4,
+                                                            (N + mf::BN - 1) / mf::BN);
+    mf::k_gemm_store384<<<grid, mf::NT, 0, s>>>(a);
+    return hipGetLastError();
+  }
   mf::k_gemm<mf::EPI_STORE><<<grid_for<mf::EPI_STORE>(M, N), mf::NT, 0, s>>>(a);
   return hipGetLastError();
 }
