@@ -34,7 +34,7 @@
 //              transposed, [Vpad, ldzt] (the dW operand, K-contiguous).
 //   EPI_STORE  fp32 result, optionally scattered to rows through a map and
 //              optionally added to the existing values.  On tile-blocked
-//              operands (dH, dW of the step) k_gemm_store384 does this on a
+//              operands (dH, dW of the step) k_gemm384 does this on a
 //              384 x 256 tile (fewer operand bytes per flop).
 #include "rft_internal.h"
 
@@ -643,27 +643,35 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 }
 
 
-// fp32-store GEMM on a 384 x 256 workgroup tile for tile-blocked operands (the
-// step's dH and dW): eight waves of 96 x 128 (6 x 8 tiles of 16x16x32, 192
-// accumulator registers), two 80 KiB stages (all of the LDS; the row map of a
-// scattered C is read in the epilogue), two loader waves.  17% fewer operand
-// bytes and 22% fewer LDS fragment bytes per flop than the 256 x 256 tile:
-// 2.4% faster on the dH shape and 5.6% on the dW shape, bit-identical.  A
-// 384-row tile starts at row 0 or 128 of a 256-row panel P0 of A and continues
-// into P1 = P0 + 1; one descriptor covers both (adjacent in memory), P1 only if
-// it holds rows < M (otherwise the tile's rows there load the same rows of P0,
-// which reach only rows of C that are not stored).  K must be a multiple of 64
-// (or come from the counter): there is no per-lane K tail, and each load takes
-// its lane part of the offset from one of two registers and its instruction's
-// part as a scalar offset (the per-instruction offsets held in registers across
-// the loop spilled).  The LDS layout, swizzle and fragment reads are those of
-// k_gemm; rows 16 i + r16 of a wave's fragments share the swizzle (r16 >> 1) & 7.
+// The GEMM on a 384 x 256 workgroup tile for tile-blocked operands: the
+// fp32 store of the step's dH and dW (EPI_STORE) and the fused step's forward
+// (EPI_STATS_Y).  Eight waves of 96 x 128 (6 x 8 tiles of 16x16x32, 192
+// accumulator registers), two 80 KiB stages (all of the LDS), two loader
+// waves.  17% fewer operand bytes and 22% fewer LDS fragment bytes per flop
+// than the 256 x 256 tile; the per-element k order is the same, so the results
+// are bit-identical to k_gemm's.  A 384-row tile starts at row 0 or 128 of a
+// 256-row panel P0 of A and continues into P1 = P0 + 1; one descriptor covers
+// both (adjacent in memory), P1 only if it holds rows < M (otherwise the tile's
+// rows there load the same rows of P0, which reach only rows of C that are not
+// stored).  K must be a multiple of 64 (or come from the counter): there is no
+// per-lane K tail, and each load takes its lane part of the offset from one of
+// two registers and its instruction's part as a scalar offset (the
+// per-instruction offsets held in registers across the loop spilled).  The LDS
+// layout, swizzle and fragment reads are those of k_gemm; rows 16 i + r16 of a
+// wave's fragments share the swizzle (r16 >> 1) & 7.
 constexpr int BM4 = 384;
 constexpr int A_BYTES4 = BM4 * BK * 2;      // 48 KiB
 constexpr int STAGE4 = A_BYTES4 + B_BYTES;  // 80 KiB
-constexpr int kSG4 = 4;
+template <int EPI> constexpr int kSG4 = EPI == EPI_STORE ? 4 : 8;
+// forward epilogue's LDS after the main loop: the y staging tile, the two
+// column halves' row maxima [2][384], the wn = 1 half's partials [384][3] and
+// the rows' token ids [384]
+constexpr int X4_MAX = STG_BYTES, X4_PART = X4_MAX + 2 * BM4 * 4, X4_IDS = X4_PART + 3 * BM4 * 4;
+static_assert(X4_IDS + BM4 * 4 <= 2 * STAGE4, "forward epilogue exceeds the LDS");
 
-__global__ void __launch_bounds__(NT, 1) k_gemm_store384(const Args g) {
+template <int EPI>
+__global__ void __launch_bounds__(NT, 1) k_gemm384(const Args g) {
+  static_assert(EPI == EPI_STORE || EPI == EPI_STATS_Y, "384-row tile: store or forward");
   __shared__ __attribute__((aligned(16))) char lds[2 * STAGE4];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -676,10 +684,10 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_store384(const Args g) {
     if (g.k_from_cnt) K = (int)((c + BK - 1) / BK * BK);
   }
   const int N = g.N;
-  if (g.k_from_cnt && K == 0 && g.accumulate) return;  // nothing to add
+  if (EPI == EPI_STORE && g.k_from_cnt && K == 0 && g.accumulate) return;  // nothing to add
   const int nTm = (M + BM4 - 1) / BM4, nTn = (N + BN - 1) / BN;
   int mt, nt;
-  if (!tile_of<kSG4>((int)blockIdx.x, nTm, nTn, mt, nt)) return;
+  if (!tile_of<kSG4<EPI>>((int)blockIdx.x, nTm, nTn, mt, nt)) return;
   const int nk = (K + BK - 1) / BK;
   constexpr int NLOAD = 2;
   const bool loader = wid < NLOAD;
@@ -692,6 +700,10 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_store384(const Args g) {
   const uint32_t pbytes = p1ok ? (uint32_t)(pa * 2) : 0u;
   const int64_t pb = (int64_t)256 * g.ldb;
   const __amdgpu_buffer_rsrc_t rB = make_rsrc(g.B + (int64_t)nt * pb, pb * 2);
+  // forward: the sampled token of each row (threads 0..383, -1 past M), held
+  // in a register through the main loop (the stages fill the LDS)
+  int tok = -1;
+  if (EPI == EPI_STATS_Y && tid < BM4 && m0 + tid < M) tok = g.ids[g.rows[g.rows_off + m0 + tid]];
   // lane part of the offsets for even / odd instructions (see load_stage)
   uint32_t vq[2];
 #pragma unroll
@@ -754,22 +766,221 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_store384(const Args g) {
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
     barrier_lds();
   }
+  // element q of tile (i, j) is row wm*96 + i*16 + q4*4 + q and column
+  // wn*128 + j*16 + r16 of the workgroup tile
+  if constexpr (EPI == EPI_STORE) {
 #pragma unroll
-  for (int i = 0; i < 6; ++i) {
-    __builtin_amdgcn_sched_barrier(0);
+    for (int i = 0; i < 6; ++i) {
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int m = m0 + wm * 96 + i * 16 + q4 * 4 + q;
-      if (m >= M) continue;
-      const int64_t dst = (int64_t)(g.c_scatter ? g.rows[g.rows_off + m] : m) * g.ldc;
+      for (int q = 0; q < 4; ++q) {
+        const int m = m0 + wm * 96 + i * 16 + q4 * 4 + q;
+        if (m >= M) continue;
+        const int64_t dst = (int64_t)(g.c_scatter ? g.rows[g.rows_off + m] : m) * g.ldc;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int col = n0 + wn * 128 + j * 16 + r16;
-        if (col < N) {
-          float v = acc4[i][j][q];
-          if (g.accumulate) v += g.C[dst + col];
-          g.C[dst + col] = v;
+        for (int j = 0; j < 8; ++j) {
+          const int col = n0 + wn * 128 + j * 16 + r16;
+          if (col < N) {
+            float v = acc4[i][j][q];
+            if (g.accumulate) v += g.C[dst + col];
+            g.C[dst + col] = v;
+          }
         }
+      }
+    }
+  } else {
+    // Forward: k_gemm's EPI_STATS_Y arithmetic per row and 256-column tile
+    // (the same maxima, exponent sums in the same order, the same merge of
+    // the two column halves), on 24 rows per lane: row e (0..23) of lane
+    // group q4 is tile row wm*96 + (e/4)*16 + q4*4 + e%4.  After the
+    // reductions lane r16 owns rows e = r16 and, for r16 < 8, e = 16 + r16.
+    // The last k-step's barrier has passed: the stages are free.
+    float* const xmax = (float*)(lds + X4_MAX);
+    float* const xm = (float*)(lds + X4_PART);
+    int32_t* const rp_i = (int32_t*)(lds + X4_IDS);
+    auto rl_of = [&](int e) { return wm * 96 + (e >> 2) * 16 + q4 * 4 + (e & 3); };
+    if (tid < BM4) rp_i[tid] = tok;
+    const int colb16 = n0 + wn * 128 + r16;
+    bool cv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) cv[j] = colb16 + j * 16 < N;
+    const bool full = n0 + BN <= N;
+    __builtin_amdgcn_sched_barrier(0);
+    float mx[24];
+    if (full) {
+#pragma unroll
+      for (int e = 0; e < 24; ++e) {
+        const floatx4* t = acc4[e >> 2];
+        const int q = e & 3;
+        mx[e] = fmaxf(fmaxf(fmaxf(t[0][q], t[1][q]), fmaxf(t[2][q], t[3][q])),
+                      fmaxf(fmaxf(t[4][q], t[5][q]), fmaxf(t[6][q], t[7][q])));
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 24; ++e) {
+        float v = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v = cv[j] ? fmaxf(v, acc4[e >> 2][j][e & 3]) : v;
+        mx[e] = v;
+      }
+    }
+    row16_max_n(mx);
+    {
+      float h0 = mx[0], h1 = mx[16];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) h0 = r16 == e ? mx[e] : h0;
+#pragma unroll
+      for (int e = 17; e < 24; ++e) h1 = r16 == e - 16 ? mx[e] : h1;
+      xmax[wn * BM4 + rl_of(r16)] = h0;
+      if (r16 < 8) xmax[wn * BM4 + rl_of(16 + r16)] = h1;
+    }
+    __syncthreads();  // token ids and half maxima visible
+    // logit of the sampled token (as in k_gemm: selects, and only in waves
+    // where one of the rows has its token in this half tile)
+    {
+      const int nw = n0 + wn * 128;
+      bool here = false;
+#pragma unroll
+      for (int e = 0; e < 24; ++e) here |= (unsigned)(rp_i[rl_of(e)] - nw) < 128u;
+      if (__builtin_amdgcn_ballot_w64(here)) {
+        // branch-free stores: a lane whose column is not the row's token
+        // stores past the end of a descriptor over the tile's 384 entries of
+        // zy, which the hardware drops
+        const __amdgpu_buffer_rsrc_t rZ = make_rsrc(g.zy + g.rows_off + m0, (int64_t)BM4 * 4);
+#pragma unroll
+        for (int e = 0; e < 24; ++e) {
+          const int yl = rp_i[rl_of(e)] - nw;
+          const int jj = yl >> 4;
+          float z = acc4[e >> 2][0][e & 3];
+#pragma unroll
+          for (int j = 1; j < 8; ++j) z = jj == j ? acc4[e >> 2][j][e & 3] : z;
+          const bool mine = (unsigned)yl < 128u && (yl & 15) == r16;
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z), rZ,
+                                                mine ? (uint32_t)rl_of(e) * 4u : 0x80000000u, 0, 0);
+        }
+      }
+    }
+    // y = z - (row maximum over the tile) in fp16, staged column by column and
+    // copied out once per 256-row panel that the tile touches: panel P0 gets
+    // tile rows [0, 256 - base0) at its rows [base0, 256), panel P1 (only if it
+    // holds rows < M) tile rows [256 - base0, 384) at its rows [0, base0 + 128).
+    // Each panel's 256 x 256 tile is column-major in the 128 KiB that the
+    // tile-blocked [rows, Vpad] layout gives it; the two row halves of a panel
+    // that two 384-row tiles share are disjoint 256-byte pieces of every column.
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      if (p == 1 && !p1ok) break;
+      const int tlo = p == 0 ? 0 : 256 - base0;
+      const int thi = p == 0 ? 256 - base0 : BM4;
+#pragma unroll
+      for (int i = 0; i < 6; ++i) {
+        const int gr = wm * 96 + i * 16;  // a 16-row group lies in one panel
+        if (gr < tlo || gr >= thi) continue;
+        const int pr = (base0 + gr + q4 * 4) & 255;  // panel row of the lane's first row
+        float mr[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) mr[q] = fmaxf(mx[i * 4 + q], xmax[(1 - wn) * BM4 + gr + q4 * 4 + q]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          uint2 hv;
+          hv.x = pk_f16(acc4[i][j][0] - mr[0], acc4[i][j][1] - mr[1]);
+          hv.y = pk_f16(acc4[i][j][2] - mr[2], acc4[i][j][3] - mr[3]);
+          *(uint2*)(lds + (wn * 128 + j * 16 + r16) * STG_PITCH_T + pr * 2) = hv;
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's staging writes done
+      barrier_lds();
+      const int plo = p == 0 ? base0 : 0;
+      const int sh = (p == 0 ? 256 - base0 : base0 + 128) == 256 ? 5 : 4;  // log2 chunks per column
+      uint16_t* const dst = g.y + (int64_t)(P0 + p) * 256 * g.ldy + (int64_t)n0 * 256 + plo;
+      const char* const src = lds + plo * 2;
+      for (int c = tid; c < (256 << sh); c += NT) {
+        const int col = c >> sh, ch = c & ((1 << sh) - 1);
+        const uint4 v = *(const uint4*)(src + col * STG_PITCH_T + ch * 16);
+        __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v),
+                                    (u32x4*)(dst + col * 256 + ch * 8));
+      }
+      // every staged value is read (its store issued) before the next panel's
+      // staging overwrites it
+      barrier_lds();
+    }
+    // exponent sums in two batches of 12 rows (registers), each reduced and
+    // picked into the lane's own rows before the next
+    float om0 = mx[0], os0 = 0.f, ou0 = 0.f, om1 = mx[16], os1 = 0.f, ou1 = 0.f;
+#pragma unroll
+    for (int e = 1; e < 16; ++e) om0 = r16 == e ? mx[e] : om0;
+#pragma unroll
+    for (int e = 17; e < 24; ++e) om1 = r16 == e - 16 ? mx[e] : om1;
+#pragma unroll
+    for (int bt = 0; bt < 2; ++bt) {
+      float sm[12], um[12];
+#pragma unroll
+      for (int k = 0; k < 12; ++k) {
+        const int e = bt * 12 + k;
+        float s0 = 0.f, u0 = 0.f;
+        if (full) {
+          const float mk = mx[e] * kLog2e;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float z = acc4[e >> 2][j][e & 3];
+            const float pe = __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mk));
+            s0 += pe;
+            u0 = fmaf(pe, z, u0);
+          }
+        } else {
+          const float mk = mx[e] == -INFINITY ? 0.f : mx[e] * kLog2e;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float z = acc4[e >> 2][j][e & 3];
+            const float pe = cv[j] ? __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mk)) : 0.f;
+            s0 += pe;
+            u0 = cv[j] ? fmaf(pe, z, u0) : u0;
+          }
+        }
+        sm[k] = s0;
+        um[k] = u0;
+      }
+      row16_sum_n(sm);
+      row16_sum_n(um);
+#pragma unroll
+      for (int k = 0; k < 12; ++k) {
+        const int e = bt * 12 + k;
+        if (e < 16) {
+          os0 = r16 == e ? sm[k] : os0;
+          ou0 = r16 == e ? um[k] : ou0;
+        } else {
+          os1 = r16 == e - 16 ? sm[k] : os1;
+          ou1 = r16 == e - 16 ? um[k] : ou1;
+        }
+      }
+    }
+    const int rl0 = rl_of(r16), rl1 = rl_of(16 + r16);  // rl1: lanes r16 < 8
+    if (wn == 1) {
+      xm[rl0 * 3 + 0] = om0;
+      xm[rl0 * 3 + 1] = os0;
+      xm[rl0 * 3 + 2] = ou0;
+      if (r16 < 8) {
+        xm[rl1 * 3 + 0] = om1;
+        xm[rl1 * 3 + 1] = os1;
+        xm[rl1 * 3 + 2] = ou1;
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    barrier_lds();  // no wait for the y stores still in flight
+    if (wn == 0) {
+      if (m0 + rl0 < M) {
+        lse_merge(om0, os0, ou0, xm[rl0 * 3 + 0], xm[rl0 * 3 + 1], xm[rl0 * 3 + 2]);
+        const int64_t o = (int64_t)nt * g.ldp + g.p_off + m0 + rl0;
+        g.pm[o] = om0;
+        g.ps[o] = os0;
+        g.pu[o] = ou0;
+      }
+      if (r16 < 8 && m0 + rl1 < M) {
+        lse_merge(om1, os1, ou1, xm[rl1 * 3 + 0], xm[rl1 * 3 + 1], xm[rl1 * 3 + 2]);
+        const int64_t o = (int64_t)nt * g.ldp + g.p_off + m0 + rl1;
+        g.pm[o] = om1;
+        g.ps[o] = os1;
+        g.pu[o] = ou1;
       }
     }
   }
@@ -782,6 +993,16 @@ template <int EPI>
 static unsigned grid_for(int64_t M_cap, int64_t N) {
   return (unsigned)mf::grid_tiles<mf::kSG<EPI>>((M_cap + mf::BM - 1) / mf::BM,
                                                 (N + mf::BN - 1) / mf::BN);
+}
+template <int EPI>
+static unsigned grid_for384(int64_t M_cap, int64_t N) {
+  return (unsigned)mf::grid_tiles<mf::kSG4<EPI>>((M_cap + mf::BM4 - 1) / mf::BM4,
+                                                 (N + mf::BN - 1) / mf::BN);
+}
+// The 384-row tile takes tile-blocked operands whose two-panel descriptor and
+// scalar offsets fit 32 bits and whose K needs no tail.
+static bool fits384(int64_t lda, int64_t ldb, int64_t K, int k_from_cnt) {
+  return lda < ((int64_t)1 << 21) && ldb < ((int64_t)1 << 22) && (k_from_cnt || K % mf::BK == 0);
 }
 
 // Forward of the policy head over the compacted hidden rows Hc [rows_off, rows_off + cap):
@@ -820,6 +1041,10 @@ hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, in
   a.rows = rows; a.rows_off = c0; a.ids = ids;
   a.pm = pm; a.ps = ps; a.pu = pu; a.ldp = Tc; a.zy = zy; a.p_off = 0;
   a.y = y; a.ldy = Vpad;
+  if (fits384(Kp, Kp, d, 0)) {
+    mf::k_gemm384<mf::EPI_STATS_Y><<<grid_for384<mf::EPI_STATS_Y>(Tc, V), mf::NT, 0, s>>>(a);
+    return hipGetLastError();
+  }
   mf::k_gemm<mf::EPI_STATS_Y><<<grid_for<mf::EPI_STATS_Y>(Tc, V), mf::NT, 0, s>>>(a);
   return hipGetLastError();
 }
@@ -865,11 +1090,8 @@ hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, in
   a.accumulate = accumulate;
   // tile-blocked operands: the 384 x 256 tile where its one descriptor over
   // two panels of A and its scalar offsets fit 32 bits and K needs no tail
-  if (a_blk && b_blk && lda < ((int64_t)1 << 21) && ldb < ((int64_t)1 << 22) &&
-      (k_from_cnt || K % mf::BK == 0)) {
-    const unsigned grid = (unsigned)mf::grid_tiles<mf::kSG4>((M + mf::BM4 - 1) / mf::BM4,
-                                                            (N + mf::BN - 1) / mf::BN);
-    mf::k_gemm_store384<<<grid, mf::NT, 0, s>>>(a);
+  if (a_blk && b_blk && fits384(lda, ldb, K, k_from_cnt)) {
+    mf::k_gemm384<mf::EPI_STORE><<<grid_for384<mf::EPI_STORE>(M, N), mf::NT, 0, s>>>(a);
     return hipGetLastError();
   }
   mf::k_gemm<mf::EPI_STORE><<<grid_for<mf::EPI_STORE>(M, N), mf::NT, 0, s>>>(a);

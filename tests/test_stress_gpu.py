@@ -186,27 +186,39 @@ def _ws_for_chunk(tok, d, V, rows):
     return hi
 
 
-def test_midsize_fused_step_full_tile_order():
-    """Row chunks of 16384 rows (64 M-tiles: the forward's full super-group of
-    8 x 8 tiles per XCD, and 64 M-tiles of d_hidden), V = 8292 (33 M-tiles of
-    the weight gradient: a full super-group of 4 x 8 and a remainder), d = 72
-    (a ragged K tail in the forward, one ragged N-tile in the backward); about
-    40k valid rows in three chunks, the last ragged.  Whole dH and dW against
+MIDSIZE_CASES = [
+    # d = 72: the forward on 256 x 256 tiles (a K tail), chunks of 16384 rows
+    # (64 M-tiles: the full super-group of 8 x 8 tiles per XCD)
+    ("d72", dict(d=72, n_prompts=5, chunk=16384)),
+    # d = 128: the forward on 384 x 256 tiles, chunks of 24576 rows (64 M-tiles
+    # of 384: its full super-group), 384-row tiles that start half way into a
+    # 256-row panel and chunk ends inside a tile
+    ("d128", dict(d=128, n_prompts=7, chunk=24576)),
+]
+
+
+@pytest.mark.parametrize("name,case", MIDSIZE_CASES, ids=[c[0] for c in MIDSIZE_CASES])
+def test_midsize_fused_step_full_tile_order(name, case):
+    """Row chunks that fill the forward's full super-group of tiles, V = 8292
+    (33 M-tiles of the 256-row weight gradient kernel, 22 of the 384-row one:
+    full super-groups of 4 x 8 and a remainder); three chunks, the last
+    ragged; the backward GEMMs on 384 x 256 tiles.  Whole dH and dW against
     the oracle."""
-    over = dict(n_prompts=5, group=8, len_lo=900, len_hi=1100, pad_to=1100, d=72, V=8292,
-                dtype="bf16")
-    b = _batch(2, "midsize", over)
+    d, V, rows = case["d"], 8292, case["chunk"]
+    over = dict(n_prompts=case["n_prompts"], group=8, len_lo=900, len_hi=1100, pad_to=1100, d=d,
+                V=V, dtype="bf16")
+    b = _batch(2, "midsize" if d == 72 else "midsize" + name, over)
     tok = tokens_of(b)
     N = int(b.mask.sum())
-    ws = _ws_for_chunk(tok, 72, 8292, 16384)
-    Tc = R.chunk_rows(R.RFT_OP_PPO_STEP, tok, 72, 8292, R.RFT_BF16, ws)
-    print(f"[stress midsize] N={N} T={b.T} chunk={Tc} chunks={-(-N // Tc)}", flush=True)
-    assert Tc == 16384 and N > 2 * Tc and N % Tc != 0     # three chunks, the last ragged
+    ws = _ws_for_chunk(tok, d, V, rows)
+    Tc = R.chunk_rows(R.RFT_OP_PPO_STEP, tok, d, V, R.RFT_BF16, ws)
+    print(f"[stress midsize {name}] N={N} T={b.T} chunk={Tc} chunks={-(-N // Tc)}", flush=True)
+    assert Tc == rows and N > 2 * Tc and N % Tc != 0     # three chunks, the last ragged
     lp, _, _ = O.token_logprobs(b.H, b.W, b.ids, b.mask)
     old, ref = perturbed_logprobs(lp, b)
     gf = gpu_fused_step(b, old, ref, ws_bytes=ws)
-    print("[stress midsize] oracle step", flush=True)
+    print(f"[stress midsize {name}] oracle step", flush=True)
     o = oracle_step(b, old, ref)
     compare_step(gf, o, b)
-    print(f"[stress midsize] dH rel {rel_fro(gf['dH'], o['dH']):.2e} dW rel "
+    print(f"[stress midsize {name}] dH rel {rel_fro(gf['dH'], o['dH']):.2e} dW rel "
           f"{rel_fro(gf['dW'], o['dW']):.2e}", flush=True)
