@@ -485,7 +485,8 @@ def main():
         fms = fwd_kernel_ms()
         fw = 2.0 * N * cfg.d * V / 1e12
         out["roofline_fwd_kernel"] = {
-            "kernel": "k_gemm<EPI_STATS> via rft_token_logprobs (timed after the benchmark)",
+            "kernel": ("k_gemm384<EPI_STATS> on tile-blocked copies (recommended workspace) via "
+                       "rft_token_logprobs: the whole call, timed after the benchmark"),
             "bound": bound, "achieved": fw / (fms / 1e3), "peak": peak, "unit": "TFLOP/s",
             "frac": fw / (fms / 1e3) / peak, "ms_per_launch": fms,
             "traffic": traffic_gb(args.workload), "traffic_unit": "GB per launch"}

@@ -169,7 +169,8 @@ const char* rft_last_error(void);
  * as in the call; dtype of hidden/weight).  For RFT_OP_PPO_BWD and
  * RFT_OP_PPO_STEP the value is the recommended size; any size >=
  * rft_workspace_min_bytes() works, a larger workspace processes more rows per
- * chunk.  Returns 0 for invalid
+ * chunk.  For RFT_OP_TOKEN_LOGPROBS the value may include tile-blocked operand
+ * copies (see rft_token_logprobs); the minimum is the size without them.  Returns 0 for invalid
  * arguments. */
 size_t rft_workspace_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
 size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, int dtype);
@@ -232,6 +233,11 @@ rft_status rft_group_advantages_ids(const float* rewards, const int32_t* group_i
  * hidden [T, d] and weight [V, d] in `dtype` (bf16: MFMA tiles with fp32
  * accumulation; f32: fp32 arithmetic).  The logits are formed tile by tile
  * and folded into an online log-sum-exp; the T x V logits are never stored.
+ * Workspace: rft_workspace_bytes(RFT_OP_TOKEN_LOGPROBS, ...) is the
+ * recommended size; for bf16 with d % 64 == 0 it includes tile-blocked copies
+ * of the valid hidden rows and of weight (about Vpad d 2 bytes more, Vpad = V
+ * rounded up to 256), with which the GEMM runs on larger tiles.  Any size >=
+ * rft_workspace_min_bytes() works and gives the same results bit for bit.
  * Outputs (f32, [T]): logp (NaN for a valid row whose id is out of range),
  * entropy (may be NULL), lse.  Masked rows are 0.  hidden and the outputs may
  * be NULL when T == 0.

@@ -644,8 +644,9 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
 
 
 // The GEMM on a 384 x 256 workgroup tile for tile-blocked operands: the
-// fp32 store of the step's dH and dW (EPI_STORE) and the fused step's forward
-// (EPI_STATS_Y).  Eight waves of 96 x 128 (6 x 8 tiles of 16x16x32, 192
+// fp32 store of the step's dH and dW (EPI_STORE), the fused step's forward
+// (EPI_STATS_Y) and the forward of rft_token_logprobs given the workspace for
+// blocked operands (EPI_STATS).  Eight waves of 96 x 128 (6 x 8 tiles of 16x16x32, 192
 // accumulator registers), two 80 KiB stages (all of the LDS), two loader
 // waves.  17% fewer operand bytes and 22% fewer LDS fragment bytes per flop
 // than the 256 x 256 tile; the per-element k order is the same, so the results
@@ -663,6 +664,7 @@ constexpr int BM4 = 384;
 constexpr int A_BYTES4 = BM4 * BK * 2;      // 48 KiB
 constexpr int STAGE4 = A_BYTES4 + B_BYTES;  // 80 KiB
 template <int EPI> constexpr int kSG4 = EPI == EPI_STORE ? 4 : 8;
+template <int EPI> constexpr int kNLoad4 = 2;
 // forward epilogue's LDS after the main loop: the y staging tile, the two
 // column halves' row maxima [2][384], the wn = 1 half's partials [384][3] and
 // the rows' token ids [384]
@@ -671,7 +673,9 @@ static_assert(X4_IDS + BM4 * 4 <= 2 * STAGE4, "forward epilogue exceeds the LDS"
 
 template <int EPI>
 __global__ void __launch_bounds__(NT, 1) k_gemm384(const Args g) {
-  static_assert(EPI == EPI_STORE || EPI == EPI_STATS_Y, "384-row tile: store or forward");
+  static_assert(EPI == EPI_STORE || EPI == EPI_STATS || EPI == EPI_STATS_Y,
+                "384-row tile: store or forward");
+  constexpr bool kStats = EPI != EPI_STORE;
   __shared__ __attribute__((aligned(16))) char lds[2 * STAGE4];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -689,7 +693,9 @@ __global__ void __launch_bounds__(NT, 1) k_gemm384(const Args g) {
   int mt, nt;
   if (!tile_of<kSG4<EPI>>((int)blockIdx.x, nTm, nTn, mt, nt)) return;
   const int nk = (K + BK - 1) / BK;
-  constexpr int NLOAD = 2;
+  constexpr int NLOAD = kNLoad4<EPI>;
+  constexpr int RA = BM4 / NLOAD, RB = BN / NLOAD;  // rows of A and of B per loader wave
+  static_assert(RA % 16 == 0 && RB % 16 == 0, "offset parity follows the row-pair swizzle");
   const bool loader = wid < NLOAD;
   const int lw = wid % NLOAD;
   const int m0 = mt * BM4, n0 = nt * BN;
@@ -703,7 +709,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm384(const Args g) {
   // forward: the sampled token of each row (threads 0..383, -1 past M), held
   // in a register through the main loop (the stages fill the LDS)
   int tok = -1;
-  if (EPI == EPI_STATS_Y && tid < BM4 && m0 + tid < M) tok = g.ids[g.rows[g.rows_off + m0 + tid]];
+  if (kStats && tid < BM4 && m0 + tid < M) tok = g.ids[g.rows[g.rows_off + m0 + tid]];
   // lane part of the offsets for even / odd instructions (see load_stage)
   uint32_t vq[2];
 #pragma unroll
@@ -712,8 +718,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm384(const Args g) {
   auto load = [&](char* dst, int k0) {
     const uint32_t kofs = (uint32_t)k0 * 512u;  // a 64-column block is 32 KiB
 #pragma unroll
-    for (int p = 0; p < 24; ++p) {  // A: rows lw * 192 + 8 p ..
-      const int R0 = lw * 192 + 8 * p;
+    for (int p = 0; p < RA / 8; ++p) {  // A: rows lw * RA + 8 p ..
+      const int R0 = lw * RA + 8 * p;
       const int pr = base0 + R0;  // row from the start of P0 (>= 256: in P1)
       const uint32_t so = __builtin_amdgcn_readfirstlane(
           kofs + (uint32_t)((pr & 255) * 128) + (uint32_t)(pr >> 8) * pbytes);
@@ -721,8 +727,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm384(const Args g) {
                                                0, 0);
     }
 #pragma unroll
-    for (int p = 0; p < 16; ++p) {  // B: rows lw * 128 + 8 p ..
-      const int R0 = lw * 128 + 8 * p;
+    for (int p = 0; p < RB / 8; ++p) {  // B: rows lw * RB + 8 p ..
+      const int R0 = lw * RB + 8 * p;
       const uint32_t so = __builtin_amdgcn_readfirstlane(kofs + (uint32_t)(R0 * 128));
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_ptr)(dst + A_BYTES4 + R0 * 128), 16,
                                                vq[p & 1], so, 0, 0);
@@ -789,7 +795,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm384(const Args g) {
       }
     }
   } else {
-    // Forward: k_gemm's EPI_STATS_Y arithmetic per row and 256-column tile
+    // Forward: k_gemm's EPI_STATS(_Y) arithmetic per row and 256-column tile
     // (the same maxima, exponent sums in the same order, the same merge of
     // the two column halves), on 24 rows per lane: row e (0..23) of lane
     // group q4 is tile row wm*96 + (e/4)*16 + q4*4 + e%4.  After the
@@ -868,7 +874,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm384(const Args g) {
     // tile-blocked [rows, Vpad] layout gives it; the two row halves of a panel
     // that two 384-row tiles share are disjoint 256-byte pieces of every column.
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
+    for (int p = 0; p < (EPI == EPI_STATS_Y ? 2 : 0); ++p) {
       if (p == 1 && !p1ok) break;
       const int tlo = p == 0 ? 0 : 256 - base0;
       const int thi = p == 0 ? 256 - base0 : BM4;
@@ -1019,6 +1025,27 @@ hipError_t mfma_fwd_stats(const uint16_t* Hc, int64_t d, const uint16_t* W, int6
   a.rows = rows; a.rows_off = rows_off; a.ids = ids;
   a.pm = pm; a.ps = ps; a.pu = pu; a.ldp = ldp; a.zy = zy; a.p_off = rows_off;
   mf::k_gemm<mf::EPI_STATS><<<grid_for<mf::EPI_STATS>(cap, V), mf::NT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+// Whether the forward from tile-blocked copies takes this d.
+bool mfma_fwd_blk_ok(int64_t d) { return d % mf::BK == 0 && fits384(d, d, d, 0); }
+
+// The same forward from tile-blocked copies: Hb [round_up(cap, 256), Kp] of the
+// compacted rows and Wb [Vpad, Kp] (Kp = d, a multiple of 64, below 2^21).
+hipError_t mfma_fwd_stats_blk(const uint16_t* Hb, int64_t d, const uint16_t* Wb, int64_t V,
+                              const int32_t* rows, const int32_t* ids, const int32_t* cnt,
+                              int64_t cap, float* pm, float* ps, float* pu, int64_t ldp, float* zy,
+                              hipStream_t s) {
+  if (!fits384(d, d, d, 0)) return hipErrorInvalidValue;
+  mf::Args a = {};
+  a.A = Hb; a.lda = d; a.a_blk = 1;
+  a.B = Wb; a.ldb = d; a.b_blk = 1;
+  a.M = (int)cap; a.N = (int)V; a.K = (int)d;
+  a.cnt = cnt; a.cnt_off = 0; a.cnt_cap = cap; a.m_from_cnt = 1;
+  a.rows = rows; a.rows_off = 0; a.ids = ids;
+  a.pm = pm; a.ps = ps; a.pu = pu; a.ldp = ldp; a.zy = zy; a.p_off = 0;
+  mf::k_gemm384<mf::EPI_STATS><<<grid_for384<mf::EPI_STATS>(cap, V), mf::NT, 0, s>>>(a);
   return hipGetLastError();
 }
 

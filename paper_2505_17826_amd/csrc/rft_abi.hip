@@ -132,17 +132,25 @@ rft_status check_ws(const char* fn, void* ws, size_t have, size_t need) {
 // ---------------------------------------------------- workspace layouts --
 struct FwdWs {
   TokMeta m;
-  uint16_t* hc;  // compacted hidden rows (bf16 path)
+  uint16_t* hc;  // compacted hidden rows (bf16 path): row-major, or tile-blocked
+  uint16_t* wb;  // tile-blocked copy of W [Vpad, d] (blocked bf16 path only)
   float *pm, *ps, *pu, *zy;
   int ntiles;
   int64_t ldp;
   size_t bytes;
 };
-FwdWs carve_fwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dtype) {
+bool fwd_blocked_ok(int dtype, int64_t d) { return dtype == RFT_BF16 && mfma_fwd_blk_ok(d); }
+// blocked: the bf16 forward from tile-blocked copies of the compacted rows
+// [round_up(T, 256), d] and of W [Vpad, d] (d a multiple of 64), for the
+// 384 x 256 GEMM tile; the copy of W adds Vpad d 2 bytes.
+FwdWs carve_fwd(void* base, const rft_tokens& tok, int64_t d, int64_t V, int dtype,
+                bool blocked = false) {
   Carver c(base);
   FwdWs w;
   w.m = carve_tokmeta(c, tok.T, tok.n_seq);
-  w.hc = dtype == RFT_BF16 ? c.take<uint16_t>((size_t)(tok.T > 0 ? tok.T : 1) * d) : nullptr;
+  const int64_t hrows = blocked ? round_up(tok.T > 0 ? tok.T : 1, 256) : (tok.T > 0 ? tok.T : 1);
+  w.hc = dtype == RFT_BF16 ? c.take<uint16_t>((size_t)hrows * d) : nullptr;
+  w.wb = blocked ? c.take<uint16_t>((size_t)round_up(V, 256) * d) : nullptr;
   int tn = dtype == RFT_BF16 ? kMfmaTileN : kSimtTileN;
   w.ntiles = (int)((V + tn - 1) / tn);
   w.ldp = tok.T > 0 ? tok.T : 1;
@@ -396,7 +404,7 @@ size_t rft_workspace_bytes(int op, const rft_tokens* tok, int64_t d, int64_t V, 
   switch (op) {
     case RFT_OP_TOKEN_LOGPROBS:
       if (dtype != RFT_F32 && dtype != RFT_BF16) return 0;
-      return carve_fwd(nullptr, *tok, d, V, dtype).bytes;
+      return carve_fwd(nullptr, *tok, d, V, dtype, fwd_blocked_ok(dtype, d)).bytes;
     case RFT_OP_TOKEN_LOGPROBS_FROM_LOGITS:
     case RFT_OP_PPO_BWD_LOGITS:
       return 0;
@@ -433,6 +441,11 @@ size_t rft_workspace_min_bytes(int op, const rft_tokens* tok, int64_t d, int64_t
       return dtype == RFT_BF16 ? carve_step(nullptr, *tok, d, V, kBf16Align).bytes
                                : step_f32_bytes(*tok, d, V, bwd_align(dtype));
     return carve_bwd(nullptr, *tok, d, V, dtype, bwd_align(dtype)).bytes;
+  }
+  if (op == RFT_OP_TOKEN_LOGPROBS) {
+    if (!tok || tok->T < 0 || tok->n_seq < 0 || V < 1) return 0;
+    if (dtype != RFT_F32 && dtype != RFT_BF16) return 0;
+    return carve_fwd(nullptr, *tok, d, V, dtype).bytes;
   }
   return rft_workspace_bytes(op, tok, d, V, dtype);
 }
@@ -526,11 +539,22 @@ rft_status rft_token_logprobs(const rft_tokens* tok, const void* hidden, const v
   if (tok->T > 0 && (!logp || !lse)) return fail(RFT_E_NULL, "%s: logp / lse is NULL", fn);
   FwdWs w = carve_fwd(nullptr, *tok, d, V, dtype);
   if ((st = check_ws(fn, ws, ws_bytes, w.bytes))) return st;
-  w = carve_fwd(ws, *tok, d, V, dtype);
+  // a workspace that also holds the tile-blocked copies selects that path
+  const bool blocked = fwd_blocked_ok(dtype, d) &&
+                       ws_bytes >= carve_fwd(nullptr, *tok, d, V, dtype, true).bytes;
+  w = carve_fwd(ws, *tok, d, V, dtype, blocked);
   hipStream_t s = (hipStream_t)stream;
   if (tok->T == 0) return RFT_OK;
   RFT_HIP(launch_tokmeta(*tok, w.m, s), fn);
-  if (dtype == RFT_BF16) {
+  if (blocked) {
+    const uint16_t* W = (const uint16_t*)weight;
+    RFT_HIP(launch_rows_to_blk((const uint16_t*)hidden, d, w.m.rows, w.m.meta, tok->T, d, w.hc, s),
+            fn);
+    RFT_HIP(launch_rows_to_blk(W, d, nullptr, nullptr, V, d, w.wb, s), fn);
+    RFT_HIP(mfma_fwd_stats_blk(w.hc, d, w.wb, V, w.m.rows, tok->token_ids, w.m.meta, tok->T,
+                               w.pm, w.ps, w.pu, w.ldp, w.zy, s),
+            fn);
+  } else if (dtype == RFT_BF16) {
     RFT_HIP(launch_gather_rows16((const uint16_t*)hidden, d, w.m.rows, w.m.meta, tok->T, w.hc, s),
             fn);
     RFT_HIP(mfma_fwd_stats(w.hc, d, (const uint16_t*)weight, V, w.m.rows,

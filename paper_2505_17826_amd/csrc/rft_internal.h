@@ -290,6 +290,11 @@ hipError_t mfma_fwd_stats(const uint16_t* H, int64_t d, const uint16_t* W, int64
                           const int32_t* rows, const int32_t* ids, const int32_t* cnt,
                           int64_t rows_off, int64_t cap, float* pm, float* ps, float* pu,
                           int64_t ldp, float* zy, hipStream_t s);
+hipError_t mfma_fwd_stats_blk(const uint16_t* Hb, int64_t d, const uint16_t* Wb, int64_t V,
+                              const int32_t* rows, const int32_t* ids, const int32_t* cnt,
+                              int64_t cap, float* pm, float* ps, float* pu, int64_t ldp, float* zy,
+                              hipStream_t s);
+bool mfma_fwd_blk_ok(int64_t d);
 hipError_t mfma_fwd_stats_y(const uint16_t* Hc, int64_t d, const uint16_t* W, int64_t V,
                             int64_t Vpad, const int32_t* rows, const int32_t* ids,
                             const int32_t* cnt, int64_t c0, int64_t Tc, float* pm, float* ps,

@@ -60,6 +60,24 @@ def test_workspace_sizes_are_consistent():
     assert L.rft_workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, None, 256, 5000, R.RFT_BF16) == 0
 
 
+def test_forward_workspace_blocked_copies():
+    """rft_token_logprobs: for bf16 with d a multiple of 64 the recommended
+    workspace adds tile-blocked copies of the compacted rows (padded to 256) and
+    of W (Vpad x d); the minimum is the row-major path's; otherwise they agree."""
+    L = R.lib()
+    tk = _tok(T=1000, n_seq=8)
+    op = R.RFT_OP_TOKEN_LOGPROBS
+    for d, V in ((256, 5000), (128, 300)):
+        big = L.rft_workspace_bytes(op, ctypes.byref(tk), d, V, R.RFT_BF16)
+        small = L.rft_workspace_min_bytes(op, ctypes.byref(tk), d, V, R.RFT_BF16)
+        vpad = (V + 255) // 256 * 256
+        extra = (1024 - 1000) * d * 2 + vpad * d * 2
+        assert extra <= big - small <= extra + 2 * 256, (d, V, big - small)
+    for d, dt in ((72, R.RFT_BF16), (256, R.RFT_F32)):
+        assert (L.rft_workspace_bytes(op, ctypes.byref(tk), d, 5000, dt) ==
+                L.rft_workspace_min_bytes(op, ctypes.byref(tk), d, 5000, dt) > 0)
+
+
 def test_chunked_workspace_sizes():
     """The step / backward workspace: the recommended size holds every row in one
     chunk up to 131072 rows and stays flat beyond; the minimum (256-row chunk)

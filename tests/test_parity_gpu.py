@@ -240,6 +240,33 @@ def test_logits_paths(V, n_prompts):
 
 
 # --------------------------------------------------------------- edge cases --
+@pytest.mark.parametrize("d,V,n_prompts", [(128, 2048, 4), (192, 5003, 6), (64, 300, 1)])
+def test_token_logprobs_blocked_equals_row_major(d, V, n_prompts):
+    """rft_token_logprobs with the recommended workspace (tile-blocked copies,
+    384 x 256 GEMM tiles) and with the minimum workspace (row-major operands,
+    256 x 256 tiles): the same numbers bit for bit, and the oracle's."""
+    over = dict(n_prompts=n_prompts, group=8, len_lo=1, len_hi=200, pad_to=200, d=d, V=V,
+                dtype="bf16")
+    b = _batch(1, f"blk{d}-{V}", over)
+    print(f"[fwd blocked] d={d} V={V} T={b.T} N={int(b.mask.sum())}", flush=True)
+    tok = tokens_of(b)
+    H, W = b.H.to(DEV).contiguous(), b.W.to(DEV).contiguous()
+    big = R.workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, tok, d, V, R.RFT_BF16)
+    small = R.workspace_bytes(R.RFT_OP_TOKEN_LOGPROBS, tok, d, V, R.RFT_BF16, minimum=True)
+    assert big > small
+    outs = []
+    for nb in (big, small):
+        ws = torch.empty(nb, dtype=torch.uint8, device=DEV)
+        outs.append([cpu(x) for x in R.rft_token_logprobs(tok, H, W, ws=ws)])
+    torch.cuda.synchronize()
+    for a_, b_, k in zip(outs[0], outs[1], ("logp", "entropy", "lse")):
+        assert np.array_equal(a_, b_), (k, np.nanmax(np.abs(a_ - b_)))
+    m = b.mask.numpy() != 0
+    for got, want, k in zip(outs[0], O.token_logprobs(b.H, b.W, b.ids, b.mask),
+                            ("logp", "entropy", "lse")):
+        assert np.abs(got[m] - np.asarray(want)[m]).max() <= TOL_LOGP, k
+
+
 def test_all_masked_batch():
     cfg = synth.config(1, n_prompts=1, group=8, len_lo=0, len_hi=0, pad_to=16, d=64, V=300)
     b = synth.make_batch(cfg, "cpu", seed_key=(3,))
