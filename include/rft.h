@@ -19,6 +19,10 @@
  *    call only enqueues work on that stream and returns without a device
  *    synchronisation.  A return value other than RFT_OK means nothing was
  *    enqueued (except RFT_E_HIP, which reports a launch failure).
+ *  - Environment.  RFT_GEMM_STORE_TILE=256 or 384 fixes the workgroup tile
+ *    of the fp32-store GEMMs on tile-blocked operands (d_hidden, d_weight);
+ *    unset, each call picks the one that takes fewer rounds of tiles on the
+ *    device's compute units.  The results are the same bit for bit.
  *  - Errors.  Calls return an rft_status; rft_last_error() gives a
  *    thread-local text describing the last failure.  No call aborts or lets
  *    an exception cross the ABI.  Problems that only the device can see

@@ -36,6 +36,8 @@
 //              optionally added to the existing values.  On tile-blocked
 //              operands (dH, dW of the step) k_gemm384 does this on a
 //              384 x 256 tile (fewer operand bytes per flop).
+#include <cstdlib>
+
 #include "rft_internal.h"
 
 namespace rft {
@@ -98,7 +100,23 @@ struct Args {
   uint16_t* dz; int64_t ldz; int64_t Vvalid;                  // EPI_DZ, tile-blocked (Kp = ldz)
   uint16_t* dzt; int64_t ldzt;                                //   and dZ^T [Vpad, ldzt] blocked (nullptr = none)
   float* C; int64_t ldc; int accumulate; int c_scatter;  // EPI_STORE
+  int sel;            // EPI_STORE with both tile sizes launched: 1 = the 384-row kernel runs
+  int ncu;            //   only if prefer384(M, N, ncu), 2 = the 256-row kernel only if not
 };
+
+// fp32-store GEMM on tile-blocked operands: whether the 384 x 256 tile beats
+// the 256 x 256 one for an M x N result on ncu compute units.  Tiles run in
+// rounds of ncu (one workgroup per CU), so the time is about ceil(tiles / ncu)
+// tile times; a 384-row tile takes 1.43 times a 256-row one (1.5 times the
+// work at ~5% more flops per cycle, measured on the 7B shapes).  E.g. d_hidden
+// of 131072 rows and d = 3584: 19 rounds of 384 (27.2) against 28 of 256;
+// with d = 1536: 9 (12.9) against 12; 36901 rows, d = 3584: 6 (8.6) against 8.
+__host__ __device__ inline bool prefer384(int64_t M, int64_t N, int64_t ncu) {
+  const int64_t tn = (N + 255) / 256;
+  const int64_t r4 = ((M + 383) / 384 * tn + ncu - 1) / ncu;
+  const int64_t r2 = ((M + 255) / 256 * tn + ncu - 1) / ncu;
+  return r4 * 143 < r2 * 100;
+}
 
 // Raw buffer descriptor (wave-uniform) over `bytes` bytes from p.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int64_t bytes) {
@@ -275,6 +293,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(const Args g) {
   const int N = g.N;
   const int NB = g.NB > 0 ? g.NB : N;
   if (EPI == EPI_STORE && g.k_from_cnt && K == 0 && g.accumulate) return;  // nothing to add
+  if (EPI == EPI_STORE && g.sel == 2 && prefer384(M, N, g.ncu)) return;  // the 384-row kernel's
   const int nTm = (M + BM - 1) / BM, nTn = (N + BN - 1) / BN;
   // The grid is sized for the largest possible M; workgroups without a tile
   // for the device count exit at once.
@@ -689,6 +708,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm384(const Args g) {
   }
   const int N = g.N;
   if (EPI == EPI_STORE && g.k_from_cnt && K == 0 && g.accumulate) return;  // nothing to add
+  if (EPI == EPI_STORE && g.sel == 1 && !prefer384(M, N, g.ncu)) return;  // the 256-row kernel's
   const int nTm = (M + BM4 - 1) / BM4, nTn = (N + BN - 1) / BN;
   int mt, nt;
   if (!tile_of<kSG4<EPI>>((int)blockIdx.x, nTm, nTn, mt, nt)) return;
@@ -1005,6 +1025,32 @@ static unsigned grid_for384(int64_t M_cap, int64_t N) {
   return (unsigned)mf::grid_tiles<mf::kSG4<EPI>>((M_cap + mf::BM4 - 1) / mf::BM4,
                                                  (N + mf::BN - 1) / mf::BN);
 }
+// RFT_GEMM_STORE_TILE: 256 or 384 fixes the tile of the fp32-store GEMM on
+// tile-blocked operands, anything else (or unset) leaves it to prefer384.
+static int store_tile_env() {
+  const char* v = std::getenv("RFT_GEMM_STORE_TILE");
+  if (!v) return 0;
+  const int t = std::atoi(v);
+  return t == 256 || t == 384 ? t : 0;
+}
+
+// Compute units of the current device (cached per device).
+static hipError_t cu_count(int* n) {
+  static int cache[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64 && cache[dev] > 0) {
+    *n = cache[dev];
+    return hipSuccess;
+  }
+  e = hipDeviceGetAttribute(n, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  if (*n < 1) *n = 1;
+  if (dev >= 0 && dev < 64) cache[dev] = *n;
+  return hipSuccess;
+}
+
 // The 384-row tile takes tile-blocked operands whose two-panel descriptor and
 // scalar offsets fit 32 bits and whose K needs no tail.
 static bool fits384(int64_t lda, int64_t ldb, int64_t K, int k_from_cnt) {
@@ -1116,10 +1162,33 @@ hipError_t mfma_gemm_store(const uint16_t* A, int64_t lda, const uint16_t* B, in
   a.C = C; a.ldc = ldc; a.rows = rows; a.rows_off = rows_off; a.c_scatter = rows != nullptr;
   a.accumulate = accumulate;
   // tile-blocked operands: the 384 x 256 tile where its one descriptor over
-  // two panels of A and its scalar offsets fit 32 bits and K needs no tail
-  if (a_blk && b_blk && fits384(lda, ldb, K, k_from_cnt)) {
-    mf::k_gemm384<mf::EPI_STORE><<<grid_for384<mf::EPI_STORE>(M, N), mf::NT, 0, s>>>(a);
-    return hipGetLastError();
+  // two panels of A and its scalar offsets fit 32 bits, K needs no tail and
+  // it takes fewer rounds of tiles (prefer384).  With the rows on the device
+  // both kernels are launched with the same test there: the other one's
+  // workgroups return at once (a few microseconds).  RFT_GEMM_STORE_TILE=256
+  // or 384 in the environment fixes the choice (the results are the same bit
+  // for bit).
+  const int force = store_tile_env();
+  if (a_blk && b_blk && fits384(lda, ldb, K, k_from_cnt) && force != 256) {
+    int ncu = 0;
+    hipError_t e = cu_count(&ncu);
+    if (e != hipSuccess) return e;
+    if (force == 384) {
+      mf::k_gemm384<mf::EPI_STORE><<<grid_for384<mf::EPI_STORE>(M, N), mf::NT, 0, s>>>(a);
+      return hipGetLastError();
+    }
+    if (!m_from_cnt) {
+      if (mf::prefer384(M, N, ncu)) {
+        mf::k_gemm384<mf::EPI_STORE><<<grid_for384<mf::EPI_STORE>(M, N), mf::NT, 0, s>>>(a);
+        return hipGetLastError();
+      }
+    } else {
+      a.ncu = ncu;
+      a.sel = 1;
+      mf::k_gemm384<mf::EPI_STORE><<<grid_for384<mf::EPI_STORE>(M, N), mf::NT, 0, s>>>(a);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      a.sel = 2;
+    }
   }
   mf::k_gemm<mf::EPI_STORE><<<grid_for<mf::EPI_STORE>(M, N), mf::NT, 0, s>>>(a);
   return hipGetLastError();

@@ -114,3 +114,32 @@ def test_step_all_masked_and_empty():
     out = R.rft_ppo_clip_step(tok, H, W, e, e, adv, R.ppo_params(0.2, 0.2, 0.01, 0))
     torch.cuda.synchronize()
     assert torch.all(out[5] == 0) and R.stats_to_dict(out[6])["n_valid"] == 0
+
+
+def test_store_tile_choice_bit_identical(monkeypatch):
+    """d_hidden and d_weight on 256 x 256 or 384 x 256 tiles (RFT_GEMM_STORE_TILE
+    fixes the choice; unset, the round model picks one per call and, for
+    d_hidden whose rows are counted on the device, on the device): the same
+    numbers bit for bit, in the fused step (two row chunks) and in the
+    separate backward."""
+    over = dict(n_prompts=4, group=8, len_lo=100, len_hi=400, pad_to=400, d=128, V=3000,
+                dtype="bf16")
+    b = _batch(1, "storetile", over)
+    lp, _, _ = O.token_logprobs(b.H, b.W, b.ids, b.mask)
+    old, ref = perturbed_logprobs(lp, b)
+    tok = tokens_of(b)
+    N = int(b.mask.sum())
+    ws = R.workspace_bytes_rows(R.RFT_OP_PPO_STEP, tok, 128, 3000, R.RFT_BF16, (N // 2 + 255) // 256 * 256)
+    outs = {}
+    for tile in ("256", "384", None):
+        if tile is None:
+            monkeypatch.delenv("RFT_GEMM_STORE_TILE", raising=False)
+        else:
+            monkeypatch.setenv("RFT_GEMM_STORE_TILE", tile)
+        print(f"[store tile] {tile}", flush=True)
+        outs[tile] = (gpu_fused_step(b, old, ref, ws_bytes=ws), gpu_step(b, old, ref))
+    for tile in ("384", None):
+        for i in range(2):
+            for k in ("dH", "dW"):
+                assert np.array_equal(outs[tile][i][k], outs["256"][i][k]), (tile, i, k)
+    compare_step(outs["384"][0], oracle_step(b, old, ref), b)

@@ -188,22 +188,24 @@ def _ws_for_chunk(tok, d, V, rows):
 
 MIDSIZE_CASES = [
     # d = 72: the forward on 256 x 256 tiles (a K tail), chunks of 16384 rows
-    # (64 M-tiles: the full super-group of 8 x 8 tiles per XCD)
-    ("d72", dict(d=72, n_prompts=5, chunk=16384)),
+    # (64 M-tiles: the full super-group of 8 x 8 tiles per XCD); d_hidden and
+    # d_weight on 384 x 256 tiles (43 M-tiles of d_hidden: a full super-group
+    # of 4 x 8 and a remainder)
+    ("d72", dict(d=72, n_prompts=5, chunk=16384, store_tile="384")),
     # d = 128: the forward on 384 x 256 tiles, chunks of 24576 rows (64 M-tiles
     # of 384: its full super-group), 384-row tiles that start half way into a
-    # 256-row panel and chunk ends inside a tile
-    ("d128", dict(d=128, n_prompts=7, chunk=24576)),
+    # 256-row panel and chunk ends inside a tile; d_hidden and d_weight on
+    # 256 x 256 tiles (96 and 33 M-tiles)
+    ("d128", dict(d=128, n_prompts=7, chunk=24576, store_tile="256")),
 ]
 
 
 @pytest.mark.parametrize("name,case", MIDSIZE_CASES, ids=[c[0] for c in MIDSIZE_CASES])
-def test_midsize_fused_step_full_tile_order(name, case):
-    """Row chunks that fill the forward's full super-group of tiles, V = 8292
-    (33 M-tiles of the 256-row weight gradient kernel, 22 of the 384-row one:
-    full super-groups of 4 x 8 and a remainder); three chunks, the last
-    ragged; the backward GEMMs on 384 x 256 tiles.  Whole dH and dW against
-    the oracle."""
+def test_midsize_fused_step_full_tile_order(name, case, monkeypatch):
+    """Row chunks that fill the forward's full super-group of tiles, V = 8292;
+    three chunks, the last ragged; the backward GEMMs on the tile size the
+    case names (RFT_GEMM_STORE_TILE).  Whole dH and dW against the oracle."""
+    monkeypatch.setenv("RFT_GEMM_STORE_TILE", case["store_tile"])
     d, V, rows = case["d"], 8292, case["chunk"]
     over = dict(n_prompts=case["n_prompts"], group=8, len_lo=900, len_hi=1100, pad_to=1100, d=d,
                 V=V, dtype="bf16")
