@@ -371,9 +371,10 @@ rft_status rft_ppo_clip_fused_logits_noalloc(const rft_tokens* tok, const float*
                                              float* grad_logp, float* d_logits,
                                              rft_ppo_stats* stats, void* stream);
 
-/* The whole trainer-side step of the policy head in one call (Sec. 3: the
- * trainer's update with the PPO-clip surrogate, k3 KL to the reference model
- * and GRPO advantages, over the masked response tokens): the outputs of
+/* The whole trainer-side step of the policy head in one call (Sec. 3.3.2 and
+ * Listing 4: the trainer's update with the PPO-clip surrogate and k3 KL to the
+ * reference model; Sec. 3.1.1: log-probs of the masked response tokens;
+ * Sec. 3.2: GRPO advantages given per rollout): the outputs of
  * rft_token_logprobs (logp, entropy, lse), of rft_ppo_clip_loss_fwd
  * (grad_logp, *stats) and of rft_ppo_clip_loss_bwd (d_hidden, d_weight), for
  * the same inputs and with the same conventions (masked rows 0, bad ids,
@@ -386,7 +387,8 @@ rft_status rft_ppo_clip_fused_logits_noalloc(const rft_tokens* tok, const float*
  * (rows x vocabulary for d_hidden, transposed for d_weight), so the
  * workspace per chunk row is about 4 Vpad + 2 d bytes (the recommended size
  * holds chunks of up to 131072 rows: ~85 GB at V = 152064, d = 3584; a
- * smaller workspace gives smaller chunks); logp, entropy, lse, grad_logp
+ * smaller workspace gives smaller chunks, and rft_workspace_bytes_rows sizes
+ * one that holds a known count of valid rows in one chunk); logp, entropy, lse, grad_logp
  * and the stats equal those of the separate calls bit for bit, d_hidden and
  * d_weight agree to the rounding of dZ.  For fp32 inputs the call runs the
  * three separate calls in order.  logits are never stored beyond one chunk.
