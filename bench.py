@@ -39,10 +39,10 @@ WORKLOADS = {"tiny": 0, "1.5b": 1, "7b": 2, "longcot": 3, "lossonly": 4}
 TRAFFIC = {
     # forward GEMM alone (k_gemm384<EPI_STATS> on the tile-blocked copies, one launch over
     # all valid rows)
-    "7b": {"sources": {'k_gemm_mfma.hip': '0509b621c48177b9', 'rft_internal.h': '08981c3504904a8e'},
+    "7b": {"sources": {'k_gemm_mfma.hip': 'dc0da0d44c0974ed', 'rft_internal.h': '08981c3504904a8e'},
            "bytes": 151531338.1 * 1024 * 2.0 + 1174412.5 * 1024 * 1.0},
     # every kernel of one rft_ppo_clip_step call (28 dispatches, two row chunks)
-    "step_7b": {"sources": {'k_gemm_mfma.hip': '0509b621c48177b9', 'k_step.hip': '39fcacd3c55e6f75', 'k_simt.hip': '79fa372b0122fc73', 'k_adv_loss.hip': 'fe9e2b4d1d0b6332', 'k_tokens.hip': 'd52b04cf394f6696', 'rft_internal.h': '08981c3504904a8e', 'rft_abi.hip': '8db0c2f778a91fe2'},
+    "step_7b": {"sources": {'k_gemm_mfma.hip': 'dc0da0d44c0974ed', 'k_step.hip': '39fcacd3c55e6f75', 'k_simt.hip': '79fa372b0122fc73', 'k_adv_loss.hip': 'fe9e2b4d1d0b6332', 'k_tokens.hip': 'd52b04cf394f6696', 'rft_internal.h': '08981c3504904a8e', 'rft_abi.hip': '8db0c2f778a91fe2'},
                 "bytes": 579511823.2 * 1024 * 2.0 + 163468902.1 * 1024 * 1.0},
     "lossonly": {"sources": {'k_logits.hip': '784099cf37962bf5', 'rft_internal.h': '08981c3504904a8e'},
                  "bytes": 8758808.5 * 1024 * 2.0 + 19478868.4 * 1024 * 1.0},

@@ -36,6 +36,7 @@
 //              optionally added to the existing values.  On tile-blocked
 //              operands (dH, dW of the step) k_gemm384 does this on a
 //              384 x 256 tile (fewer operand bytes per flop).
+#include <atomic>
 #include <cstdlib>
 
 #include "rft_internal.h"
@@ -1034,20 +1035,24 @@ static int store_tile_env() {
   return t == 256 || t == 384 ? t : 0;
 }
 
-// Compute units of the current device (cached per device).
+// Compute units of the current device (cached per device; host threads may
+// call concurrently, so the cache entries are atomic).
 static hipError_t cu_count(int* n) {
-  static int cache[64] = {0};
+  static std::atomic<int> cache[64];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if (dev >= 0 && dev < 64 && cache[dev] > 0) {
-    *n = cache[dev];
-    return hipSuccess;
+  if (dev >= 0 && dev < 64) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) {
+      *n = c;
+      return hipSuccess;
+    }
   }
   e = hipDeviceGetAttribute(n, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
   if (*n < 1) *n = 1;
-  if (dev >= 0 && dev < 64) cache[dev] = *n;
+  if (dev >= 0 && dev < 64) cache[dev].store(*n, std::memory_order_relaxed);
   return hipSuccess;
 }
 
